@@ -1,0 +1,183 @@
+/*
+ * ssa.h - mixed chunked-prefill + decode attention over a paged KV cache, for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * One serving iteration executes a batch B = {(c_i, u_i)}: request i computes
+ * c_i new tokens on top of u_i tokens already in its KV cache (SlidingServe,
+ * Sec. 3.2).  Requests with c_i <= 1 form the decode set, the others the
+ * prefill (chunk) set (Sec. 3.2, Eq. 2); a batch is pure decode, pure prefill
+ * or mixed (Eq. 3).  A chunk's new token j, at absolute position u_i + j,
+ * attends causally to keys 0 .. u_i + j of its own request (chunked prefill,
+ * Sec. 1 and Sec. 2.1); a decode token is the case c_i = 1, j = 0.  Query head
+ * h reads kv head floor(h / G), G = Hq / Hkv.
+ *
+ * Call sequence for one iteration (all on one stream):
+ *   ssa_plan_size   -> sizes of the plan blob and the workspace      (host)
+ *   ssa_plan        -> fills the plan blob from (q_len, ctx_len)      (host)
+ *   caller copies the plan blob to device memory (same bytes)
+ *   ssa_kv_append   -> writes the new K/V rows into their pages      (1 kernel)
+ *   ssa_mixed_attention -> outputs of every new token                (1 kernel)
+ *
+ * Conventions shared by every call:
+ *   - Every function returns SSA_OK (0) or a negative SSA_ERR_* code.  All
+ *     arguments are validated before any HIP call; on an error nothing is
+ *     written and nothing is launched.  No C++ exception crosses this ABI and
+ *     nothing is printed.
+ *   - The library allocates no memory and keeps no state between calls.
+ *   - "bf16" arguments are bfloat16 bit patterns (uint16_t); they are device
+ *     pointers unless the name ends in _host.
+ *   - stream is a hipStream_t passed as void* (NULL = the null stream).
+ *
+ * Memory layouts (row-major, dense, no padding):
+ *   q, out         [T, Hq, D]       T = sum of q_len; rows grouped by request,
+ *                                    requests in the order given to ssa_plan
+ *   k_new, v_new   [T, Hkv, D]
+ *   k_cache        [num_pages, Hkv, P, D]   key page: P slots of D values
+ *   v_cache        [num_pages, Hkv, D, P]   value page: D rows of P slots
+ *   block_table    int32 [num_reqs, max_pages_per_req]; token position t of
+ *                  request i lives in page block_table[i][t / P], slot t % P.
+ *                  Only the first ceil((u_i + c_i) / P) entries of a row are
+ *                  read; their values must lie in [0, num_pages) (the caller's
+ *                  responsibility: the library cannot check device memory).
+ *   P (page_size) is 16; D (head_dim) is 64 or 128; 1 <= Hq / Hkv <= 16.
+ */
+#ifndef SSA_H
+#define SSA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SSA_PAGE_SIZE 16
+
+enum {
+  SSA_OK = 0,
+  SSA_ERR_NULL = -1,          /* a required pointer is NULL */
+  SSA_ERR_SHAPE = -2,         /* Hq, Hkv not positive, Hq % Hkv != 0, or Hq/Hkv > 16 */
+  SSA_ERR_HEAD_DIM = -3,      /* head_dim not 64 or 128 */
+  SSA_ERR_PAGE_SIZE = -4,     /* page_size not 16 */
+  SSA_ERR_LENGTH = -5,        /* negative q_len / ctx_len, or a length sum beyond 2^30 */
+  SSA_ERR_PAGES = -6,         /* ceil((u+c)/P) > max_pages_per_req, or num_pages < 1 */
+  SSA_ERR_PLAN_SIZE = -7,     /* the plan buffer is smaller than ssa_plan_size says */
+  SSA_ERR_WORKSPACE = -8,     /* workspace NULL or smaller than the plan requires */
+  SSA_ERR_PLAN_MISMATCH = -9, /* plan_host is not a plan of this shape (magic/hash) */
+  SSA_ERR_HIP = -10,          /* a HIP launch failed */
+  SSA_ERR_SCALE = -11,        /* softmax_scale not finite */
+  SSA_ERR_TUNING = -12        /* a tuning field out of range */
+};
+
+/* Scene of a batch (Sec. 3.2, Eq. 3).  A batch with no new token is EMPTY. */
+enum { SSA_SCENE_EMPTY = 0, SSA_SCENE_PURE_DECODE = 1, SSA_SCENE_PURE_PREFILL = 2,
+       SSA_SCENE_MIXED = 3 };
+
+typedef struct ssa_shape {
+  int32_t num_q_heads;       /* Hq */
+  int32_t num_kv_heads;      /* Hkv */
+  int32_t head_dim;          /* D: 64 or 128 */
+  int32_t page_size;         /* P: 16 */
+  int32_t num_pages;         /* pages in each pool */
+  int32_t max_pages_per_req; /* row stride of block_table */
+  float softmax_scale;       /* multiplies <q, k> before the softmax (1/sqrt(D) usually) */
+} ssa_shape;
+
+/*
+ * Optional planner knobs (pass NULL to ssa_plan_size / ssa_plan for the
+ * defaults).  Zero in a field selects its default.  Results do not depend on
+ * them beyond floating-point summation order.
+ *   chunk_tile_cols  columns (token x q-head-in-group pairs) per chunk work
+ *                    item: 64, 128 or 256 (default 256)
+ *   chunk_split_keys if > 0, a chunk tile's key range is cut into pieces of this
+ *                    many keys (multiple of 32); default: chosen by the planner
+ *   decode_split_keys keys per decode work item (multiple of 32); default:
+ *                    chosen by the planner
+ *   num_cus          compute units the planner balances for (default 256)
+ */
+typedef struct ssa_tuning {
+  int32_t chunk_tile_cols;
+  int32_t chunk_split_keys;
+  int32_t decode_split_keys;
+  int32_t num_cus;
+} ssa_tuning;
+
+/*
+ * What ssa_plan derived from the batch.  Byte and flop counts are the
+ * algorithmic work (what the method must move or compute), not the work the
+ * kernels actually do.
+ *   decode_bytes  K/V bytes of the decode rows, sum over D of (u+1)*Hkv*D*2*2,
+ *                 plus their q and out rows (2*Hq*D*2 per row)
+ *   chunk_bytes   K/V bytes of the chunk requests, (u+c)*Hkv*D*2*2 each, plus
+ *                 their q and out rows
+ *   chunk_flops   4*Hq*D*(c*u + c*(c+1)/2) summed over the prefill set
+ *   decode_flops  4*Hq*D*(u+1) summed over the decode set
+ *   append_bytes  bytes kv_append reads plus writes: T*Hkv*D*2*2*2
+ *   x[0..6]       the paper's batch features x1..x7 (Tab. 1)
+ */
+typedef struct ssa_plan_info {
+  int32_t num_reqs, num_tokens, num_decode_reqs, num_chunk_reqs;
+  int32_t num_items, num_chunk_items, num_decode_items, num_merge_groups;
+  int32_t num_append_segments, scene;
+  double decode_bytes, chunk_bytes, chunk_flops, decode_flops, append_bytes;
+  double x[7];
+} ssa_plan_info;
+
+/* Static description of an error code ("ok" for SSA_OK, "unknown" otherwise). */
+const char* ssa_status_string(int code);
+
+/*
+ * Sizes of the plan blob and of the workspace for this batch.
+ *   q_len_host[i] = c_i, ctx_len_host[i] = u_i (host arrays of num_reqs).
+ *   num_reqs may be 0.  tuning may be NULL.
+ * Errors: NULL, SHAPE, HEAD_DIM, PAGE_SIZE, SCALE, LENGTH, PAGES, TUNING.
+ */
+int ssa_plan_size(const ssa_shape* shape, const int32_t* q_len_host, const int32_t* ctx_len_host,
+                  int32_t num_reqs, const ssa_tuning* tuning, size_t* plan_bytes,
+                  size_t* workspace_bytes);
+
+/*
+ * Build the plan (pure host code, no HIP call): request starts, the decode /
+ * chunk routing of Eq. 2, the work items of the attention launch, the merge
+ * groups of split work items, the append segments, and info (may be NULL).
+ * plan_host must hold plan_bytes >= ssa_plan_size's value; the blob is
+ * position-independent and is used as is on the device after a byte copy.
+ * Errors: those of ssa_plan_size, and PLAN_SIZE.
+ */
+int ssa_plan(const ssa_shape* shape, const int32_t* q_len_host, const int32_t* ctx_len_host,
+             int32_t num_reqs, const ssa_tuning* tuning, void* plan_host, size_t plan_bytes,
+             ssa_plan_info* info);
+
+/*
+ * KV append (one kernel): new token j of request i, at position t = u_i + j,
+ * is copied bit for bit from k_new/v_new row (q_start_i + j) into page
+ * block_table[i][t / P], slot t % P, of k_cache / v_cache.  No other pool
+ * byte is written.  plan_host is the plan blob on the host (read for the
+ * launch size and checked against shape), plan_dev its device copy.
+ * Errors: NULL, the shape errors, PLAN_MISMATCH, HIP.
+ */
+int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                  const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache,
+                  uint16_t* v_cache, const int32_t* block_table, void* stream);
+
+/*
+ * Mixed attention (exactly one kernel launch): out[q_start_i + j, h, :] =
+ * softmax_t(scale * <q, k_t>) weighted sum of v_t over keys t = 0 .. u_i + j of
+ * request i (kv head floor(h / G)), for every new token and q head, in bf16
+ * (fp32 accumulation).  Reads the chunk's own keys from the pools, so
+ * ssa_kv_append of the same plan must have run before it on the stream.
+ * workspace: device memory of at least the plan's workspace size, zero-filled
+ * by the caller once before its first use; each call leaves its counters at
+ * zero again.  Calls that share a workspace must not overlap in time.
+ * Errors: NULL, the shape errors, PLAN_MISMATCH, WORKSPACE, HIP.
+ */
+int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                        const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                        const int32_t* block_table, uint16_t* out, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSA_H */

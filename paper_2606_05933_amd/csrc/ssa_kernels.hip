@@ -1,0 +1,697 @@
+// HIP kernels for gfx950 (CDNA4) and the two launching entry points of the
+// C ABI: ssa_kv_append and ssa_mixed_attention.
+//
+// Attention work is one launch of a flat grid; workgroup b runs work item b of
+// the plan (longest first).  Two kinds of item share the launch:
+//
+//  * chunk tile (prefill rows, c_i > 1; Sec. 2.1 chunked prefill, Tab. 1 x1/x2):
+//    256 columns = (token, q head of the kv group) pairs of one request and kv
+//    head; each of the 4 waves owns 64 columns as four 16-wide MFMA N tiles.
+//    Key blocks of 32 keys (two 16-slot pages) are staged through LDS, double
+//    buffered, and shared by the 4 waves.  S^T = K Q^T and O^T += V^T P run on
+//    v_mfma_f32_16x16x32_bf16 with fp32 accumulation; softmax is online, in
+//    base 2, fp32.  Causal masking is applied only on blocks that cross the
+//    diagonal.
+//
+//  * decode split (c_i == 1; Tab. 1 x4/x5): the G q heads of one kv head are the
+//    N columns of the same MFMA formulation, so each K/V byte read from HBM is
+//    used by the whole GQA group.  The 4 waves of the workgroup take
+//    interleaved 32-key blocks of the split's key range straight from global
+//    memory (16-byte coalesced loads, next block prefetched into registers),
+//    and merge their (m, l, O) partials through LDS at the end.
+//
+// Items that cover part of a key range write an fp32 partial record; the last
+// item of the group to finish (atomic ticket) merges the records in split
+// order and writes bf16 output, then zeroes the ticket for the next launch.
+//
+// MFMA operand mapping (16x16x32 bf16, wave64, lane l, g = l / 16, r = l % 16):
+// A row r and B column r live in lane r of each 16-lane group; lane group g
+// holds 8 consecutive K-dim elements.  The output holds rows 4g..4g+3 of
+// column r.  Keys are permuted inside a 32-key block so that after the two
+// QK^T MFMAs (key halves h = 0, 1) lane group g holds keys 8g..8g+7: A row r of
+// half h is key 8*(r/4) + 4h + r%4.  Those 8 probabilities are exactly the B
+// operand of the PV MFMA, whose A operand (V^T) is then 8 consecutive slots of
+// one value-page row: a single 16-byte load.  That is why value pages are
+// stored dim-major ([D][16 slots]).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/ssa.h"
+#include "ssa_plan_format.h"
+
+namespace ssa {
+int check_plan(const ssa_shape* s, const void* plan_host, const PlanHeader** out);
+}
+
+namespace {
+using namespace ssa;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegInf = -__builtin_inff();
+
+template <int D>
+struct Cfg {
+  static constexpr int KK = D / 32;          // MFMA k-steps over the head dim
+  static constexpr int MT = D / 16;          // 16-row output tiles over the head dim
+  static constexpr int CPR = D / 8;          // 16-byte chunks per key row
+  static constexpr int K_ROW = D * 2;        // LDS bytes per key row (chunks XOR-swizzled)
+  static constexpr int K_STAGE = 32 * K_ROW; // one 32-key block of K
+  static constexpr int V_ROW = 80;           // LDS bytes per value row: 32 slots + 16 pad
+  static constexpr int V_STAGE = D * V_ROW;
+  static constexpr int STAGE = K_STAGE + V_STAGE;
+  static constexpr int LDS_CHUNK = 2 * STAGE;
+  static constexpr int LDS_DECODE = kWaves * (32 + 16 * D) * 4;
+  static constexpr int LDS = LDS_CHUNK > LDS_DECODE ? LDS_CHUNK : LDS_DECODE;
+  static constexpr int LOADS = D / 64;       // 16-byte K (and V) chunks per thread per block
+};
+
+struct AttnArgs {
+  const uint8_t* plan;
+  uint64_t hash;
+  const uint16_t* q;
+  const uint16_t* kc;
+  const uint16_t* vc;
+  const int32_t* bt;
+  uint16_t* out;
+  uint8_t* ws;
+  float scale_log2;
+  int hq, hkv, G, maxp;
+};
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+__device__ __forceinline__ bf16x8 pack8(const float (&p)[8]) {
+  u32x4 r = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
+  return as_bf16x8(r);
+}
+
+// Keep the first `keep` (0..8) bf16 elements of a 16-byte chunk, zero the rest.
+__device__ __forceinline__ u32x4 keep_first(u32x4 v, int keep) {
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = 2 * i;
+    uint32_t m = (e < keep ? 0x0000FFFFu : 0u) | (e + 1 < keep ? 0xFFFF0000u : 0u);
+    r[i] = v[i] & m;
+  }
+  return r;
+}
+
+// XOR swizzle of the 16-byte chunk index of key row `key` in the LDS K block, so
+// that the 8 rows a ds_read_b128 lane octet touches (keys 8*(r/4)+4h+r%4) fall
+// in distinct bank groups.
+__device__ __forceinline__ int kswz(int key) { return (key & 3) | ((key & 8) >> 1); }
+
+__device__ __forceinline__ float wave_max_cols(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  x = fmaxf(x, __shfl_xor(x, 32));
+  return x;
+}
+__device__ __forceinline__ float wave_sum_cols(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+// Online-softmax step for one 16-column tile and one 32-key block.  sv holds the
+// lane's 8 logits (base-2 scaled, masked ones -inf); on return it holds the
+// unnormalised probabilities relative to the running maximum.
+template <int MT>
+__device__ __forceinline__ void softmax_step(float (&sv)[8], float& m_run, float& l_run,
+                                             f32x4 (&o)[MT]) {
+  float mx = sv[0];
+#pragma unroll
+  for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
+  mx = wave_max_cols(mx);
+  const float m_new = fmaxf(m_run, mx);
+  const float m_use = (m_new == kNegInf) ? 0.f : m_new;
+  const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+  m_run = m_new;
+  float sum = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    sv[e] = __builtin_amdgcn_exp2f(sv[e] - m_use);
+    sum += sv[e];
+  }
+  l_run = l_run * alpha + sum;
+  if (alpha != 1.f) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) o[mt] *= alpha;
+  }
+}
+
+__device__ __forceinline__ void store_bf16x4(uint16_t* dst, float a, float b, float c, float d) {
+  u32x2 v = {pack2(a, b), pack2(c, d)};
+  *reinterpret_cast<u32x2*>(dst) = v;
+}
+
+// Output row and q head of column `col` (local to the item) of an item.
+__device__ __forceinline__ void col_target(const WorkItem& it, const ReqEntry& rq, int G, int col,
+                                           int& row, int& head) {
+  if (it.kind == kItemDecode) {
+    row = rq.q_start;
+    head = it.kvh * G + col;
+  } else {
+    const int cc = it.col0 + col;
+    const int j = cc / G;
+    row = rq.q_start + j;
+    head = it.kvh * G + (cc - j * G);
+  }
+}
+
+// Last arriver of a merge group: combine the split records in split order.
+template <int D>
+__device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
+                            const MergeGroup& grp) {
+  const float* base = reinterpret_cast<const float*>(
+      a.ws + reinterpret_cast<const PlanHeader*>(a.plan)->ws_partials_off) + grp.ws_off;
+  const int C = grp.ncols;
+  const int64_t rec = (int64_t)C * (D + 2);
+  for (int idx = threadIdx.x; idx < C * (D / 4); idx += kThreads) {
+    const int col = idx / (D / 4);
+    const int d0 = (idx % (D / 4)) * 4;
+    float M = kNegInf;
+    for (int s = 0; s < grp.nsplit; ++s) M = fmaxf(M, base[s * rec + col]);
+    float L = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < grp.nsplit; ++s) {
+      const float* r = base + s * rec;
+      const float w = __builtin_amdgcn_exp2f(r[col] - M);
+      L += w * r[C + col];
+      const f32x4 o = *reinterpret_cast<const f32x4*>(r + 2 * C + (int64_t)col * D + d0);
+      acc += w * o;
+    }
+    const float inv = 1.f / L;
+    int row, head;
+    col_target(it, rq, a.G, col, row, head);
+    store_bf16x4(a.out + ((size_t)row * a.hq + head) * D + d0, acc[0] * inv, acc[1] * inv,
+                 acc[2] * inv, acc[3] * inv);
+  }
+}
+
+// After this workgroup wrote its partial record: take a ticket; the last one
+// merges.  Release/acquire at agent scope orders the records across XCDs.
+template <int D>
+__device__ void finish_split(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq) {
+  __shared__ int s_last;
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
+  const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + hdr->off_groups)[it.group];
+  int* tickets = reinterpret_cast<int*>(a.ws);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int prev = __hip_atomic_fetch_add(&tickets[it.group], 1, __ATOMIC_ACQ_REL,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (prev == grp.nsplit - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  merge_group<D>(a, it, rq, grp);
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&tickets[it.group], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------- chunk tiles
+
+template <int D>
+__device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
+                           char* lds) {
+  using C = Cfg<D>;
+  constexpr int KK = C::KK, MT = C::MT, NT = 4;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int G = a.G;
+  const int u = rq.ctx_len;
+  const int nvalid = rq.ctx_len + rq.q_len;
+  const int32_t* bt = a.bt + (size_t)it.req * a.maxp;
+  const size_t page_stride = (size_t)a.hkv * 16 * D;
+  const size_t head_off = (size_t)it.kvh * 16 * D;
+
+  // this wave's columns: [wc0, wc1)
+  const int colend = it.col0 + it.ncols;
+  const int wc0 = it.col0 + w * kChunkWaveCols;
+  const int wc1 = min(wc0 + kChunkWaveCols, colend);
+  const bool wave_has = wc0 < colend;
+  const int wpmin = wave_has ? u + wc0 / G : 0;                     // smallest position
+  const int wkend = wave_has ? min(it.key1, u + (wc1 - 1) / G + 1) : it.key0;
+
+  bf16x8 qop[NT][KK];
+  int pos[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int col = wc0 + nt * 16 + r16;
+    if (col < colend) {
+      const int j = col / G;
+      const int hg = col - j * G;
+      pos[nt] = u + j;
+      const uint16_t* qrow = a.q + ((size_t)(rq.q_start + j) * a.hq + it.kvh * G + hg) * D;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) qop[nt][kk] = as_bf16x8(ld16(qrow + kk * 32 + g * 8));
+    } else {
+      pos[nt] = -1;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) qop[nt][kk] = as_bf16x8(u32x4{0, 0, 0, 0});
+    }
+  }
+
+  float m_run[NT], l_run[NT];
+  f32x4 o[NT][MT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    m_run[nt] = kNegInf;
+    l_run[nt] = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) o[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // cooperative global -> register -> LDS staging of one 32-key block
+  u32x4 kreg[C::LOADS], vreg[C::LOADS];
+  auto gload = [&](int kb) {
+#pragma unroll
+    for (int r = 0; r < C::LOADS; ++r) {
+      const int ci = tid + r * kThreads;
+      const int page = ci / (2 * D);
+      const int within = ci % (2 * D);
+      const int lp = kb / 16 + page;
+      if (lp < rq.n_pages) {
+        const size_t pb = (size_t)bt[lp] * page_stride + head_off;
+        const int slot = within / C::CPR, c = within % C::CPR;
+        kreg[r] = ld16(a.kc + pb + slot * D + c * 8);
+        const int d = within >> 1, half = within & 1;
+        u32x4 v = ld16(a.vc + pb + d * 16 + half * 8);
+        const int kfirst = kb + page * 16 + half * 8;
+        if (kfirst + 8 > nvalid) v = keep_first(v, nvalid - kfirst);
+        vreg[r] = v;
+      } else {
+        kreg[r] = u32x4{0, 0, 0, 0};
+        vreg[r] = u32x4{0, 0, 0, 0};
+      }
+    }
+  };
+  auto lstore = [&](char* stage) {
+#pragma unroll
+    for (int r = 0; r < C::LOADS; ++r) {
+      const int ci = tid + r * kThreads;
+      const int page = ci / (2 * D);
+      const int within = ci % (2 * D);
+      const int key = page * 16 + within / C::CPR, c = within % C::CPR;
+      st16(stage + key * C::K_ROW + ((c ^ kswz(key)) << 4), kreg[r]);
+      const int d = within >> 1, half = within & 1;
+      st16(stage + C::K_STAGE + d * C::V_ROW + (page * 2 + half) * 16, vreg[r]);
+    }
+  };
+  auto compute = [&](const char* stage, int kb) {
+    if (kb >= wkend) return;
+    bf16x8 kop[2][KK];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int key = 8 * (r16 >> 2) + 4 * h + (r16 & 3);
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const int c = kk * 4 + g;
+        kop[h][kk] = as_bf16x8(ld16(stage + key * C::K_ROW + ((c ^ kswz(key)) << 4)));
+      }
+    }
+    const bool need_mask = kb + 31 > wpmin;
+    bf16x8 pop[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        s0 = mfma(kop[0][kk], qop[nt][kk], s0);
+        s1 = mfma(kop[1][kk], qop[nt][kk], s1);
+      }
+      float sv[8];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        sv[jj] = s0[jj] * a.scale_log2;
+        sv[4 + jj] = s1[jj] * a.scale_log2;
+      }
+      if (need_mask) {
+        const int kg = kb + 8 * g;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (kg + e > pos[nt]) sv[e] = kNegInf;
+      }
+      softmax_step<MT>(sv, m_run[nt], l_run[nt], o[nt]);
+      pop[nt] = pack8(sv);
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const bf16x8 vop =
+          as_bf16x8(ld16(stage + C::K_STAGE + (mt * 16 + r16) * C::V_ROW + g * 16));
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) o[nt][mt] = mfma(vop, pop[nt], o[nt][mt]);
+    }
+  };
+
+  const int nb = (it.key1 - it.key0 + 31) / 32;
+  if (nb > 0) {
+    gload(it.key0);
+    lstore(lds);
+  }
+  __syncthreads();
+  for (int b = 0; b < nb; ++b) {
+    const int kb = it.key0 + b * 32;
+    char* cur = lds + (b & 1) * C::STAGE;
+    if (b + 1 < nb) gload(kb + 32);
+    compute(cur, kb);
+    if (b + 1 < nb) lstore(lds + ((b + 1) & 1) * C::STAGE);
+    __syncthreads();
+  }
+
+  // epilogue
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) l_run[nt] = wave_sum_cols(l_run[nt]);
+  if (it.group < 0) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int col = wc0 + nt * 16 + r16;
+      if (col >= colend) continue;
+      const int j = col / G;
+      const int hg = col - j * G;
+      uint16_t* orow = a.out + ((size_t)(rq.q_start + j) * a.hq + it.kvh * G + hg) * D;
+      const float inv = 1.f / l_run[nt];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        store_bf16x4(orow + mt * 16 + 4 * g, o[nt][mt][0] * inv, o[nt][mt][1] * inv,
+                     o[nt][mt][2] * inv, o[nt][mt][3] * inv);
+    }
+  } else {
+    const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
+    const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + hdr->off_groups)[it.group];
+    const int Cn = grp.ncols;
+    float* rec = reinterpret_cast<float*>(a.ws + hdr->ws_partials_off) + grp.ws_off +
+                 (int64_t)it.split * Cn * (D + 2);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int col = wc0 + nt * 16 + r16;
+      if (col >= colend) continue;
+      const int cl = col - it.col0;
+      if (g == 0) {
+        rec[cl] = m_run[nt];
+        rec[Cn + cl] = l_run[nt];
+      }
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        *reinterpret_cast<f32x4*>(rec + 2 * Cn + (int64_t)cl * D + mt * 16 + 4 * g) = o[nt][mt];
+    }
+    finish_split<D>(a, it, rq);
+  }
+}
+
+// --------------------------------------------------------------- decode splits
+
+template <int D>
+struct DecodeRegs {
+  bf16x8 k[2][Cfg<D>::KK];
+  bf16x8 v[Cfg<D>::MT];
+};
+
+template <int D>
+__device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
+                            char* lds) {
+  using C = Cfg<D>;
+  constexpr int KK = C::KK, MT = C::MT;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = lane >> 4, r16 = lane & 15;
+  const int G = a.G;
+  const int32_t* bt = a.bt + (size_t)it.req * a.maxp;
+  const size_t page_stride = (size_t)a.hkv * 16 * D;
+  const size_t head_off = (size_t)it.kvh * 16 * D;
+  const int key1 = it.key1;
+
+  bf16x8 qop[KK];
+  if (r16 < G) {
+    const uint16_t* qrow = a.q + ((size_t)rq.q_start * a.hq + it.kvh * G + r16) * D;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qop[kk] = as_bf16x8(ld16(qrow + kk * 32 + g * 8));
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qop[kk] = as_bf16x8(u32x4{0, 0, 0, 0});
+  }
+  float m_run = kNegInf, l_run = 0.f;
+  f32x4 o[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) o[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto load = [&](DecodeRegs<D>& R, int kb) {
+    const bool tail = kb + 32 > key1;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int key = 8 * (r16 >> 2) + 4 * h + (r16 & 3);
+      const int lp = kb / 16 + (key >> 4);
+      if (!tail || lp < rq.n_pages) {
+        const uint16_t* src = a.kc + (size_t)bt[lp] * page_stride + head_off + (key & 15) * D + g * 8;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) R.k[h][kk] = as_bf16x8(ld16(src + kk * 32));
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) R.k[h][kk] = as_bf16x8(u32x4{0, 0, 0, 0});
+      }
+    }
+    const int lp = kb / 16 + (g >> 1);
+    if (!tail || lp < rq.n_pages) {
+      const uint16_t* src = a.vc + (size_t)bt[lp] * page_stride + head_off + r16 * 16 + (g & 1) * 8;
+      const int keep = key1 - (kb + 8 * g);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        u32x4 v = ld16(src + mt * 16 * 16);
+        if (tail && keep < 8) v = keep_first(v, keep < 0 ? 0 : keep);
+        R.v[mt] = as_bf16x8(v);
+      }
+    } else {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) R.v[mt] = as_bf16x8(u32x4{0, 0, 0, 0});
+    }
+  };
+  auto compute = [&](const DecodeRegs<D>& R, int kb) {
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      s0 = mfma(R.k[0][kk], qop[kk], s0);
+      s1 = mfma(R.k[1][kk], qop[kk], s1);
+    }
+    float sv[8];
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      sv[jj] = s0[jj] * a.scale_log2;
+      sv[4 + jj] = s1[jj] * a.scale_log2;
+    }
+    if (kb + 32 > key1) {
+      const int kg = kb + 8 * g;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (kg + e >= key1) sv[e] = kNegInf;
+    }
+    softmax_step<MT>(sv, m_run, l_run, o);
+    const bf16x8 pop = pack8(sv);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) o[mt] = mfma(R.v[mt], pop, o[mt]);
+  };
+
+  const int nb = (key1 - it.key0 + 31) / 32;
+  DecodeRegs<D> R0, R1;
+  int b = w;
+  if (b < nb) load(R0, it.key0 + b * 32);
+  while (b < nb) {
+    int bn = b + kWaves;
+    if (bn < nb) load(R1, it.key0 + bn * 32);
+    compute(R0, it.key0 + b * 32);
+    b = bn;
+    if (b >= nb) break;
+    bn = b + kWaves;
+    if (bn < nb) load(R0, it.key0 + bn * 32);
+    compute(R1, it.key0 + b * 32);
+    b = bn;
+  }
+  l_run = wave_sum_cols(l_run);
+
+  // merge the 4 waves through LDS: per wave m[16], l[16], o[D][16]
+  float* sm = reinterpret_cast<float*>(lds);
+  float* wm = sm + w * (32 + 16 * D);
+  if (g == 0) {
+    wm[r16] = m_run;
+    wm[16 + r16] = l_run;
+  }
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) wm[32 + (mt * 16 + 4 * g + jj) * 16 + r16] = o[mt][jj];
+  __syncthreads();
+
+  float* rec = nullptr;
+  if (it.group >= 0) {
+    const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
+    const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + hdr->off_groups)[it.group];
+    rec = reinterpret_cast<float*>(a.ws + hdr->ws_partials_off) + grp.ws_off +
+          (int64_t)it.split * G * (D + 2);
+  }
+  for (int idx = tid; idx < G * (D / 4); idx += kThreads) {
+    const int col = idx % G;
+    const int d0 = (idx / G) * 4;
+    float M = kNegInf;
+#pragma unroll
+    for (int ww = 0; ww < kWaves; ++ww) M = fmaxf(M, sm[ww * (32 + 16 * D) + col]);
+    float L = 0.f;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ww = 0; ww < kWaves; ++ww) {
+      const float* pw = sm + ww * (32 + 16 * D);
+      const float wt = (pw[col] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(pw[col] - M);
+      L += wt * pw[16 + col];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc[k] += wt * pw[32 + (d0 + k) * 16 + col];
+    }
+    if (rec) {
+      if (d0 == 0) {
+        rec[col] = M;
+        rec[G + col] = L;
+      }
+      *reinterpret_cast<f32x4*>(rec + 2 * G + (int64_t)col * D + d0) =
+          f32x4{acc[0], acc[1], acc[2], acc[3]};
+    } else {
+      const float inv = 1.f / L;
+      store_bf16x4(a.out + ((size_t)rq.q_start * a.hq + it.kvh * G + col) * D + d0,
+                   acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+    }
+  }
+  if (rec) finish_split<D>(a, it, rq);
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 1) void mixed_attention_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) char lds[Cfg<D>::LDS];
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
+  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
+  const WorkItem it = reinterpret_cast<const WorkItem*>(a.plan + hdr->off_items)[blockIdx.x];
+  const ReqEntry rq = reinterpret_cast<const ReqEntry*>(a.plan + hdr->off_reqs)[it.req];
+  if (it.kind == kItemChunk)
+    chunk_item<D>(a, it, rq, lds);
+  else
+    decode_item<D>(a, it, rq, lds);
+}
+
+// ------------------------------------------------------------------ kv_append
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint8_t* plan, uint64_t hash,
+                                                             const uint16_t* k_new,
+                                                             const uint16_t* v_new, uint16_t* kc,
+                                                             uint16_t* vc, const int32_t* bt,
+                                                             int hkv, int maxp) {
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(plan);
+  if (hdr->magic != kPlanMagic || hdr->hash != hash) return;
+  const AppendSeg sg = reinterpret_cast<const AppendSeg*>(plan + hdr->off_segments)[blockIdx.x];
+  const int h = blockIdx.y;
+  const int slot0 = sg.pos0 % 16;
+  const size_t pb = (size_t)bt[(size_t)sg.req * maxp + sg.pos0 / 16] * hkv * 16 * D + (size_t)h * 16 * D;
+  constexpr int CPR = D / 8;
+  for (int idx = threadIdx.x; idx < sg.n * CPR; idx += kThreads) {
+    const int r = idx / CPR, c = idx % CPR;
+    st16(kc + pb + (size_t)(slot0 + r) * D + c * 8,
+         ld16(k_new + ((size_t)(sg.row0 + r) * hkv + h) * D + c * 8));
+  }
+  for (int idx = threadIdx.x; idx < 2 * D; idx += kThreads) {
+    const int d = idx >> 1, half = idx & 1;
+    const int lo = max(half * 8, slot0), hi = min(half * 8 + 8, slot0 + sg.n);
+    if (lo >= hi) continue;
+    uint16_t* dst = vc + pb + (size_t)d * 16;
+    // value of slot s: token row row0 + (s - slot0), kv head h, dim d
+    auto src = [&](int s) { return v_new[((size_t)(sg.row0 + s - slot0) * hkv + h) * D + d]; };
+    if (lo == half * 8 && hi == half * 8 + 8) {
+      uint32_t wv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        wv[i] = (uint32_t)src(lo + 2 * i) | ((uint32_t)src(lo + 2 * i + 1) << 16);
+      st16(dst + lo, u32x4{wv[0], wv[1], wv[2], wv[3]});
+    } else {
+      for (int s = lo; s < hi; ++s) dst[s] = src(s);
+    }
+  }
+}
+
+hipError_t clear_and_check() { return hipGetLastError(); }
+
+}  // namespace
+
+extern "C" {
+
+int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                  const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache,
+                  uint16_t* v_cache, const int32_t* block_table, void* stream) {
+  const PlanHeader* h = nullptr;
+  int rc = check_plan(shape, plan_host, &h);
+  if (rc) return rc;
+  if (!plan_dev) return SSA_ERR_NULL;
+  if (h->num_segments == 0) return SSA_OK;
+  if (!k_new || !v_new || !k_cache || !v_cache || !block_table) return SSA_ERR_NULL;
+  (void)clear_and_check();
+  dim3 grid(h->num_segments, h->hkv);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const uint8_t* p = static_cast<const uint8_t*>(plan_dev);
+  if (h->head_dim == 128)
+    kv_append_kernel<128><<<grid, kThreads, 0, st>>>(p, h->hash, k_new, v_new, k_cache, v_cache,
+                                                     block_table, h->hkv, h->max_pages_per_req);
+  else
+    kv_append_kernel<64><<<grid, kThreads, 0, st>>>(p, h->hash, k_new, v_new, k_cache, v_cache,
+                                                    block_table, h->hkv, h->max_pages_per_req);
+  return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+}
+
+int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                        const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                        const int32_t* block_table, uint16_t* out, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  const PlanHeader* h = nullptr;
+  int rc = check_plan(shape, plan_host, &h);
+  if (rc) return rc;
+  if (!plan_dev) return SSA_ERR_NULL;
+  if (h->num_items == 0) return SSA_OK;
+  if (!q || !k_cache || !v_cache || !block_table || !out) return SSA_ERR_NULL;
+  if (h->ws_bytes > 0 && (!workspace || workspace_bytes < (size_t)h->ws_bytes))
+    return SSA_ERR_WORKSPACE;
+  AttnArgs a;
+  a.plan = static_cast<const uint8_t*>(plan_dev);
+  a.hash = h->hash;
+  a.q = q;
+  a.kc = k_cache;
+  a.vc = v_cache;
+  a.bt = block_table;
+  a.out = out;
+  a.ws = static_cast<uint8_t*>(workspace);
+  a.scale_log2 = h->softmax_scale * kLog2e;
+  a.hq = h->hq;
+  a.hkv = h->hkv;
+  a.G = h->hq / h->hkv;
+  a.maxp = h->max_pages_per_req;
+  (void)clear_and_check();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (h->head_dim == 128)
+    mixed_attention_kernel<128><<<h->num_items, kThreads, 0, st>>>(a);
+  else
+    mixed_attention_kernel<64><<<h->num_items, kThreads, 0, st>>>(a);
+  return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,395 @@
+// Host side of the library: argument validation, the iteration plan, status
+// strings.  Pure host code (no HIP call), so it is testable without a GPU.
+//
+// The plan turns the batch B = {(c_i, u_i)} (SlidingServe Sec. 3.2) into the
+// work of one attention launch:
+//   - request starts: q_start_i = c_0 + ... + c_{i-1};
+//   - routing by Eq. 2: c_i == 1 -> decode split items, c_i > 1 -> chunk tile
+//     items, c_i == 0 -> nothing (it belongs to the decode set but has no row);
+//   - merge groups for items that cover only part of a key range;
+//   - append segments for kv_append (new tokens cut at page boundaries);
+//   - the scene of Eq. 3 and the batch features x1..x7 of Tab. 1.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/ssa.h"
+#include "ssa_plan_format.h"
+
+namespace ssa {
+namespace {
+
+constexpr int kDefaultTileCols = 256;
+constexpr int kDefaultCus = 256;
+constexpr int kMaxLen = 1 << 30;
+// Nominal rates for balancing only (fractions of MI355X peaks): bf16 MFMA per
+// CU at half of peak, HBM at 70% of 8 TB/s shared by all CUs.
+constexpr double kMfmaRatePerCu = 2.5e15 / 256.0 * 0.5;
+constexpr double kHbmRate = 8.0e12 * 0.7;
+// A chunk tile's key range is cut only into pieces of at least this many keys:
+// each piece costs a partial record of ncols*(D+2) floats written and read back.
+constexpr int kMinChunkSplitKeys = 1024;
+constexpr int kMaxChunkSplits = 16;
+
+struct Tuning {
+  int tile_cols, chunk_split_keys, decode_split_keys, num_cus;
+};
+
+int check_shape(const ssa_shape* s) {
+  if (!s) return SSA_ERR_NULL;
+  if (s->num_q_heads <= 0 || s->num_kv_heads <= 0 || s->num_q_heads % s->num_kv_heads != 0 ||
+      s->num_q_heads / s->num_kv_heads > 16)
+    return SSA_ERR_SHAPE;
+  if (s->head_dim != 64 && s->head_dim != 128) return SSA_ERR_HEAD_DIM;
+  if (s->page_size != SSA_PAGE_SIZE) return SSA_ERR_PAGE_SIZE;
+  if (!std::isfinite(s->softmax_scale)) return SSA_ERR_SCALE;
+  if (s->num_pages < 1 || s->max_pages_per_req < 1) return SSA_ERR_PAGES;
+  return SSA_OK;
+}
+
+int resolve_tuning(const ssa_tuning* t, Tuning* out) {
+  Tuning r{kDefaultTileCols, 0, 0, kDefaultCus};
+  if (t) {
+    if (t->chunk_tile_cols) {
+      if (t->chunk_tile_cols != 64 && t->chunk_tile_cols != 128 && t->chunk_tile_cols != 256)
+        return SSA_ERR_TUNING;
+      r.tile_cols = t->chunk_tile_cols;
+    }
+    if (t->chunk_split_keys < 0 || t->chunk_split_keys % kBlockKeys) return SSA_ERR_TUNING;
+    if (t->decode_split_keys < 0 || t->decode_split_keys % kBlockKeys) return SSA_ERR_TUNING;
+    if (t->num_cus < 0 || t->num_cus > 4096) return SSA_ERR_TUNING;
+    r.chunk_split_keys = t->chunk_split_keys;
+    r.decode_split_keys = t->decode_split_keys;
+    if (t->num_cus) r.num_cus = t->num_cus;
+  }
+  *out = r;
+  return SSA_OK;
+}
+
+uint64_t fnv1a(uint64_t h, const void* p, size_t n) {
+  const unsigned char* b = static_cast<const unsigned char*>(p);
+  for (size_t i = 0; i < n; ++i) {
+    h ^= b[i];
+    h *= 1099511628211ull;
+  }
+  return h;
+}
+
+struct Plan {
+  std::vector<ReqEntry> reqs;
+  std::vector<WorkItem> items;
+  std::vector<MergeGroup> groups;
+  std::vector<AppendSeg> segs;
+  PlanHeader hdr;
+  ssa_plan_info info;
+};
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int32_t n,
+          const ssa_tuning* tuning, Plan* p) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (n < 0) return SSA_ERR_LENGTH;
+  if (n > 0 && (!q_len || !ctx_len)) return SSA_ERR_NULL;
+  Tuning tu;
+  rc = resolve_tuning(tuning, &tu);
+  if (rc) return rc;
+
+  const int Hq = s->num_q_heads, Hkv = s->num_kv_heads, D = s->head_dim, P = s->page_size;
+  const int G = Hq / Hkv;
+  int64_t T = 0;
+  for (int i = 0; i < n; ++i) {
+    if (q_len[i] < 0 || ctx_len[i] < 0) return SSA_ERR_LENGTH;
+    if ((int64_t)q_len[i] + ctx_len[i] > kMaxLen) return SSA_ERR_LENGTH;
+    if (ceil_div((int64_t)q_len[i] + ctx_len[i], P) > s->max_pages_per_req) return SSA_ERR_PAGES;
+    T += q_len[i];
+    if (T > kMaxLen) return SSA_ERR_LENGTH;
+  }
+
+  ssa_plan_info& in = p->info;
+  std::memset(&in, 0, sizeof in);
+  in.num_reqs = n;
+  in.num_tokens = (int32_t)T;
+
+  // requests, routing (Eq. 2), features (Tab. 1)
+  p->reqs.resize(n);
+  int64_t qs = 0;
+  double x7 = 0;
+  for (int i = 0; i < n; ++i) {
+    const int64_t c = q_len[i], u = ctx_len[i];
+    p->reqs[i] = ReqEntry{(int32_t)qs, (int32_t)c, (int32_t)u, (int32_t)ceil_div(c + u, P)};
+    qs += c;
+    in.x[2] += (double)u;
+    if (c <= 1) {
+      in.num_decode_reqs++;
+      in.x[3] += 1;
+      in.x[4] += (double)u;
+    } else {
+      in.num_chunk_reqs++;
+      in.x[0] += (double)c * (double)(u + c);
+      in.x[1] += (double)c * (double)c;
+      in.x[5] += (double)c;
+      x7 = std::max(x7, (double)c);
+    }
+    if (c == 1) {
+      in.decode_bytes += (double)(u + 1) * Hkv * D * 4.0 + 2.0 * Hq * D * 2.0;
+      in.decode_flops += 4.0 * Hq * D * (double)(u + 1);
+    } else if (c > 1) {
+      in.chunk_bytes += (double)(u + c) * Hkv * D * 4.0 + (double)c * 2.0 * Hq * D * 2.0;
+      in.chunk_flops += 4.0 * Hq * D * ((double)c * u + (double)c * (c + 1) / 2.0);
+    }
+  }
+  in.x[6] = x7;
+  in.append_bytes = (double)T * Hkv * D * 8.0;
+  if (T == 0) in.scene = SSA_SCENE_EMPTY;
+  else if (in.num_chunk_reqs == 0) in.scene = SSA_SCENE_PURE_DECODE;
+  else if (in.num_decode_reqs == 0) in.scene = SSA_SCENE_PURE_PREFILL;
+  else in.scene = SSA_SCENE_MIXED;
+
+  // append segments: runs of new tokens inside one page
+  p->segs.clear();
+  for (int i = 0; i < n; ++i) {
+    int64_t pos = ctx_len[i], end = (int64_t)ctx_len[i] + q_len[i], row = p->reqs[i].q_start;
+    while (pos < end) {
+      int64_t m = std::min<int64_t>(P - pos % P, end - pos);
+      p->segs.push_back(AppendSeg{i, (int32_t)row, (int32_t)pos, (int32_t)m});
+      pos += m;
+      row += m;
+    }
+  }
+
+  // balancing estimates (seconds): chunk work per CU at the nominal MFMA rate,
+  // decode bytes at the nominal HBM rate shared by num_cus CUs
+  const int ncu = tu.num_cus;
+  double decode_blocks = 0, chunk_time_total = 0;
+  for (int i = 0; i < n; ++i) {
+    if (q_len[i] == 1) decode_blocks += (double)Hkv * ceil_div((int64_t)ctx_len[i] + 1, kBlockKeys);
+    if (q_len[i] > 1)
+      chunk_time_total += 4.0 * Hq * D * ((double)q_len[i] * ctx_len[i] + (double)q_len[i] * q_len[i]) /
+                          kMfmaRatePerCu;
+  }
+  const double makespan =
+      chunk_time_total / ncu + decode_blocks * kBlockKeys * D * 4.0 / kHbmRate;
+
+  int dec_split = tu.decode_split_keys;
+  if (dec_split == 0) {
+    int64_t blocks = (int64_t)std::ceil(decode_blocks / (double)(ncu * 4));
+    blocks = std::max<int64_t>(kWaves, ceil_div(blocks, kWaves) * kWaves);
+    dec_split = (int)std::min<int64_t>(blocks * kBlockKeys, kMaxLen);
+  }
+
+  struct Est {
+    WorkItem it;
+    double t;
+  };
+  std::vector<Est> est;
+  p->groups.clear();
+  int64_t ws_floats = 0;
+  auto add_group = [&](int nsplit, int ncols) {
+    MergeGroup g{nsplit, ncols, ws_floats};
+    ws_floats += (int64_t)nsplit * ncols * (D + 2);
+    p->groups.push_back(g);
+    return (int32_t)p->groups.size() - 1;
+  };
+
+  for (int i = 0; i < n; ++i) {
+    const int c = q_len[i], u = ctx_len[i];
+    if (c > 1) {
+      const int total_cols = c * G;
+      for (int col0 = 0; col0 < total_cols; col0 += tu.tile_cols) {
+        const int ncols = std::min(tu.tile_cols, total_cols - col0);
+        const int j_last = (col0 + ncols - 1) / G;
+        const int kend = u + j_last + 1;
+        for (int h = 0; h < Hkv; ++h) {
+          const double t_tile = 4.0 * D * (double)tu.tile_cols * kend / kMfmaRatePerCu;
+          int nsplit = 1;
+          if (tu.chunk_split_keys > 0) {
+            nsplit = (int)ceil_div(kend, tu.chunk_split_keys);
+          } else if (makespan > 0) {
+            nsplit = (int)std::ceil(t_tile / (0.5 * makespan));
+            nsplit = std::min(nsplit, std::max(1, kend / kMinChunkSplitKeys));
+            nsplit = std::max(1, std::min(nsplit, kMaxChunkSplits));
+          }
+          int piece = (int)ceil_div(ceil_div(kend, nsplit), kBlockKeys) * kBlockKeys;
+          nsplit = (int)ceil_div(kend, piece);
+          const int32_t grp = nsplit > 1 ? add_group(nsplit, ncols) : -1;
+          for (int sp = 0; sp < nsplit; ++sp) {
+            WorkItem it{};
+            it.kind = kItemChunk;
+            it.req = i;
+            it.kvh = h;
+            it.col0 = col0;
+            it.ncols = ncols;
+            it.key0 = sp * piece;
+            it.key1 = std::min(kend, (sp + 1) * piece);
+            it.group = grp;
+            it.split = sp;
+            est.push_back({it, 4.0 * D * (double)tu.tile_cols * (it.key1 - it.key0) / kMfmaRatePerCu});
+          }
+        }
+      }
+    } else if (c == 1) {
+      const int keys = u + 1;
+      const int nsplit = (int)ceil_div(keys, dec_split);
+      for (int h = 0; h < Hkv; ++h) {
+        const int32_t grp = nsplit > 1 ? add_group(nsplit, G) : -1;
+        for (int sp = 0; sp < nsplit; ++sp) {
+          WorkItem it{};
+          it.kind = kItemDecode;
+          it.req = i;
+          it.kvh = h;
+          it.col0 = 0;
+          it.ncols = G;
+          it.key0 = sp * dec_split;
+          it.key1 = std::min(keys, (sp + 1) * dec_split);
+          it.group = grp;
+          it.split = sp;
+          est.push_back({it, (double)(it.key1 - it.key0) * D * 4.0 * ncu / kHbmRate});
+        }
+      }
+    }
+  }
+  // longest first: the dispatcher hands out workgroups in index order
+  std::stable_sort(est.begin(), est.end(), [](const Est& a, const Est& b) { return a.t > b.t; });
+  p->items.resize(est.size());
+  for (size_t k = 0; k < est.size(); ++k) p->items[k] = est[k].it;
+  for (const WorkItem& it : p->items) {
+    if (it.kind == kItemChunk) in.num_chunk_items++;
+    else in.num_decode_items++;
+  }
+  in.num_items = (int32_t)p->items.size();
+  in.num_merge_groups = (int32_t)p->groups.size();
+  in.num_append_segments = (int32_t)p->segs.size();
+
+  PlanHeader& h = p->hdr;
+  std::memset(&h, 0, sizeof h);
+  h.magic = kPlanMagic;
+  h.version = kPlanVersion;
+  h.num_reqs = n;
+  h.num_tokens = (int32_t)T;
+  h.num_items = in.num_items;
+  h.num_chunk_items = in.num_chunk_items;
+  h.num_decode_items = in.num_decode_items;
+  h.num_groups = in.num_merge_groups;
+  h.num_segments = in.num_append_segments;
+  h.hq = Hq;
+  h.hkv = Hkv;
+  h.head_dim = D;
+  h.page_size = P;
+  h.max_pages_per_req = s->max_pages_per_req;
+  h.num_pages = s->num_pages;
+  h.chunk_tile_cols = tu.tile_cols;
+  h.softmax_scale = s->softmax_scale;
+  int64_t off = sizeof(PlanHeader);
+  h.off_reqs = (int32_t)off;
+  off += (int64_t)sizeof(ReqEntry) * n;
+  h.off_items = (int32_t)off;
+  off += (int64_t)sizeof(WorkItem) * p->items.size();
+  h.off_groups = (int32_t)off;
+  off += (int64_t)sizeof(MergeGroup) * p->groups.size();
+  h.off_segments = (int32_t)off;
+  off += (int64_t)sizeof(AppendSeg) * p->segs.size();
+  h.plan_bytes = off;
+  const int64_t tickets = ceil_div((int64_t)p->groups.size() * 4, 256) * 256;
+  h.ws_partials_off = tickets;
+  h.ws_bytes = p->groups.empty() ? 0 : tickets + ws_floats * 4;
+
+  uint64_t hv = 1469598103934665603ull;
+  int32_t fields[8] = {Hq, Hkv, D, P, s->num_pages, s->max_pages_per_req, n, 0};
+  hv = fnv1a(hv, fields, sizeof fields);
+  hv = fnv1a(hv, &s->softmax_scale, sizeof(float));
+  hv = fnv1a(hv, &tu, sizeof tu);
+  if (n > 0) {
+    hv = fnv1a(hv, q_len, sizeof(int32_t) * n);
+    hv = fnv1a(hv, ctx_len, sizeof(int32_t) * n);
+  }
+  h.hash = hv;
+  return SSA_OK;
+}
+
+}  // namespace
+
+// Check that plan_host is a plan built for this shape; used by the launchers.
+int check_plan(const ssa_shape* s, const void* plan_host, const PlanHeader** out) {
+  int rc = check_shape(s);
+  if (rc) return rc;
+  if (!plan_host) return SSA_ERR_NULL;
+  const PlanHeader* h = static_cast<const PlanHeader*>(plan_host);
+  if (h->magic != kPlanMagic || h->version != kPlanVersion || h->hq != s->num_q_heads ||
+      h->hkv != s->num_kv_heads || h->head_dim != s->head_dim || h->page_size != s->page_size ||
+      h->num_pages != s->num_pages || h->max_pages_per_req != s->max_pages_per_req ||
+      std::memcmp(&h->softmax_scale, &s->softmax_scale, sizeof(float)) != 0)
+    return SSA_ERR_PLAN_MISMATCH;
+  *out = h;
+  return SSA_OK;
+}
+
+}  // namespace ssa
+
+extern "C" {
+
+const char* ssa_status_string(int code) {
+  switch (code) {
+    case SSA_OK: return "ok";
+    case SSA_ERR_NULL: return "a required pointer is NULL";
+    case SSA_ERR_SHAPE: return "invalid head counts (Hq, Hkv > 0, Hq % Hkv == 0, Hq/Hkv <= 16)";
+    case SSA_ERR_HEAD_DIM: return "head_dim must be 64 or 128";
+    case SSA_ERR_PAGE_SIZE: return "page_size must be 16";
+    case SSA_ERR_LENGTH: return "negative or too large q_len / ctx_len";
+    case SSA_ERR_PAGES: return "a request needs more pages than max_pages_per_req, or no pages";
+    case SSA_ERR_PLAN_SIZE: return "plan buffer too small";
+    case SSA_ERR_WORKSPACE: return "workspace missing or too small";
+    case SSA_ERR_PLAN_MISMATCH: return "plan does not belong to this shape";
+    case SSA_ERR_HIP: return "HIP launch failed";
+    case SSA_ERR_SCALE: return "softmax_scale is not finite";
+    case SSA_ERR_TUNING: return "tuning field out of range";
+    default: return "unknown";
+  }
+}
+
+int ssa_plan_size(const ssa_shape* shape, const int32_t* q_len_host, const int32_t* ctx_len_host,
+                  int32_t num_reqs, const ssa_tuning* tuning, size_t* plan_bytes,
+                  size_t* workspace_bytes) {
+  if (!plan_bytes || !workspace_bytes) return SSA_ERR_NULL;
+  try {
+    ssa::Plan p;
+    int rc = ssa::build(shape, q_len_host, ctx_len_host, num_reqs, tuning, &p);
+    if (rc) return rc;
+    *plan_bytes = (size_t)p.hdr.plan_bytes;
+    *workspace_bytes = (size_t)p.hdr.ws_bytes;
+    return SSA_OK;
+  } catch (const std::bad_alloc&) {
+    return SSA_ERR_LENGTH;
+  }
+}
+
+int ssa_plan(const ssa_shape* shape, const int32_t* q_len_host, const int32_t* ctx_len_host,
+             int32_t num_reqs, const ssa_tuning* tuning, void* plan_host, size_t plan_bytes,
+             ssa_plan_info* info) {
+  if (!plan_host) return SSA_ERR_NULL;
+  try {
+    ssa::Plan p;
+    int rc = ssa::build(shape, q_len_host, ctx_len_host, num_reqs, tuning, &p);
+    if (rc) return rc;
+    if (plan_bytes < (size_t)p.hdr.plan_bytes) return SSA_ERR_PLAN_SIZE;
+    char* b = static_cast<char*>(plan_host);
+    std::memcpy(b, &p.hdr, sizeof p.hdr);
+    if (!p.reqs.empty())
+      std::memcpy(b + p.hdr.off_reqs, p.reqs.data(), sizeof(ssa::ReqEntry) * p.reqs.size());
+    if (!p.items.empty())
+      std::memcpy(b + p.hdr.off_items, p.items.data(), sizeof(ssa::WorkItem) * p.items.size());
+    if (!p.groups.empty())
+      std::memcpy(b + p.hdr.off_groups, p.groups.data(), sizeof(ssa::MergeGroup) * p.groups.size());
+    if (!p.segs.empty())
+      std::memcpy(b + p.hdr.off_segments, p.segs.data(), sizeof(ssa::AppendSeg) * p.segs.size());
+    if (info) *info = p.info;
+    return SSA_OK;
+  } catch (const std::bad_alloc&) {
+    return SSA_ERR_LENGTH;
+  }
+}
+
+}  // extern "C"

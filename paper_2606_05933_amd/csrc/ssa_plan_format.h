@@ -1,0 +1,86 @@
+// Plan blob of one iteration: written by the host planner, read unchanged by
+// the kernels after a byte copy to device memory.  Every field is a fixed-size
+// integer or float at a fixed offset, so host and device agree byte for byte.
+//
+//   [PlanHeader 128 B][ReqEntry x num_reqs][WorkItem x num_items]
+//   [MergeGroup x num_groups][AppendSeg x num_segments]
+//
+// The workspace of ssa_mixed_attention holds one int32 ticket per merge group
+// (zero at rest) followed, at ws_partials_off, by fp32 partial results:
+// for merge group g and split s, a record of ncols * (D + 2) floats at float
+// offset ws_off + s * ncols * (D + 2): m[ncols], l[ncols], o[ncols][D].
+#pragma once
+#include <stdint.h>
+
+namespace ssa {
+
+constexpr uint32_t kPlanMagic = 0x31415353u;  // "SSA1"
+constexpr uint32_t kPlanVersion = 1;
+constexpr int kBlockKeys = 32;  // keys per attention block: two 16-slot pages
+constexpr int kWaves = 4;       // waves per workgroup
+constexpr int kThreads = 256;   // threads per workgroup
+constexpr int kChunkWaveCols = 64;  // columns a wave owns in a chunk tile
+
+enum ItemKind : int32_t { kItemChunk = 0, kItemDecode = 1 };
+
+struct PlanHeader {
+  uint32_t magic;
+  uint32_t version;
+  uint64_t hash;  // FNV-1a of the shape, the tuning and the length arrays
+  int32_t num_reqs, num_tokens;
+  int32_t num_items, num_chunk_items, num_decode_items, num_groups, num_segments;
+  int32_t hq, hkv, head_dim, page_size, max_pages_per_req, num_pages;
+  int32_t chunk_tile_cols;
+  int32_t off_reqs, off_items, off_groups, off_segments;  // byte offsets in the blob
+  int64_t ws_partials_off;  // byte offset of the partial records in the workspace
+  int64_t ws_bytes;         // workspace bytes the plan needs (0: none)
+  int64_t plan_bytes;       // total blob size
+  float softmax_scale;
+  int32_t reserved[3];
+};
+static_assert(sizeof(PlanHeader) == 128, "plan header size");
+
+struct ReqEntry {
+  int32_t q_start;  // first token row of the request in q / out / k_new / v_new
+  int32_t q_len;    // c_i
+  int32_t ctx_len;  // u_i
+  int32_t n_pages;  // ceil((u_i + c_i) / P): block-table entries that may be read
+};
+
+// One workgroup of the attention launch.
+//   chunk tile: columns [col0, col0 + ncols) of the request's column space, where
+//     column n is (token j = n / G, q head kvh * G + n % G); keys [key0, key1).
+//   decode split: the request's single new token, q heads kvh*G .. kvh*G+G-1
+//     (ncols = G), keys [key0, key1).
+// group < 0: the item writes the final output; otherwise it writes partial
+// record `split` of merge group `group`, and the last of the group's items to
+// finish merges them.
+struct WorkItem {
+  int32_t kind;
+  int32_t req;
+  int32_t kvh;
+  int32_t col0;
+  int32_t ncols;
+  int32_t key0;
+  int32_t key1;
+  int32_t group;
+  int32_t split;
+  int32_t reserved[3];
+};
+static_assert(sizeof(WorkItem) == 48, "work item size");
+
+struct MergeGroup {
+  int32_t nsplit;
+  int32_t ncols;
+  int64_t ws_off;  // float offset of split 0's record from ws_partials_off
+};
+
+// kv_append: n consecutive new tokens of one request that land in one page.
+struct AppendSeg {
+  int32_t req;
+  int32_t row0;  // token row of the first of them
+  int32_t pos0;  // its position u_i + j
+  int32_t n;
+};
+
+}  // namespace ssa

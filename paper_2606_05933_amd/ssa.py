@@ -1,0 +1,215 @@
+"""Thin ctypes binding of ``libssa.so`` (declared in ``include/ssa.h``).
+
+Argument marshalling only: every step of the attention path runs in the
+library's host planner and HIP kernels.  The functions carry the C names.
+Device arrays are torch tensors (``torch.bfloat16`` or 16-bit integer views for
+bf16 data, ``torch.int32`` for the block table, ``torch.uint8`` for the plan
+copy and the workspace); shapes are checked here against the layouts in
+``ssa.h`` so that no launch can index outside a buffer it was given.
+
+The library must be built (``paper_2606_05933_amd.build``); importing this
+module without it raises - there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libssa.so")
+
+SSA_OK = 0
+SCENES = {0: "empty", 1: "pure decode", 2: "pure prefill", 3: "mixed"}
+
+
+class SsaError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {ssa_status_string(code)} ({code})")
+        self.code = code
+
+
+class SsaShape(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32), ("max_pages_per_req", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float)]
+
+
+class SsaTuning(ctypes.Structure):
+    _fields_ = [("chunk_tile_cols", ctypes.c_int32), ("chunk_split_keys", ctypes.c_int32),
+                ("decode_split_keys", ctypes.c_int32), ("num_cus", ctypes.c_int32)]
+
+
+class SsaPlanInfo(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "num_reqs", "num_tokens", "num_decode_reqs", "num_chunk_reqs", "num_items",
+        "num_chunk_items", "num_decode_items", "num_merge_groups", "num_append_segments",
+        "scene")] + [(n, ctypes.c_double) for n in (
+            "decode_bytes", "chunk_bytes", "chunk_flops", "decode_flops", "append_bytes")] + [
+        ("x", ctypes.c_double * 7)]
+
+    def as_dict(self):
+        d = {n: getattr(self, n) for n, _ in self._fields_ if n != "x"}
+        d["x"] = list(self.x)
+        d["scene_name"] = SCENES.get(self.scene, "?")
+        return d
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run paper_2606_05933_amd.build.build() "
+                          "(there is no non-HIP fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    P = ctypes.POINTER
+    lib.ssa_status_string.argtypes = [ctypes.c_int]
+    lib.ssa_status_string.restype = ctypes.c_char_p
+    lib.ssa_plan_size.argtypes = [P(SsaShape), vp, vp, ctypes.c_int32, P(SsaTuning), P(sz), P(sz)]
+    lib.ssa_plan_size.restype = ctypes.c_int
+    lib.ssa_plan.argtypes = [P(SsaShape), vp, vp, ctypes.c_int32, P(SsaTuning), vp, sz,
+                             P(SsaPlanInfo)]
+    lib.ssa_plan.restype = ctypes.c_int
+    lib.ssa_kv_append.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.ssa_kv_append.restype = ctypes.c_int
+    lib.ssa_mixed_attention.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.ssa_mixed_attention.restype = ctypes.c_int
+    return lib
+
+
+LIB = _load()
+
+EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
+            "ssa_mixed_attention")
+
+
+def ssa_status_string(code: int) -> str:
+    return LIB.ssa_status_string(int(code)).decode()
+
+
+def make_shape(hq, hkv, d, num_pages, max_pages_per_req, scale, page_size=16) -> SsaShape:
+    return SsaShape(int(hq), int(hkv), int(d), int(page_size), int(num_pages),
+                    int(max_pages_per_req), float(np.float32(scale)))
+
+
+def make_tuning(chunk_tile_cols=0, chunk_split_keys=0, decode_split_keys=0, num_cus=0):
+    return SsaTuning(int(chunk_tile_cols), int(chunk_split_keys), int(decode_split_keys),
+                     int(num_cus))
+
+
+def _lens(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.int32).reshape(-1))
+    return a, (a.ctypes.data if a.size else None)
+
+
+def ssa_plan_size(shape: SsaShape, q_len, ctx_len, tuning: SsaTuning | None = None):
+    ql, pq = _lens(q_len)
+    cl, pc = _lens(ctx_len)
+    if ql.shape != cl.shape:
+        raise ValueError("q_len and ctx_len differ in length")
+    pb, wb = ctypes.c_size_t(), ctypes.c_size_t()
+    rc = LIB.ssa_plan_size(ctypes.byref(shape), pq, pc, ql.shape[0],
+                           ctypes.byref(tuning) if tuning is not None else None,
+                           ctypes.byref(pb), ctypes.byref(wb))
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_plan_size")
+    return pb.value, wb.value
+
+
+def ssa_plan(shape: SsaShape, q_len, ctx_len, tuning: SsaTuning | None = None, out=None):
+    """Plan blob (numpy uint8, or written into ``out``: a host buffer exposing
+    ``data_ptr()``/``numel()`` or a numpy array) and the plan info."""
+    ql, pq = _lens(q_len)
+    cl, pc = _lens(ctx_len)
+    nbytes, _ = ssa_plan_size(shape, ql, cl, tuning)
+    if out is None:
+        out = np.zeros(nbytes, dtype=np.uint8)
+    if isinstance(out, np.ndarray):
+        ptr, cap = out.ctypes.data, out.nbytes
+    else:
+        ptr, cap = out.data_ptr(), out.numel() * out.element_size()
+    info = SsaPlanInfo()
+    rc = LIB.ssa_plan(ctypes.byref(shape), pq, pc, ql.shape[0],
+                      ctypes.byref(tuning) if tuning is not None else None, ptr, cap,
+                      ctypes.byref(info))
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_plan")
+    return out, info
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _check_dev(name, t, numel, itemsize):
+    if t is None:
+        return
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.element_size() != itemsize:
+        raise ValueError(f"{name} must have {itemsize}-byte elements")
+    if t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, the layout needs {numel}")
+
+
+def _plan_header(plan_host):
+    h = np.frombuffer(bytes(np.asarray(_as_np(plan_host))[:128]), dtype=np.int32)
+    return {"num_reqs": int(h[4]), "num_tokens": int(h[5]), "num_items": int(h[6]),
+            "num_segments": int(h[10])}
+
+
+def _as_np(plan_host):
+    if isinstance(plan_host, np.ndarray):
+        return plan_host
+    return plan_host.numpy()
+
+
+def ssa_kv_append(shape: SsaShape, plan_host, plan_dev, k_new, v_new, k_cache, v_cache,
+                  block_table, stream=None):
+    h = _plan_header(plan_host)
+    T, n = h["num_tokens"], h["num_reqs"]
+    row = shape.num_kv_heads * shape.head_dim
+    pool = shape.num_pages * shape.num_kv_heads * shape.page_size * shape.head_dim
+    _check_dev("k_new", k_new, T * row, 2)
+    _check_dev("v_new", v_new, T * row, 2)
+    _check_dev("k_cache", k_cache, pool, 2)
+    _check_dev("v_cache", v_cache, pool, 2)
+    _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+    rc = LIB.ssa_kv_append(ctypes.byref(shape), _ptr(plan_host), _ptr(plan_dev), _ptr(k_new),
+                           _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                           _stream(stream))
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_kv_append")
+
+
+def ssa_mixed_attention(shape: SsaShape, plan_host, plan_dev, q, k_cache, v_cache, block_table,
+                        out, workspace, stream=None):
+    h = _plan_header(plan_host)
+    T, n = h["num_tokens"], h["num_reqs"]
+    qrow = shape.num_q_heads * shape.head_dim
+    pool = shape.num_pages * shape.num_kv_heads * shape.page_size * shape.head_dim
+    _check_dev("q", q, T * qrow, 2)
+    _check_dev("out", out, T * qrow, 2)
+    _check_dev("k_cache", k_cache, pool, 2)
+    _check_dev("v_cache", v_cache, pool, 2)
+    _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    rc = LIB.ssa_mixed_attention(ctypes.byref(shape), _ptr(plan_host), _ptr(plan_dev), _ptr(q),
+                                 _ptr(k_cache), _ptr(v_cache), _ptr(block_table), _ptr(out),
+                                 _ptr(workspace), ws_bytes, _stream(stream))
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_mixed_attention")

@@ -1,0 +1,290 @@
+"""Host-side tests of the C ABI (no GPU): exports, argument validation, and the
+plan's coverage of the batch (SlidingServe Sec. 3.2: B = {(c_i, u_i)}, Eq. 2
+routing, Eq. 3 scene, Tab. 1 features)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_05933_amd import ssa, workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+HDR = np.dtype([("magic", "<u4"), ("version", "<u4"), ("hash", "<u8"), ("num_reqs", "<i4"),
+                ("num_tokens", "<i4"), ("num_items", "<i4"), ("num_chunk_items", "<i4"),
+                ("num_decode_items", "<i4"), ("num_groups", "<i4"), ("num_segments", "<i4"),
+                ("hq", "<i4"), ("hkv", "<i4"), ("head_dim", "<i4"), ("page_size", "<i4"),
+                ("max_pages_per_req", "<i4"), ("num_pages", "<i4"), ("chunk_tile_cols", "<i4"),
+                ("off_reqs", "<i4"), ("off_items", "<i4"), ("off_groups", "<i4"),
+                ("off_segments", "<i4"), ("ws_partials_off", "<i8"), ("ws_bytes", "<i8"),
+                ("plan_bytes", "<i8"), ("scale", "<f4"), ("reserved", "<i4", 3)])
+REQ = np.dtype([("q_start", "<i4"), ("q_len", "<i4"), ("ctx_len", "<i4"), ("n_pages", "<i4")])
+ITEM = np.dtype([("kind", "<i4"), ("req", "<i4"), ("kvh", "<i4"), ("col0", "<i4"),
+                 ("ncols", "<i4"), ("key0", "<i4"), ("key1", "<i4"), ("group", "<i4"),
+                 ("split", "<i4"), ("reserved", "<i4", 3)])
+GROUP = np.dtype([("nsplit", "<i4"), ("ncols", "<i4"), ("ws_off", "<i8")])
+SEG = np.dtype([("req", "<i4"), ("row0", "<i4"), ("pos0", "<i4"), ("n", "<i4")])
+
+
+def parse(blob):
+    blob = np.asarray(blob, dtype=np.uint8)
+    h = np.frombuffer(blob[:128].tobytes(), HDR)[0]
+
+    def arr(off, dt, n):
+        return np.frombuffer(blob[off: off + dt.itemsize * n].tobytes(), dt)
+
+    return (h, arr(h["off_reqs"], REQ, h["num_reqs"]), arr(h["off_items"], ITEM, h["num_items"]),
+            arr(h["off_groups"], GROUP, h["num_groups"]),
+            arr(h["off_segments"], SEG, h["num_segments"]))
+
+
+def shape_of(hq, hkv, d, q_len, ctx_len, extra_pages=0, num_pages=None, scale=None):
+    maxp = max([1] + [(u + c + 15) // 16 for c, u in zip(q_len, ctx_len)]) + extra_pages
+    npages = num_pages if num_pages is not None else 4096
+    return ssa.make_shape(hq, hkv, d, npages, maxp, scale if scale is not None else d ** -0.5)
+
+
+def test_library_exports_every_declared_symbol():
+    text = open(os.path.join(ROOT, "include", "ssa.h")).read()
+    declared = set(re.findall(r"\b(ssa_[a-z_]+)\s*\(", text))
+    assert declared == set(ssa.EXPORTED)
+    lib = ctypes.CDLL(ssa.LIB_PATH)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def check_plan_covers_batch(hq, hkv, d, q_len, ctx_len, tuning=None):
+    shape = shape_of(hq, hkv, d, q_len, ctx_len)
+    blob, info = ssa.ssa_plan(shape, q_len, ctx_len, tuning)
+    h, reqs, items, groups, segs = parse(blob)
+    G = hq // hkv
+    n = len(q_len)
+    assert h["magic"] == 0x31415353 and h["num_reqs"] == n
+    qs = np.concatenate([[0], np.cumsum(q_len)[:-1]]) if n else np.zeros(0)
+    assert np.array_equal(reqs["q_start"], qs) and np.array_equal(reqs["q_len"], q_len)
+    # every (row, head) is covered by key ranges that partition [0, pos + 1)
+    cover = {}
+    for it in items:
+        i = it["req"]
+        c, u = int(q_len[i]), int(ctx_len[i])
+        if it["kind"] == 1:
+            assert c == 1 and it["ncols"] == G
+            cols = [(int(reqs["q_start"][i]), it["kvh"] * G + hg, u) for hg in range(G)]
+        else:
+            assert c > 1
+            cols = []
+            for cc in range(it["col0"], it["col0"] + it["ncols"]):
+                j, hg = divmod(cc, G)
+                assert j < c
+                cols.append((int(reqs["q_start"][i]) + j, it["kvh"] * G + hg, u + j))
+        for row, head, pos in cols:
+            lo, hi = it["key0"], min(it["key1"], pos + 1)
+            if hi > lo:
+                cover.setdefault((row, head), []).append((lo, hi))
+            else:  # a split beyond this column's diagonal: empty but allowed
+                assert it["group"] >= 0
+    for i in range(n):
+        for j in range(int(q_len[i])):
+            for head in range(hq):
+                rngs = sorted(cover.pop((int(reqs["q_start"][i]) + j, head)))
+                assert rngs[0][0] == 0 and rngs[-1][1] == int(ctx_len[i]) + j + 1
+                assert all(a[1] == b[0] for a, b in zip(rngs, rngs[1:]))
+    assert not cover
+    # merge groups: every split exactly once, records disjoint and inside the workspace
+    for gi, g in enumerate(groups):
+        mem = items[items["group"] == gi]
+        assert sorted(mem["split"]) == list(range(g["nsplit"]))
+        assert (mem["ncols"] == g["ncols"]).all()
+        end = h["ws_partials_off"] + 4 * (g["ws_off"] + g["nsplit"] * g["ncols"] * (d + 2))
+        assert end <= h["ws_bytes"]
+    offs = sorted((g["ws_off"], g["ws_off"] + g["nsplit"] * g["ncols"] * (d + 2)) for g in groups)
+    assert all(a[1] <= b[0] for a, b in zip(offs, offs[1:]))
+    assert ((items["group"] < 0) | (items["group"] < len(groups))).all()
+    # append segments: each new token exactly once, inside one page
+    seen = []
+    for sg in segs:
+        assert sg["pos0"] // 16 == (sg["pos0"] + sg["n"] - 1) // 16
+        i = sg["req"]
+        for k in range(sg["n"]):
+            seen.append((sg["row0"] + k, sg["pos0"] + k - int(ctx_len[i])))
+    expect = [(int(reqs["q_start"][i]) + j, j) for i in range(n) for j in range(int(q_len[i]))]
+    assert sorted(seen) == sorted(expect)
+    return info, items
+
+
+PLAN_CASES = [
+    (8, 8, 64, [64, 1, 1, 1, 1], [192, 128, 256, 384, 512]),
+    (32, 8, 128, [512] + [1] * 9, [2048] + list(range(500, 4100, 400))),
+    (28, 4, 128, [64, 256, 0, 1, 1, 3], [7000, 13, 5, 0, 16383, 1]),
+    (16, 16, 64, [2, 1, 0], [0, 0, 0]),
+    (4, 1, 128, [1000, 1], [33000, 32767]),
+]
+
+
+@pytest.mark.parametrize("case", PLAN_CASES)
+def test_plan_partitions_every_output_key_range(case):
+    hq, hkv, d, q_len, ctx_len = case
+    check_plan_covers_batch(hq, hkv, d, np.array(q_len, np.int32), np.array(ctx_len, np.int32))
+
+
+@pytest.mark.parametrize("tile", [64, 128, 256])
+@pytest.mark.parametrize("csplit", [0, 1024, 4096])
+def test_plan_partitions_under_tuning(tile, csplit):
+    q_len = np.array([700, 33, 1, 1], np.int32)
+    ctx_len = np.array([5000, 100, 9000, 31], np.int32)
+    tu = ssa.make_tuning(chunk_tile_cols=tile, chunk_split_keys=csplit, decode_split_keys=512)
+    info, items = check_plan_covers_batch(28, 4, 128, q_len, ctx_len, tu)
+    assert info.num_items == len(items)
+
+
+def test_plan_on_generated_workloads():
+    for name in workload.WORKLOADS:
+        shape, q_len, ctx_len = workload.workload_lengths(name, seed=3)
+        check_plan_covers_batch(shape.hq, shape.hkv, shape.d, q_len, ctx_len)
+
+
+def test_scene_and_features_follow_the_paper():
+    # Eq. 2: D = {c <= 1}, P = {c > 1}; Eq. 3 scene; Tab. 1 features x1..x7
+    q_len = np.array([5, 1, 0, 9, 1], np.int32)
+    ctx_len = np.array([10, 20, 30, 0, 7], np.int32)
+    shape = shape_of(8, 2, 64, q_len, ctx_len)
+    _, info = ssa.ssa_plan(shape, q_len, ctx_len)
+    P = q_len > 1
+    Dm = ~P
+    x = [np.sum(q_len[P] * (ctx_len[P] + q_len[P])), np.sum(q_len[P] ** 2), np.sum(ctx_len),
+         np.sum(Dm), np.sum(ctx_len[Dm]), np.sum(q_len[P]), np.max(q_len[P])]
+    assert list(info.x) == [float(v) for v in x]
+    assert info.scene == 3 and info.num_decode_reqs == 3 and info.num_chunk_reqs == 2
+    hq, hkv, d = 8, 2, 64
+    cf = sum(4 * hq * d * (c * u + c * (c + 1) / 2) for c, u in zip(q_len[P], ctx_len[P]))
+    assert info.chunk_flops == cf
+    db = sum((u + 1) * hkv * d * 4 + 2 * hq * d * 2 for c, u in zip(q_len, ctx_len) if c == 1)
+    assert info.decode_bytes == db
+    for ql, scene in (([1, 1, 0], 1), ([4, 2], 2), ([0, 0], 0), ([], 0)):
+        ql = np.array(ql, np.int32)
+        cl = np.zeros_like(ql)
+        _, inf = ssa.ssa_plan(shape_of(8, 2, 64, ql, cl), ql, cl)
+        assert inf.scene == scene
+
+
+def test_plan_is_deterministic():
+    q_len = np.array([300, 1, 1, 1], np.int32)
+    ctx_len = np.array([0, 5, 900, 40], np.int32)
+    shape = shape_of(32, 8, 128, q_len, ctx_len)
+    a, _ = ssa.ssa_plan(shape, q_len, ctx_len)
+    b, _ = ssa.ssa_plan(shape, q_len, ctx_len)
+    assert a.tobytes() == b.tobytes()
+    c, _ = ssa.ssa_plan(shape, q_len, ctx_len + np.array([0, 0, 1, 0], np.int32))
+    assert parse(a)[0]["hash"] != parse(c)[0]["hash"]
+
+
+# ---------------------------------------------------------------- validation
+
+def plan_rc(shape, q_len, ctx_len, tuning=None, cap=None):
+    ql = np.asarray(q_len, np.int32)
+    cl = np.asarray(ctx_len, np.int32)
+    buf = np.zeros(cap if cap is not None else 1 << 16, np.uint8)
+    info = ssa.SsaPlanInfo()
+    return ssa.LIB.ssa_plan(ctypes.byref(shape), ql.ctypes.data if ql.size else None,
+                            cl.ctypes.data if cl.size else None, ql.shape[0],
+                            ctypes.byref(tuning) if tuning is not None else None,
+                            buf.ctypes.data, buf.nbytes, ctypes.byref(info)), buf
+
+
+@pytest.mark.parametrize("mutate,code", [
+    (dict(num_q_heads=0), -2), (dict(num_kv_heads=3), -2), (dict(num_q_heads=34, num_kv_heads=2), -2),
+    (dict(head_dim=96), -3), (dict(page_size=8), -4), (dict(softmax_scale=float("inf")), -11),
+    (dict(num_pages=0), -6), (dict(max_pages_per_req=0), -6),
+])
+def test_bad_shape_codes(mutate, code):
+    shape = ssa.make_shape(8, 2, 64, 100, 8, 0.125)
+    for k, v in mutate.items():
+        setattr(shape, k, v)
+    rc, buf = plan_rc(shape, [3, 1], [5, 6])
+    assert rc == code
+    assert not buf.any()  # nothing written on error
+    assert ssa.ssa_status_string(code) not in ("ok", "unknown")
+
+
+def test_bad_lengths_and_pages_and_buffers():
+    shape = ssa.make_shape(8, 2, 64, 100, 4, 0.125)
+    assert plan_rc(shape, [-1, 1], [5, 6])[0] == -5
+    assert plan_rc(shape, [1, 1], [5, -6])[0] == -5
+    assert plan_rc(shape, [1, 1], [5, 64])[0] == -6  # 65 keys need 5 pages > 4
+    assert plan_rc(shape, [1, 1], [5, 63])[0] == 0
+    assert plan_rc(shape, [1, 1], [5, 6], cap=64)[0] == -7
+    assert plan_rc(shape, [1], [5], tuning=ssa.make_tuning(chunk_tile_cols=96))[0] == -12
+    assert plan_rc(shape, [1], [5], tuning=ssa.make_tuning(decode_split_keys=100))[0] == -12
+    pb, wb = ctypes.c_size_t(), ctypes.c_size_t()
+    assert ssa.LIB.ssa_plan_size(None, None, None, 0, None, ctypes.byref(pb), ctypes.byref(wb)) == -1
+    assert ssa.LIB.ssa_plan_size(ctypes.byref(shape), None, None, 2, None, ctypes.byref(pb),
+                                 ctypes.byref(wb)) == -1
+    assert ssa.ssa_status_string(12345) == "unknown"
+
+
+def test_launchers_validate_before_any_hip_call():
+    q_len = np.array([40, 1, 1], np.int32)
+    ctx_len = np.array([5000, 3000, 9000], np.int32)
+    shape = shape_of(32, 8, 128, q_len, ctx_len)
+    blob, info = ssa.ssa_plan(shape, q_len, ctx_len, ssa.make_tuning(decode_split_keys=1024))
+    assert info.num_merge_groups > 0
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
+    L = ssa.LIB
+    p = blob.ctypes.data
+    # NULL arguments
+    assert L.ssa_kv_append(ctypes.byref(shape), p, None, fake, fake, fake, fake, fake, None) == -1
+    assert L.ssa_kv_append(ctypes.byref(shape), p, fake, None, fake, fake, fake, fake, None) == -1
+    assert L.ssa_mixed_attention(ctypes.byref(shape), p, fake, fake, fake, fake, fake, None, fake,
+                                 1 << 30, None) == -1
+    assert L.ssa_mixed_attention(ctypes.byref(shape), None, fake, fake, fake, fake, fake, fake,
+                                 fake, 1 << 30, None) == -1
+    # workspace too small / missing
+    _, ws = ssa.ssa_plan_size(shape, q_len, ctx_len, ssa.make_tuning(decode_split_keys=1024))
+    assert ws > 0
+    assert L.ssa_mixed_attention(ctypes.byref(shape), p, fake, fake, fake, fake, fake, fake, fake,
+                                 ws - 1, None) == -8
+    assert L.ssa_mixed_attention(ctypes.byref(shape), p, fake, fake, fake, fake, fake, fake, None,
+                                 ws, None) == -8
+    # a plan of another shape
+    other = shape_of(32, 8, 128, q_len, ctx_len, num_pages=77)
+    assert L.ssa_mixed_attention(ctypes.byref(other), p, fake, fake, fake, fake, fake, fake, fake,
+                                 ws, None) == -9
+    assert L.ssa_kv_append(ctypes.byref(other), p, fake, fake, fake, fake, fake, fake, None) == -9
+    junk = np.zeros(256, np.uint8)
+    assert L.ssa_kv_append(ctypes.byref(shape), junk.ctypes.data, fake, fake, fake, fake, fake,
+                           fake, None) == -9
+
+
+def test_empty_batch_launches_nothing():
+    shape = ssa.make_shape(8, 2, 64, 10, 1, 0.125)
+    blob, info = ssa.ssa_plan(shape, np.zeros(0, np.int32), np.zeros(0, np.int32))
+    assert info.num_items == 0 and info.scene == 0
+    L = ssa.LIB
+    # no work: returns OK without touching (NULL) buffers or launching
+    assert L.ssa_kv_append(ctypes.byref(shape), blob.ctypes.data, ctypes.c_void_p(0x1000), None,
+                           None, None, None, None, None) == 0
+    assert L.ssa_mixed_attention(ctypes.byref(shape), blob.ctypes.data, ctypes.c_void_p(0x1000),
+                                 None, None, None, None, None, None, 0, None) == 0
+
+
+def test_generator_is_deterministic_and_poisons_unwritten_slots():
+    a = workload.make_workload("tiny", seed=4)
+    b = workload.make_workload("tiny", seed=4)
+    c = workload.make_workload("tiny", seed=5)
+    assert a.digest() == b.digest() != c.digest()
+    nan = workload.BF16_NAN
+    for i, (cq, u) in enumerate(zip(a.q_len, a.ctx_len)):
+        for t in range(u, u + cq):
+            pg, sl = a.block_table[i, t // 16], t % 16
+            assert (a.k_cache[pg, :, sl, :] == nan).all() and (a.v_cache[pg, :, :, sl] == nan).all()
+        if u:
+            pg = a.block_table[i, (u - 1) // 16]
+            assert not (a.k_cache[pg, :, (u - 1) % 16, :] == nan).any()
+    used = set(a.block_table[a.block_table >= 0].tolist())
+    spare = [p for p in range(a.num_pages) if p not in used]
+    assert len(spare) == 64 and (a.k_cache[spare] == nan).all()
+    x = np.float32([1.0, 1.00390625, 1.01171875, -2.5, 3.1415926])
+    assert np.array_equal(workload.bf16_bits_to_f32(workload.f32_to_bf16_bits(x)),
+                          np.float32([1.0, 1.0, 1.015625, -2.5, 3.140625]))

@@ -1,0 +1,183 @@
+"""Parity of the HIP path with the CPU oracle, through the C ABI, on an MI355X.
+
+Bars: kv_append bit-exact (the whole pool image, untouched bytes included);
+attention within max |err| <= 2e-2 and mean |err| <= 2e-3 of the fp64 oracle on
+bf16 outputs (fp32 accumulation on the GPU).  Pools are NaN-poisoned wherever a
+kernel must not read (unwritten slots, the tail of a request's last page, spare
+pages), so a leak shows up as a non-finite output.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS = 2e-2
+MEAN_ABS = 2e-3
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    torch.cuda.set_device(0)
+    return torch
+
+
+def run(b, tuning=None):
+    import torch
+    from paper_2606_05933_amd.device import DeviceBatch
+    say(f"[gpu] {b.name} reqs={b.num_reqs} T={b.num_tokens} hq/hkv/d={b.shape.hq}/{b.shape.hkv}/"
+        f"{b.shape.d} seed={b.seed}")
+    db = DeviceBatch(b, tuning)
+    db.step()
+    torch.cuda.synchronize()
+    return db
+
+
+def assert_close(got, ref, what=""):
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    err = np.abs(got.astype(np.float64) - ref)
+    say(f"    {what}: max_abs={err.max() if err.size else 0:.3e} "
+        f"mean_abs={err.mean() if err.size else 0:.3e} n={err.size}")
+    if err.size:
+        assert err.max() <= MAX_ABS, f"{what}: max abs {err.max()}"
+        assert err.mean() <= MEAN_ABS, f"{what}: mean abs {err.mean()}"
+
+
+def full_parity(b, tuning=None):
+    from oracle import oracle
+    from paper_2606_05933_amd.device import bits_of
+    db = run(b, tuning)
+    kc, vc = oracle.batch_kv_append(b)
+    assert np.array_equal(bits_of(db.k_cache).reshape(kc.shape), kc), "K pool image differs"
+    assert np.array_equal(bits_of(db.v_cache).reshape(vc.shape), vc), "V pool image differs"
+    ref, _ = oracle.batch_attention(b, kc, vc)
+    assert_close(db.out_f32(), ref, b.name)
+    return db
+
+
+def small(hq, hkv, d, cu, seed=0, name="small"):
+    from paper_2606_05933_amd import workload
+    shape = workload.Shape(hq, hkv, d)
+    q_len = [c for c, _ in cu]
+    ctx = [u for _, u in cu]
+    return workload.make_batch(shape, q_len, ctx, seed=seed, spare_pages=7, name=name)
+
+
+SMALL = [
+    # edge cases: u = 0, a single key, c = 0 rows, unaligned prefixes, chunks crossing pages
+    (8, 8, 64, [(1, 0)]),
+    (8, 8, 64, [(1, 0), (0, 5), (2, 0), (1, 15), (1, 16), (1, 31), (1, 32), (1, 33)]),
+    (32, 8, 128, [(17, 0), (1, 0), (33, 31), (0, 0), (1, 47)]),
+    (28, 4, 128, [(64, 0), (1, 100), (100, 1000), (1, 2047)]),        # G = 7
+    (64, 8, 128, [(70, 400), (1, 1), (1, 4097)]),                    # G = 8
+    (16, 1, 64, [(40, 60), (1, 500)]),                               # G = 16
+    (4, 4, 128, [(300, 77), (1, 129)]),                               # G = 1, D = 128
+    (12, 4, 64, [(2, 0), (3, 1), (65, 1023), (1, 0)]),                # G = 3, D = 64
+]
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_small_batches_match_oracle(torch_dev, case):
+    hq, hkv, d, cu = SMALL[case]
+    full_parity(small(hq, hkv, d, cu, seed=case, name=f"small{case}"))
+
+
+def test_tiny_workload_matches_oracle(torch_dev):
+    from paper_2606_05933_amd import workload
+    full_parity(workload.make_workload("tiny", seed=0))
+
+
+def test_llama8b_mixed_full_parity(torch_dev):
+    from paper_2606_05933_amd import workload
+    full_parity(workload.make_workload("l8b", seed=0))
+
+
+@pytest.mark.parametrize("tile,csplit,dsplit", [(64, 0, 0), (128, 1024, 256), (256, 512, 128),
+                                                (256, 0, 4096)])
+def test_tuning_variants_match_oracle(torch_dev, tile, csplit, dsplit):
+    from paper_2606_05933_amd import ssa
+    b = small(32, 8, 128, [(300, 1500), (1, 3000), (1, 100), (45, 0)], seed=11, name="tuned")
+    full_parity(b, ssa.make_tuning(chunk_tile_cols=tile, chunk_split_keys=csplit,
+                                   decode_split_keys=dsplit))
+
+
+def test_scenes_pure_decode_and_pure_prefill(torch_dev):
+    from paper_2606_05933_amd import workload
+    b = workload.make_workload("l8b", seed=1)
+    dec = workload.sub_batch(b, b.q_len == 1)
+    dec.name = "l8b-pure-decode"
+    db = full_parity(dec)
+    assert db.info.scene == 1
+    pre = workload.sub_batch(b, b.q_len > 1)
+    pre.name = "l8b-pure-prefill"
+    db = full_parity(pre)
+    assert db.info.scene == 2
+
+
+def sampled_parity(b, n_chunk_rows=24, heads_per_row=4, seed=0):
+    """Oracle at sampled (row, head) pairs of a full-size batch."""
+    from oracle import oracle
+    db = run(b)
+    out = db.out_f32()
+    rng = np.random.default_rng(seed)
+    starts = np.concatenate([[0], np.cumsum(b.q_len)])
+    rows = []
+    for i in range(b.num_reqs):
+        c = int(b.q_len[i])
+        if c == 1:
+            rows.append(starts[i])
+        elif c > 1:
+            pick = {0, 1, c - 1, c // 2} | set(rng.integers(0, c, size=n_chunk_rows).tolist())
+            rows.extend(starts[i] + j for j in sorted(pick))
+    sel_rows, sel_heads = [], []
+    for r in rows:
+        for h in rng.choice(b.shape.hq, size=min(heads_per_row, b.shape.hq), replace=False):
+            sel_rows.append(r)
+            sel_heads.append(h)
+    s = b.shape
+    # the device pools hold the appended rows; the oracle appends on its own copy
+    kc, vc = oracle.batch_kv_append(b)
+    ref, _ = oracle.attention_rows(s.hq, s.hkv, s.d, s.page, s.softmax_scale, b.q_len, b.ctx_len,
+                                   b.block_table, b.q, kc, vc, np.array(sel_rows),
+                                   np.array(sel_heads))
+    got = out[np.array(sel_rows), np.array(sel_heads)]
+    assert_close(got, ref, f"{b.name} sampled")
+    assert np.isfinite(out).all(), "non-finite output outside the sample"
+
+
+@pytest.mark.parametrize("name,chunk,prefix", [
+    ("multi", None, None), ("l70b", None, None),
+    ("l8b_sweep", 2048, 6144), ("l8b_sweep", 128, 0), ("l8b_sweep", 1024, 2048),
+])
+def test_full_size_sampled_parity(torch_dev, name, chunk, prefix):
+    from paper_2606_05933_amd import workload
+    b = workload.make_workload(name, seed=0, chunk=chunk, prefix=prefix)
+    b.name = f"{name}(c={chunk},u={prefix})"
+    sampled_parity(b)
+
+
+def test_repeat_launches_are_bitwise_identical_and_reset_tickets(torch_dev):
+    import torch
+    from paper_2606_05933_amd import ssa
+    b = small(32, 8, 128, [(300, 1500), (1, 3000), (1, 5000)], seed=3, name="repeat")
+    db = run(b, ssa.make_tuning(chunk_split_keys=512, decode_split_keys=256))
+    assert db.info.num_merge_groups > 0
+    first = db.out.clone()
+    for k in range(200):
+        db.out.zero_()
+        db.attention()
+        if k % 50 == 49:
+            torch.cuda.synchronize()
+            assert torch.equal(db.out.view(torch.int16), first.view(torch.int16)), k
+    torch.cuda.synchronize()
+    ng = db.info.num_merge_groups
+    tickets = db.workspace[: 4 * ng].view(torch.int32)
+    assert int(tickets.abs().sum()) == 0
