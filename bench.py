@@ -1,0 +1,366 @@
+#!/usr/bin/env python3
+"""Benchmark of one serving iteration's attention hot path on one MI355X.
+
+A step is the whole path for one batch B = {(c_i, u_i)} (SlidingServe Sec. 3.2):
+host planning (routing by Eq. 2, work items), the plan's copy to the device,
+``ssa_kv_append`` and the single ``ssa_mixed_attention`` launch.  The default
+workload is the Llama-3-8B-shaped mixed batch (32 q / 8 kv heads, D = 128, page
+16; one 512-token chunk on a 2048-token prefix plus 64 decodes with contexts
+uniform in [512, 4096]), synthetic and seeded; inputs are resident in HBM before
+the timed region starts.
+
+Printed on stdout, as the last line: one JSON object with the metric (µs per
+iteration), the dominant kernel's roofline (live HIP-event timing of the
+attention launch against MI355X's 8 TB/s HBM peak), and the CPU oracle timed on
+this host (a reported baseline, not the target).
+
+Other modes (all single GPU):
+  --sweep OUT        latency-vs-chunk-size table of every workload (JSON lines)
+  --copy-probe       plain 1 GiB device copies (the scale of the traffic counters)
+  --only-attention   time the attention launch alone (for counter runs)
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "mixed prefill+decode attention µs/iter vs chunk size; % HBM / MFMA roofline"
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_05933_amd", "csrc", "ssa_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_mixed_attention_l8b.json")
+
+DESCR = {
+    "tiny": "tiny mixed: 8q/8kv/D64, 1 chunk (u=192,c=64) + 4 decodes u in {128,256,384,512}",
+    "l8b": "Llama-3-8B-shaped mixed layer: 32q/8kv/D128, 1 chunk (u=2048,c=512) + 64 decodes "
+           "u~U[512,4096], page 16",
+    "l8b_sweep": "Llama-3-8B-shaped chunk sweep: 32q/8kv/D128, 1 chunk of an 8192-token prompt "
+                 "+ 128 decodes u~round(LogN(7.0,0.8)) in [64,8192]",
+    "multi": "multi-chunk: 28q/4kv/D128, 4 chunks {64,256,512,1024} at u~U[0,8192] + 256 decodes "
+             "u~round(LogN(7.2,1.0)) in [64,16384]",
+    "l70b": "Llama-3-70B-shaped layer: 64q/8kv/D128, 1 chunk (u=32768,c=1024) + 32 decodes "
+            "u~U[8192,32768]",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def sha256_file(p):
+    with open(p, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def time_kernel_events(fn, n, flush=None):
+    """Average duration (s) of fn's launches, bracketed by events on the current stream."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(n)]
+    for a, b in evs:
+        if flush is not None:
+            flush()
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return statistics.mean(a.elapsed_time(b) for a, b in evs) / 1e3
+
+
+class Flusher:
+    """1 GiB device write between launches: evicts the L2s and the 256 MB MALL."""
+
+    def __init__(self):
+        import torch
+        self.buf = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+
+    def __call__(self):
+        self.buf.fill_(1.0)
+
+
+def segment_stats(db, n, flush=None):
+    us = time_kernel_events(db.attention, n, flush) * 1e6
+    info = db.info
+    hbm = info.decode_bytes + info.chunk_bytes
+    return {"us": round(us, 2), "scene": info.scene,
+            "hbm_GBps": round(hbm / us / 1e3, 1), "hbm_frac": round(hbm / us / 1e3 / HBM_PEAK_GBS, 4),
+            "mfma_TFLOPs": round(info.chunk_flops / us / 1e6, 1),
+            "mfma_frac": round(info.chunk_flops / us / 1e6 / MFMA_BF16_PEAK_TFLOPS, 4)}
+
+
+def cpu_baseline(b, min_seconds=10.0, max_reps=30):
+    """The fp64 oracle (kv_append + attention) of the same batch on this host's cores."""
+    import numpy as np
+    from oracle import oracle
+    s = b.shape
+    times, used = [], 0
+    t_start = time.perf_counter()
+    while len(times) < max_reps and (time.perf_counter() - t_start < min_seconds or len(times) < 3):
+        kc = b.k_cache.copy()
+        vc = b.v_cache.copy()
+        t0 = time.perf_counter()
+        oracle.kv_append_inplace(s.hkv, s.d, s.page, b.q_len, b.ctx_len, b.block_table, b.k_new,
+                                 b.v_new, kc, vc)
+        _, used = oracle.attention(s.hq, s.hkv, s.d, s.page, s.softmax_scale, b.q_len, b.ctx_len,
+                                   b.block_table, b.q, kc, vc)
+        times.append(time.perf_counter() - t0)
+        del kc, vc
+    med = statistics.median(times)
+    return {"value": round(med * 1e6, 1), "unit": "us/iter", "cores": int(used), "kind": "oracle",
+            "sample": f"the whole {b.name} iteration (kv_append + attention of all "
+                      f"{b.num_tokens} new tokens), fp64, median of {len(times)} runs",
+            "tokens_per_s": round(b.num_tokens / med, 1)}
+
+
+def traffic_bytes():
+    """HBM bytes per attention launch from committed rocprofv3 counter runs, if
+    they were taken on the current kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    t = json.load(open(TRAFFIC_FILE))
+    if t.get("kernel_source_sha256") != sha256_file(KERNEL_SRC):
+        return None
+    return (t["fetch_kib"] / t["copy_fetch_factor"] + t["write_kib"] / t["copy_write_factor"]) * 1024
+
+
+def main_bench(args):
+    import torch
+    from paper_2606_05933_amd import workload
+    from paper_2606_05933_amd.device import DeviceBatch
+
+    torch.cuda.set_device(0)
+    log(f"[bench] generating {args.workload} seed={args.seed}")
+    b = workload.make_workload(args.workload, seed=args.seed)
+    db = DeviceBatch(b)
+    info = db.info
+    log(f"[bench] items={info.num_items} (chunk {info.num_chunk_items}, decode "
+        f"{info.num_decode_items}) groups={info.num_merge_groups} scene={info.scene}")
+
+    def step():
+        db.replan_host()
+        db.kv_append()
+        db.attention()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev_a = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ev_b = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ev_c = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    plan_s = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        tp = time.perf_counter()
+        db.replan_host()
+        plan_s.append(time.perf_counter() - tp)
+        ev_a[i].record()
+        db.kv_append()
+        ev_b[i].record()
+        db.attention()
+        ev_c[i].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall / args.steps * 1e3
+    attn_s = statistics.mean(b_.elapsed_time(c_) for b_, c_ in zip(ev_b, ev_c)) / 1e3
+    app_s = statistics.mean(a_.elapsed_time(b_) for a_, b_ in zip(ev_a, ev_b)) / 1e3
+    log(f"[bench] step {ms_per_step * 1e3:.1f} us, attention {attn_s * 1e6:.1f} us, "
+        f"kv_append {app_s * 1e6:.1f} us, plan {statistics.mean(plan_s) * 1e6:.1f} us")
+
+    alg_bytes = info.decode_bytes + info.chunk_bytes
+    achieved = alg_bytes / attn_s / 1e9
+    tb = traffic_bytes()
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": None if tb is None else round(tb),
+                "kernel": "mixed_attention", "algorithmic_bytes": round(alg_bytes),
+                "kernel_us": round(attn_s * 1e6, 2)}
+
+    extra = {}
+    if not args.quick:
+        flush = Flusher()
+        extra["attention_cold_us"] = round(time_kernel_events(db.attention, 20, flush) * 1e6, 2)
+        dec = workload.sub_batch(b, b.q_len == 1)
+        pre = workload.sub_batch(b, b.q_len > 1)
+        dd, dp = DeviceBatch(dec), DeviceBatch(pre)
+        dd.step(), dp.step()
+        torch.cuda.synchronize()
+        extra["pure_decode"] = segment_stats(dd, 20, flush)
+        extra["pure_prefill"] = segment_stats(dp, 20, flush)
+        del dd, dp, flush
+        torch.cuda.empty_cache()
+
+    res = {
+        "metric": METRIC, "value": round(ms_per_step * 1e3, 2), "unit": "us/iter",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 Q/K/V, seeded random block tables; stands in "
+                "for the paper's ShareGPT/arXiv request mixes)",
+        "config": {"workload": DESCR[args.workload], "name": args.workload, "seed": args.seed,
+                   "num_tokens": b.num_tokens, "num_reqs": b.num_reqs,
+                   "chunk_tokens": int(b.q_len[b.q_len > 1].sum()),
+                   "decode_reqs": int((b.q_len == 1).sum())},
+        "tokens_per_s": round(b.num_tokens / (ms_per_step / 1e3), 1),
+        "attention_us": round(attn_s * 1e6, 2), "kv_append_us": round(app_s * 1e6, 2),
+        "plan_us": round(statistics.mean(plan_s) * 1e6, 2),
+        "roofline": roofline,
+    }
+    res.update(extra)
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on this host")
+        res["cpu_baseline"] = cpu_baseline(b)
+    print(json.dumps(res), flush=True)
+
+
+def sweep_rows(name):
+    """(chunk, prefix) rows of the latency-vs-chunk table of a workload; chunk 0 is
+    the pure-decode row (Eq. 3)."""
+    if name == "tiny":
+        return [(c, 192) for c in (0, 16, 32, 64, 128)]
+    if name == "l8b":
+        return [(c, 2048) for c in (0, 128, 256, 512, 1024, 2048)]
+    if name == "l8b_sweep":
+        return [(0, 0)] + [(c, u) for u in (0, 2048, 6144) for c in (128, 256, 512, 1024, 2048)]
+    if name == "multi":
+        return [(0, None)] + [(c, None) for c in (128, 256, 512, 1024)]
+    if name == "l70b":
+        return [(c, 32768) for c in (0, 128, 256, 512, 1024, 2048)]
+    raise KeyError(name)
+
+
+def main_sweep(args):
+    import torch
+    from paper_2606_05933_amd import workload
+    from paper_2606_05933_amd.device import DeviceBatch
+    torch.cuda.set_device(0)
+    flush = Flusher()
+    names = args.sweep_workloads.split(",") if args.sweep_workloads else list(workload.WORKLOADS)
+    done = set()
+    if os.path.exists(args.sweep):
+        for line in open(args.sweep):
+            r = json.loads(line)
+            done.add((r["workload"], r["chunk"], r["prefix"]))
+    out = open(args.sweep, "a")
+    for name in names:
+        for chunk, prefix in sweep_rows(name):
+            if (name, chunk, prefix) in done:
+                continue
+            b = workload.make_workload(name, seed=args.seed, chunk=chunk, prefix=prefix)
+            db = DeviceBatch(b)
+            db.step()
+            torch.cuda.synchronize()
+            n = args.steps
+            app = time_kernel_events(db.kv_append, n, flush) * 1e6
+            attn = time_kernel_events(db.attention, n, flush) * 1e6
+            warm = time_kernel_events(db.attention, n) * 1e6
+            tp = time.perf_counter()
+            for _ in range(n):
+                db.replan_host()
+            plan = (time.perf_counter() - tp) / n * 1e6
+            segs = {}
+            for label, keep in (("decode", b.q_len == 1), ("chunk", b.q_len > 1)):
+                if keep.any() and not keep.all():
+                    sb = DeviceBatch(workload.sub_batch(b, keep))
+                    sb.step()
+                    torch.cuda.synchronize()
+                    segs[label] = segment_stats(sb, n, flush)
+                    del sb
+            info = db.info
+            step_us = plan + app + attn
+            row = {"workload": name, "chunk": chunk, "prefix": prefix, "seed": args.seed,
+                   "scene": info.scene, "tokens": b.num_tokens,
+                   "attention_us": round(attn, 2), "attention_warm_us": round(warm, 2),
+                   "kv_append_us": round(app, 2), "plan_us": round(plan, 2),
+                   "step_us": round(step_us, 2),
+                   "tokens_per_s": round(b.num_tokens / step_us * 1e6, 1),
+                   "hbm_GBps": round((info.decode_bytes + info.chunk_bytes) / attn / 1e3, 1),
+                   "mfma_TFLOPs": round(info.chunk_flops / attn / 1e6, 1),
+                   "decode_bytes": info.decode_bytes, "chunk_flops": info.chunk_flops,
+                   "x": list(info.x), "segments": segs,
+                   "items": info.num_items}
+            out.write(json.dumps(row) + "\n")
+            out.flush()
+            log(f"[sweep] {name} c={chunk} u={prefix}: attention {attn:.1f} us "
+                f"(warm {warm:.1f}), step {step_us:.1f} us, segs "
+                + ", ".join(f"{k} {v['us']} us" for k, v in segs.items()))
+            del db
+            torch.cuda.empty_cache()
+
+
+def main_copy_probe(args):
+    import torch
+    torch.cuda.set_device(0)
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+    dst = torch.empty_like(src)
+    for _ in range(args.steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": src.numel() * 4, "launches": args.steps}), flush=True)
+
+
+def main_only_attention(args):
+    import torch
+    from paper_2606_05933_amd import workload
+    from paper_2606_05933_amd.device import DeviceBatch
+    torch.cuda.set_device(0)
+    b = workload.make_workload(args.workload, seed=args.seed, chunk=args.chunk, prefix=args.prefix)
+    if args.scene == "decode":
+        b = workload.sub_batch(b, b.q_len == 1)
+    elif args.scene == "prefill":
+        b = workload.sub_batch(b, b.q_len > 1)
+    db = DeviceBatch(b)
+    db.kv_append()
+    torch.cuda.synchronize()
+    us = time_kernel_events(db.attention, args.steps) * 1e6
+    info = db.info
+    print(json.dumps({"workload": args.workload, "scene": args.scene, "attention_us": round(us, 2),
+                      "algorithmic_bytes": info.decode_bytes + info.chunk_bytes,
+                      "chunk_flops": info.chunk_flops, "launches": args.steps}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__,
+                                 formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="l8b")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--chunk", type=int, default=None)
+    ap.add_argument("--prefix", type=int, default=None)
+    ap.add_argument("--scene", choices=["mixed", "decode", "prefill"], default="mixed")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--quick", action="store_true", help="skip the cold and per-segment timings")
+    ap.add_argument("--sweep", metavar="OUT", default=None)
+    ap.add_argument("--sweep-workloads", default=None)
+    ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--only-attention", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU: this attention path has no multi-GPU mode "
+              "(head-parallel sharding needs no exchange inside attention); run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.sweep:
+        main_sweep(args)
+    elif args.copy_probe:
+        main_copy_probe(args)
+    elif args.only_attention:
+        main_only_attention(args)
+    else:
+        main_bench(args)
+
+
+if __name__ == "__main__":
+    main()

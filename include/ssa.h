@@ -65,7 +65,7 @@ enum {
   SSA_ERR_WORKSPACE = -8,     /* workspace NULL or smaller than the plan requires */
   SSA_ERR_PLAN_MISMATCH = -9, /* plan_host is not a plan of this shape (magic/hash) */
   SSA_ERR_HIP = -10,          /* a HIP launch failed */
-  SSA_ERR_SCALE = -11,        /* softmax_scale not finite */
+  SSA_ERR_SCALE = -11,        /* softmax_scale negative or not finite */
   SSA_ERR_TUNING = -12        /* a tuning field out of range */
 };
 
@@ -80,7 +80,7 @@ typedef struct ssa_shape {
   int32_t page_size;         /* P: 16 */
   int32_t num_pages;         /* pages in each pool */
   int32_t max_pages_per_req; /* row stride of block_table */
-  float softmax_scale;       /* multiplies <q, k> before the softmax (1/sqrt(D) usually) */
+  float softmax_scale;       /* >= 0; multiplies <q, k> before the softmax (1/sqrt(D) usually) */
 } ssa_shape;
 
 /*
@@ -88,7 +88,7 @@ typedef struct ssa_shape {
  * defaults).  Zero in a field selects its default.  Results do not depend on
  * them beyond floating-point summation order.
  *   chunk_tile_cols  columns (token x q-head-in-group pairs) per chunk work
- *                    item: 64, 128 or 256 (default 256)
+ *                    item: 32, 64 or 128 (default 128)
  *   chunk_split_keys if > 0, a chunk tile's key range is cut into pieces of this
  *                    many keys (multiple of 32); default: chosen by the planner
  *   decode_split_keys keys per decode work item (multiple of 32); default:

@@ -78,6 +78,22 @@ def kv_append(hkv, d, page, q_len, ctx_len, block_table, k_new, v_new, k_cache, 
     return kc, vc
 
 
+def kv_append_inplace(hkv, d, page, q_len, ctx_len, block_table, k_new, v_new, k_cache,
+                      v_cache, lib=None):
+    """The same append, written into the given C-contiguous uint16 pools."""
+    lib = _load(lib)
+    for a in (k_cache, v_cache):
+        if a.dtype != np.uint16 or not a.flags.c_contiguous:
+            raise ValueError("pools must be C-contiguous uint16 arrays")
+    ql, pql = _c(q_len, np.int32)
+    cl, pcl = _c(ctx_len, np.int32)
+    bt, pbt = _c(block_table, np.int32)
+    kn, pkn = _c(k_new, np.uint16)
+    vn, pvn = _c(v_new, np.uint16)
+    lib.oracle_kv_append(hkv, d, page, ql.shape[0], pql, pcl, pbt, bt.shape[1], pkn, pvn,
+                         k_cache.ctypes.data, v_cache.ctypes.data)
+
+
 def attention(hq, hkv, d, page, scale, q_len, ctx_len, block_table, q, k_cache, v_cache,
               threads: int = 0, lib=None):
     """fp64 output [T, Hq, D] and the number of threads used."""

@@ -5,8 +5,9 @@
 // the plan (longest first).  Two kinds of item share the launch:
 //
 //  * chunk tile (prefill rows, c_i > 1; Sec. 2.1 chunked prefill, Tab. 1 x1/x2):
-//    256 columns = (token, q head of the kv group) pairs of one request and kv
-//    head; each of the 4 waves owns 64 columns as four 16-wide MFMA N tiles.
+//    128 columns = (token, q head of the kv group) pairs of one request and kv
+//    head; each of the 4 waves owns 32 columns as two 16-wide MFMA N tiles, so
+//    that a wave fits in 256 registers and two workgroups share a CU.
 //    Key blocks of 32 keys (two 16-slot pages) are staged through LDS, double
 //    buffered, and shared by the 4 waves.  S^T = K Q^T and O^T += V^T P run on
 //    v_mfma_f32_16x16x32_bf16 with fp32 accumulation; softmax is online, in
@@ -53,7 +54,17 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
+// Block-table and plan reads go through the constant address space: the
+// kernels never write them, and wave-uniform reads then become scalar loads,
+// which are not ordered with the vector loads of K/V pages.
+typedef const __attribute__((address_space(4))) int32_t cint32;
+
 constexpr float kLog2e = 1.4426950408889634f;
+// The running maximum of a column is raised only when a block's logit exceeds
+// it by more than this (base 2): probabilities then stay below 2^8, and the
+// O accumulators are rescaled rarely.  The final normalisation uses the same
+// reference, so the result does not depend on it.
+constexpr float kRescaleThreshold = 8.0f;
 constexpr float kNegInf = -__builtin_inff();
 
 template <int D>
@@ -131,31 +142,48 @@ __device__ __forceinline__ float wave_sum_cols(float x) {
   return x;
 }
 
-// Online-softmax step for one 16-column tile and one 32-key block.  sv holds the
-// lane's 8 logits (base-2 scaled, masked ones -inf); on return it holds the
-// unnormalised probabilities relative to the running maximum.
-template <int MT>
-__device__ __forceinline__ void softmax_step(float (&sv)[8], float& m_run, float& l_run,
-                                             f32x4 (&o)[MT]) {
-  float mx = sv[0];
+// Online-softmax step for one 16-column tile and one 32-key block.
+//   s      the lane's 8 raw logits <q, k> (keys 8g .. 8g+7 of the block)
+//   c      softmax_scale * log2(e) >= 0: probabilities are exp2(c*s - m)
+//   MASKED whether some keys of the block are invisible to some column; then
+//          bit e of `valid` says whether key e is visible to this lane's column
+// m_run is the running reference in base-2 units.  It moves only when the
+// block's maximum exceeds it by more than kRescaleThreshold (or while it is
+// still -inf); the O accumulators and l_run are rescaled only then, in a
+// wave-uniform branch.  Returns P in bf16 (the PV operand); l_run accumulates
+// the fp32 probabilities.
+template <int MT, bool MASKED>
+__device__ __forceinline__ bf16x8 softmax_step(const float (&s)[8], unsigned valid, float c,
+                                               float& m_run, float& l_run, f32x4 (&o)[MT]) {
+  float mr;
+  if (MASKED) {
+    mr = kNegInf;
 #pragma unroll
-  for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
-  mx = wave_max_cols(mx);
-  const float m_new = fmaxf(m_run, mx);
-  const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-  const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-  m_run = m_new;
-  float sum = 0.f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    sv[e] = __builtin_amdgcn_exp2f(sv[e] - m_use);
-    sum += sv[e];
+    for (int e = 0; e < 8; ++e) mr = fmaxf(mr, ((valid >> e) & 1) ? s[e] : kNegInf);
+  } else {
+    mr = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
   }
-  l_run = l_run * alpha + sum;
-  if (alpha != 1.f) {
+  mr = wave_max_cols(mr);
+  const float mx = (mr == kNegInf) ? kNegInf : mr * c;
+  const bool raise = mx > m_run + kRescaleThreshold;  // false while mx is -inf
+  if (__builtin_amdgcn_ballot_w64(raise)) {
+    const float m_new = raise ? mx : m_run;
+    const float alpha = (m_run == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+    l_run *= alpha;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) o[mt] *= alpha;
+    m_run = m_new;
   }
+  const float nm = (m_run == kNegInf) ? 0.f : -m_run;
+  float p[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, nm));
+    if (MASKED) p[e] = ((valid >> e) & 1) ? p[e] : 0.f;
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) l_run += p[e];
+  return pack8(p);
 }
 
 __device__ __forceinline__ void store_bf16x4(uint16_t* dst, float a, float b, float c, float d) {
@@ -177,6 +205,20 @@ __device__ __forceinline__ void col_target(const WorkItem& it, const ReqEntry& r
   }
 }
 
+// Partial records cross workgroups (and XCDs, whose L2s are not coherent with
+// each other).  They are written with device-scope stores, which write through
+// to the device coherence point, and read back with device-scope loads, which
+// do not hit a stale L2 copy; the ticket is a device-scope atomic.  This needs
+// no L2 write-back or invalidation.
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// s_waitcnt vmcnt(0): this wave's stores have completed at their scope.
+__device__ __forceinline__ void wait_vm_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Last arriver of a merge group: combine the split records in split order.
 template <int D>
 __device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
@@ -189,15 +231,17 @@ __device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntr
     const int col = idx / (D / 4);
     const int d0 = (idx % (D / 4)) * 4;
     float M = kNegInf;
-    for (int s = 0; s < grp.nsplit; ++s) M = fmaxf(M, base[s * rec + col]);
+    for (int s = 0; s < grp.nsplit; ++s) M = fmaxf(M, ld_dev(base + s * rec + col));
     float L = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < grp.nsplit; ++s) {
       const float* r = base + s * rec;
-      const float w = __builtin_amdgcn_exp2f(r[col] - M);
-      L += w * r[C + col];
-      const f32x4 o = *reinterpret_cast<const f32x4*>(r + 2 * C + (int64_t)col * D + d0);
-      acc += w * o;
+      const float ms = ld_dev(r + col);
+      const float w = (ms == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(ms - M);
+      L += w * ld_dev(r + C + col);
+      const float* o = r + 2 * C + (int64_t)col * D + d0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) acc[k] += w * ld_dev(o + k);
     }
     const float inv = 1.f / L;
     int row, head;
@@ -207,24 +251,24 @@ __device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntr
   }
 }
 
-// After this workgroup wrote its partial record: take a ticket; the last one
-// merges.  Release/acquire at agent scope orders the records across XCDs.
+// After this workgroup wrote its partial record (device-scope stores): wait for
+// the stores, take a ticket; the last of the group's items merges and resets
+// the ticket for the next launch.
 template <int D>
 __device__ void finish_split(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq) {
   __shared__ int s_last;
   const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
   const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + hdr->off_groups)[it.group];
   int* tickets = reinterpret_cast<int*>(a.ws);
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  wait_vm_stores();
   __syncthreads();
   if (threadIdx.x == 0) {
-    const int prev = __hip_atomic_fetch_add(&tickets[it.group], 1, __ATOMIC_ACQ_REL,
+    const int prev = __hip_atomic_fetch_add(&tickets[it.group], 1, __ATOMIC_RELAXED,
                                             __HIP_MEMORY_SCOPE_AGENT);
     s_last = (prev == grp.nsplit - 1);
   }
   __syncthreads();
   if (!s_last) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   merge_group<D>(a, it, rq, grp);
   if (threadIdx.x == 0)
     __hip_atomic_store(&tickets[it.group], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -236,15 +280,16 @@ template <int D>
 __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
                            char* lds) {
   using C = Cfg<D>;
-  constexpr int KK = C::KK, MT = C::MT, NT = 4;
+  constexpr int KK = C::KK, MT = C::MT, NT = kChunkWaveCols / 16;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
   const int G = a.G;
   const int u = rq.ctx_len;
   const int nvalid = rq.ctx_len + rq.q_len;
-  const int32_t* bt = a.bt + (size_t)it.req * a.maxp;
+  cint32* bt = (cint32*)a.bt + (size_t)it.req * a.maxp;
   const size_t page_stride = (size_t)a.hkv * 16 * D;
-  const size_t head_off = (size_t)it.kvh * 16 * D;
+  const uint16_t* kbase = a.kc + (size_t)it.kvh * 16 * D;
+  const uint16_t* vbase = a.vc + (size_t)it.kvh * 16 * D;
 
   // this wave's columns: [wc0, wc1)
   const int colend = it.col0 + it.ncols;
@@ -283,100 +328,124 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     for (int mt = 0; mt < MT; ++mt) o[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // cooperative global -> register -> LDS staging of one 32-key block
+  // LDS read addresses (bytes from a stage's base).  A row r16 of key half h
+  // is key 8*(r16/4) + 4h + r16%4; the XOR swizzle of its 16-byte chunks does
+  // not depend on h, so half 1 sits 4 rows after half 0.
+  const int key0 = 8 * (r16 >> 2) + (r16 & 3);
+  const int sw = kswz(key0);
+  int kaddr[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) kaddr[kk] = key0 * C::K_ROW + (((kk * 4 + g) ^ sw) << 4);
+  const int vaddr = C::K_STAGE + r16 * C::V_ROW + g * 16;
+
+  // Cooperative staging of one 32-key block: each thread moves LOADS 16-byte
+  // chunks of K and of V.  The two page indices of a block are wave-uniform
+  // scalar loads; a page past the request's last one is read from the first
+  // page instead (in bounds): its keys are beyond every position and its
+  // values are zeroed at store time together with the unwritten tail slots.
+  int kgo[C::LOADS], vgo[C::LOADS], kso[C::LOADS], vso[C::LOADS], vkb[C::LOADS];
+  bool second[C::LOADS];
+#pragma unroll
+  for (int r = 0; r < C::LOADS; ++r) {
+    const int ci = tid + r * kThreads;
+    const int page = __builtin_amdgcn_readfirstlane(ci / (2 * D));
+    const int within = ci % (2 * D);
+    const int slot = within / C::CPR, c = within % C::CPR;
+    const int key = page * 16 + slot;
+    kgo[r] = slot * D + c * 8;
+    kso[r] = key * C::K_ROW + ((c ^ kswz(key)) << 4);
+    const int d = within >> 1, half = within & 1;
+    vgo[r] = d * 16 + half * 8;
+    vso[r] = C::K_STAGE + d * C::V_ROW + (page * 2 + half) * 16;
+    vkb[r] = page * 16 + half * 8;
+    second[r] = page != 0;
+  }
   u32x4 kreg[C::LOADS], vreg[C::LOADS];
+  int vkeep[C::LOADS];
   auto gload = [&](int kb) {
+    const int lp0 = kb >> 4;
+    const int pg0 = bt[lp0];
+    const int pg1 = (lp0 + 1 < rq.n_pages) ? bt[lp0 + 1] : pg0;
 #pragma unroll
     for (int r = 0; r < C::LOADS; ++r) {
-      const int ci = tid + r * kThreads;
-      const int page = ci / (2 * D);
-      const int within = ci % (2 * D);
-      const int lp = kb / 16 + page;
-      if (lp < rq.n_pages) {
-        const size_t pb = (size_t)bt[lp] * page_stride + head_off;
-        const int slot = within / C::CPR, c = within % C::CPR;
-        kreg[r] = ld16(a.kc + pb + slot * D + c * 8);
-        const int d = within >> 1, half = within & 1;
-        u32x4 v = ld16(a.vc + pb + d * 16 + half * 8);
-        const int kfirst = kb + page * 16 + half * 8;
-        if (kfirst + 8 > nvalid) v = keep_first(v, nvalid - kfirst);
-        vreg[r] = v;
-      } else {
-        kreg[r] = u32x4{0, 0, 0, 0};
-        vreg[r] = u32x4{0, 0, 0, 0};
-      }
+      const size_t pb = (size_t)(second[r] ? pg1 : pg0) * page_stride;
+      kreg[r] = ld16(kbase + pb + kgo[r]);
+      vreg[r] = ld16(vbase + pb + vgo[r]);
+      vkeep[r] = nvalid - (kb + vkb[r]);
     }
   };
   auto lstore = [&](char* stage) {
 #pragma unroll
     for (int r = 0; r < C::LOADS; ++r) {
-      const int ci = tid + r * kThreads;
-      const int page = ci / (2 * D);
-      const int within = ci % (2 * D);
-      const int key = page * 16 + within / C::CPR, c = within % C::CPR;
-      st16(stage + key * C::K_ROW + ((c ^ kswz(key)) << 4), kreg[r]);
-      const int d = within >> 1, half = within & 1;
-      st16(stage + C::K_STAGE + d * C::V_ROW + (page * 2 + half) * 16, vreg[r]);
+      st16(stage + kso[r], kreg[r]);
+      st16(stage + vso[r], vkeep[r] >= 8 ? vreg[r] : keep_first(vreg[r], vkeep[r]));
     }
   };
   auto compute = [&](const char* stage, int kb) {
     if (kb >= wkend) return;
     bf16x8 kop[2][KK];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int key = 8 * (r16 >> 2) + 4 * h + (r16 & 3);
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const int c = kk * 4 + g;
-        kop[h][kk] = as_bf16x8(ld16(stage + key * C::K_ROW + ((c ^ kswz(key)) << 4)));
-      }
+    for (int kk = 0; kk < KK; ++kk) {
+      kop[0][kk] = as_bf16x8(ld16(stage + kaddr[kk]));
+      kop[1][kk] = as_bf16x8(ld16(stage + kaddr[kk] + 4 * C::K_ROW));
     }
-    const bool need_mask = kb + 31 > wpmin;
-    bf16x8 pop[NT];
+    f32x4 s0[NT], s1[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+      s0[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      s1[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        s0 = mfma(kop[0][kk], qop[nt][kk], s0);
-        s1 = mfma(kop[1][kk], qop[nt][kk], s1);
-      }
-      float sv[8];
+    for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        sv[jj] = s0[jj] * a.scale_log2;
-        sv[4 + jj] = s1[jj] * a.scale_log2;
+      for (int nt = 0; nt < NT; ++nt) {
+        s0[nt] = mfma(kop[0][kk], qop[nt][kk], s0[nt]);
+        s1[nt] = mfma(kop[1][kk], qop[nt][kk], s1[nt]);
       }
+    bf16x8 pop[NT];
+    const bool need_mask = kb + 31 > wpmin;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const float sv[8] = {s0[nt][0], s0[nt][1], s0[nt][2], s0[nt][3],
+                           s1[nt][0], s1[nt][1], s1[nt][2], s1[nt][3]};
       if (need_mask) {
-        const int kg = kb + 8 * g;
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (kg + e > pos[nt]) sv[e] = kNegInf;
+        const int lim = pos[nt] - (kb + 8 * g);  // key e visible iff e <= lim
+        const unsigned valid = lim < 0 ? 0u : (lim >= 7 ? 0xFFu : (2u << lim) - 1u);
+        pop[nt] = softmax_step<MT, true>(sv, valid, a.scale_log2, m_run[nt], l_run[nt], o[nt]);
+      } else {
+        pop[nt] = softmax_step<MT, false>(sv, 0xFFu, a.scale_log2, m_run[nt], l_run[nt], o[nt]);
       }
-      softmax_step<MT>(sv, m_run[nt], l_run[nt], o[nt]);
-      pop[nt] = pack8(sv);
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const bf16x8 vop =
-          as_bf16x8(ld16(stage + C::K_STAGE + (mt * 16 + r16) * C::V_ROW + g * 16));
+      const bf16x8 vop = as_bf16x8(ld16(stage + vaddr + mt * 16 * C::V_ROW));
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) o[nt][mt] = mfma(vop, pop[nt], o[nt][mt]);
     }
   };
 
+  // Two LDS stages, loop unrolled by two so that stage offsets are constants.
+  // The next block's global loads are issued before the current block is
+  // computed and stored to the other stage after it; they are unconditional
+  // (the last block is loaded again at the end) so that the loop body is
+  // straight code with exact memory-counter waits.
   const int nb = (it.key1 - it.key0 + 31) / 32;
+  char* st0 = lds;
+  char* st1 = lds + C::STAGE;
   if (nb > 0) {
     gload(it.key0);
-    lstore(lds);
+    lstore(st0);
   }
   __syncthreads();
-  for (int b = 0; b < nb; ++b) {
-    const int kb = it.key0 + b * 32;
-    char* cur = lds + (b & 1) * C::STAGE;
-    if (b + 1 < nb) gload(kb + 32);
-    compute(cur, kb);
-    if (b + 1 < nb) lstore(lds + ((b + 1) & 1) * C::STAGE);
+  for (int b = 0; b < nb; b += 2) {
+    gload(it.key0 + min(b + 1, nb - 1) * 32);
+    compute(st0, it.key0 + b * 32);
+    lstore(st1);
+    __syncthreads();
+    if (b + 1 >= nb) break;
+    gload(it.key0 + min(b + 2, nb - 1) * 32);
+    compute(st1, it.key0 + (b + 1) * 32);
+    lstore(st0);
     __syncthreads();
   }
 
@@ -409,12 +478,14 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
       if (col >= colend) continue;
       const int cl = col - it.col0;
       if (g == 0) {
-        rec[cl] = m_run[nt];
-        rec[Cn + cl] = l_run[nt];
+        st_dev(rec + cl, m_run[nt]);
+        st_dev(rec + Cn + cl, l_run[nt]);
       }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
-        *reinterpret_cast<f32x4*>(rec + 2 * Cn + (int64_t)cl * D + mt * 16 + 4 * g) = o[nt][mt];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          st_dev(rec + 2 * Cn + (int64_t)cl * D + mt * 16 + 4 * g + jj, o[nt][mt][jj]);
     }
     finish_split<D>(a, it, rq);
   }
@@ -425,7 +496,7 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
 template <int D>
 struct DecodeRegs {
   bf16x8 k[2][Cfg<D>::KK];
-  bf16x8 v[Cfg<D>::MT];
+  u32x4 v[Cfg<D>::MT];
 };
 
 template <int D>
@@ -436,7 +507,7 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, r16 = lane & 15;
   const int G = a.G;
-  const int32_t* bt = a.bt + (size_t)it.req * a.maxp;
+  cint32* bt = (cint32*)a.bt + (size_t)it.req * a.maxp;
   const size_t page_stride = (size_t)a.hkv * 16 * D;
   const size_t head_off = (size_t)it.kvh * 16 * D;
   const int key1 = it.key1;
@@ -455,75 +526,68 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) o[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // The two page indices of a block are wave-uniform scalar loads (no
+  // vector-memory wait before the K/V loads).  A page past the request's last
+  // one is read from the first page instead (in bounds); keys from it are at or
+  // beyond key1, so their logits are masked and their values zeroed in compute.
   auto load = [&](DecodeRegs<D>& R, int kb) {
-    const bool tail = kb + 32 > key1;
+    const int lp0 = kb >> 4;
+    const int pg0 = bt[lp0];
+    const int pg1 = (lp0 + 1 < rq.n_pages) ? bt[lp0 + 1] : pg0;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int key = 8 * (r16 >> 2) + 4 * h + (r16 & 3);
-      const int lp = kb / 16 + (key >> 4);
-      if (!tail || lp < rq.n_pages) {
-        const uint16_t* src = a.kc + (size_t)bt[lp] * page_stride + head_off + (key & 15) * D + g * 8;
+      const uint16_t* src = a.kc + (size_t)((key >> 4) ? pg1 : pg0) * page_stride + head_off +
+                            (key & 15) * D + g * 8;
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) R.k[h][kk] = as_bf16x8(ld16(src + kk * 32));
-      } else {
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) R.k[h][kk] = as_bf16x8(u32x4{0, 0, 0, 0});
-      }
+      for (int kk = 0; kk < KK; ++kk) R.k[h][kk] = as_bf16x8(ld16(src + kk * 32));
     }
-    const int lp = kb / 16 + (g >> 1);
-    if (!tail || lp < rq.n_pages) {
-      const uint16_t* src = a.vc + (size_t)bt[lp] * page_stride + head_off + r16 * 16 + (g & 1) * 8;
-      const int keep = key1 - (kb + 8 * g);
+    const uint16_t* src = a.vc + (size_t)((g >> 1) ? pg1 : pg0) * page_stride + head_off +
+                          r16 * 16 + (g & 1) * 8;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        u32x4 v = ld16(src + mt * 16 * 16);
-        if (tail && keep < 8) v = keep_first(v, keep < 0 ? 0 : keep);
-        R.v[mt] = as_bf16x8(v);
-      }
-    } else {
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) R.v[mt] = as_bf16x8(u32x4{0, 0, 0, 0});
-    }
+    for (int mt = 0; mt < MT; ++mt) R.v[mt] = ld16(src + mt * 16 * 16);
   };
-  auto compute = [&](const DecodeRegs<D>& R, int kb) {
+  auto compute = [&](DecodeRegs<D>& R, int kb) {
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       s0 = mfma(R.k[0][kk], qop[kk], s0);
       s1 = mfma(R.k[1][kk], qop[kk], s1);
     }
-    float sv[8];
-#pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      sv[jj] = s0[jj] * a.scale_log2;
-      sv[4 + jj] = s1[jj] * a.scale_log2;
-    }
+    const float sv[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+    bf16x8 pop;
     if (kb + 32 > key1) {
-      const int kg = kb + 8 * g;
+      const int lim = key1 - (kb + 8 * g);  // key e of the lane group valid iff e < lim
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (kg + e >= key1) sv[e] = kNegInf;
+      for (int mt = 0; mt < MT; ++mt) R.v[mt] = keep_first(R.v[mt], lim);
+      const unsigned valid = lim <= 0 ? 0u : (lim >= 8 ? 0xFFu : (1u << lim) - 1u);
+      pop = softmax_step<MT, true>(sv, valid, a.scale_log2, m_run, l_run, o);
+    } else {
+      pop = softmax_step<MT, false>(sv, 0xFFu, a.scale_log2, m_run, l_run, o);
     }
-    softmax_step<MT>(sv, m_run, l_run, o);
-    const bf16x8 pop = pack8(sv);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) o[mt] = mfma(R.v[mt], pop, o[mt]);
+    for (int mt = 0; mt < MT; ++mt) o[mt] = mfma(as_bf16x8(R.v[mt]), pop, o[mt]);
   };
 
+  // Wave w takes blocks w, w+4, ...  The next block's loads are issued before
+  // the current block is computed; they are unconditional (clamped to the last
+  // block, an L2 hit, once the wave runs out) so that the code stays straight
+  // and the memory-counter waits only cover the block being computed.
   const int nb = (key1 - it.key0 + 31) / 32;
   DecodeRegs<D> R0, R1;
-  int b = w;
-  if (b < nb) load(R0, it.key0 + b * 32);
-  while (b < nb) {
-    int bn = b + kWaves;
-    if (bn < nb) load(R1, it.key0 + bn * 32);
-    compute(R0, it.key0 + b * 32);
-    b = bn;
-    if (b >= nb) break;
-    bn = b + kWaves;
-    if (bn < nb) load(R0, it.key0 + bn * 32);
-    compute(R1, it.key0 + b * 32);
-    b = bn;
+  int b = __builtin_amdgcn_readfirstlane(w);
+  if (b < nb) {
+    load(R0, it.key0 + b * 32);
+    for (;;) {
+      load(R1, it.key0 + min(b + kWaves, nb - 1) * 32);
+      compute(R0, it.key0 + b * 32);
+      b += kWaves;
+      if (b >= nb) break;
+      load(R0, it.key0 + min(b + kWaves, nb - 1) * 32);
+      compute(R1, it.key0 + b * 32);
+      b += kWaves;
+      if (b >= nb) break;
+    }
   }
   l_run = wave_sum_cols(l_run);
 
@@ -565,11 +629,11 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
     }
     if (rec) {
       if (d0 == 0) {
-        rec[col] = M;
-        rec[G + col] = L;
+        st_dev(rec + col, M);
+        st_dev(rec + G + col, L);
       }
-      *reinterpret_cast<f32x4*>(rec + 2 * G + (int64_t)col * D + d0) =
-          f32x4{acc[0], acc[1], acc[2], acc[3]};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) st_dev(rec + 2 * G + (int64_t)col * D + d0 + k, acc[k]);
     } else {
       const float inv = 1.f / L;
       store_bf16x4(a.out + ((size_t)rq.q_start * a.hq + it.kvh * G + col) * D + d0,
@@ -580,7 +644,7 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
 }
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void mixed_attention_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kThreads, 2) void mixed_attention_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[Cfg<D>::LDS];
   const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
   if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;

@@ -21,7 +21,7 @@
 namespace ssa {
 namespace {
 
-constexpr int kDefaultTileCols = 256;
+constexpr int kDefaultTileCols = 128;
 constexpr int kDefaultCus = 256;
 constexpr int kMaxLen = 1 << 30;
 // Nominal rates for balancing only (fractions of MI355X peaks): bf16 MFMA per
@@ -32,6 +32,11 @@ constexpr double kHbmRate = 8.0e12 * 0.7;
 // each piece costs a partial record of ncols*(D+2) floats written and read back.
 constexpr int kMinChunkSplitKeys = 1024;
 constexpr int kMaxChunkSplits = 16;
+// Decode key ranges are cut into items of at least kMinDecodeSplitBlocks blocks,
+// aiming at about kDecodeItemsPerCu items per compute unit: enough to balance
+// contexts of different lengths, few enough that merging partials stays cheap.
+constexpr int kMinDecodeSplitBlocks = 128;
+constexpr int kDecodeItemsPerCu = 1;
 
 struct Tuning {
   int tile_cols, chunk_split_keys, decode_split_keys, num_cus;
@@ -44,7 +49,7 @@ int check_shape(const ssa_shape* s) {
     return SSA_ERR_SHAPE;
   if (s->head_dim != 64 && s->head_dim != 128) return SSA_ERR_HEAD_DIM;
   if (s->page_size != SSA_PAGE_SIZE) return SSA_ERR_PAGE_SIZE;
-  if (!std::isfinite(s->softmax_scale)) return SSA_ERR_SCALE;
+  if (!std::isfinite(s->softmax_scale) || s->softmax_scale < 0.f) return SSA_ERR_SCALE;
   if (s->num_pages < 1 || s->max_pages_per_req < 1) return SSA_ERR_PAGES;
   return SSA_OK;
 }
@@ -53,7 +58,7 @@ int resolve_tuning(const ssa_tuning* t, Tuning* out) {
   Tuning r{kDefaultTileCols, 0, 0, kDefaultCus};
   if (t) {
     if (t->chunk_tile_cols) {
-      if (t->chunk_tile_cols != 64 && t->chunk_tile_cols != 128 && t->chunk_tile_cols != 256)
+      if (t->chunk_tile_cols != 32 && t->chunk_tile_cols != 64 && t->chunk_tile_cols != 128)
         return SSA_ERR_TUNING;
       r.tile_cols = t->chunk_tile_cols;
     }
@@ -176,8 +181,8 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
 
   int dec_split = tu.decode_split_keys;
   if (dec_split == 0) {
-    int64_t blocks = (int64_t)std::ceil(decode_blocks / (double)(ncu * 4));
-    blocks = std::max<int64_t>(kWaves, ceil_div(blocks, kWaves) * kWaves);
+    int64_t blocks = (int64_t)std::ceil(decode_blocks / (double)(ncu * kDecodeItemsPerCu));
+    blocks = std::max<int64_t>(kMinDecodeSplitBlocks, ceil_div(blocks, kWaves) * kWaves);
     dec_split = (int)std::min<int64_t>(blocks * kBlockKeys, kMaxLen);
   }
 
@@ -344,7 +349,7 @@ const char* ssa_status_string(int code) {
     case SSA_ERR_WORKSPACE: return "workspace missing or too small";
     case SSA_ERR_PLAN_MISMATCH: return "plan does not belong to this shape";
     case SSA_ERR_HIP: return "HIP launch failed";
-    case SSA_ERR_SCALE: return "softmax_scale is not finite";
+    case SSA_ERR_SCALE: return "softmax_scale is negative or not finite";
     case SSA_ERR_TUNING: return "tuning field out of range";
     default: return "unknown";
   }

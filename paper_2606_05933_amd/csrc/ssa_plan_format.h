@@ -19,7 +19,7 @@ constexpr uint32_t kPlanVersion = 1;
 constexpr int kBlockKeys = 32;  // keys per attention block: two 16-slot pages
 constexpr int kWaves = 4;       // waves per workgroup
 constexpr int kThreads = 256;   // threads per workgroup
-constexpr int kChunkWaveCols = 64;  // columns a wave owns in a chunk tile
+constexpr int kChunkWaveCols = 32;  // columns a wave owns in a chunk tile
 
 enum ItemKind : int32_t { kItemChunk = 0, kItemDecode = 1 };
 

@@ -58,20 +58,36 @@ class DeviceBatch:
             self.tuning = tuning
         b = self.b
         nbytes, ws_bytes = ssa.ssa_plan_size(self.shape, b.q_len, b.ctx_len, self.tuning)
-        self.plan_host = torch.zeros(max(nbytes, 128), dtype=torch.uint8).pin_memory()
+        # two pinned host buffers: the host plans into one while the copy out of
+        # the other may still be queued on the stream
+        self._ring = [torch.zeros(max(nbytes, 128), dtype=torch.uint8).pin_memory()
+                      for _ in range(2)]
+        self._ring_ev = [None, None]
+        self._slot = 0
+        self.plan_host = self._ring[0]
         _, self.info = ssa.ssa_plan(self.shape, b.q_len, b.ctx_len, self.tuning,
                                     out=self.plan_host)
         self.plan_dev = torch.empty_like(self.plan_host, device=self.device)
         self.plan_dev.copy_(self.plan_host, non_blocking=True)
+        self._ring_ev[0] = torch.cuda.Event()
+        self._ring_ev[0].record()
         if not hasattr(self, "workspace") or self.workspace.numel() < ws_bytes:
             self.workspace = torch.zeros(max(ws_bytes, 256), dtype=torch.uint8, device=self.device)
         return self.info
 
     def replan_host(self):
-        """Host planning of the same batch into the pinned buffer (what a serving
+        """Host planning of the same batch into a pinned buffer (what a serving
         loop does every iteration), followed by the async copy to the device."""
-        ssa.ssa_plan(self.shape, self.b.q_len, self.b.ctx_len, self.tuning, out=self.plan_host)
-        self.plan_dev.copy_(self.plan_host, non_blocking=True)
+        self._slot ^= 1
+        buf, ev = self._ring[self._slot], self._ring_ev[self._slot]
+        if ev is not None:
+            ev.synchronize()  # the copy that last read this buffer has run
+        ssa.ssa_plan(self.shape, self.b.q_len, self.b.ctx_len, self.tuning, out=buf)
+        self.plan_host = buf
+        self.plan_dev.copy_(buf, non_blocking=True)
+        if ev is None:
+            ev = self._ring_ev[self._slot] = torch.cuda.Event()
+        ev.record()
 
     def kv_append(self, stream=None):
         ssa.ssa_kv_append(self.shape, self.plan_host, self.plan_dev, self.k_new, self.v_new,

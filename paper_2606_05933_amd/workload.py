@@ -29,9 +29,11 @@ multiplies a masked weight by such a slot, shows up as NaN.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
 import hashlib
 import math
+import os
 
 import numpy as np
 
@@ -46,8 +48,12 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     add never arises.
     """
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+    b = u >> np.uint32(16)
+    b &= np.uint32(1)
+    b += np.uint32(0x7FFF)
+    b += u
+    b >>= np.uint32(16)
+    return b.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -107,13 +113,29 @@ class Batch:
         return h.hexdigest()
 
 
-def _normal_bf16(rng: np.random.Generator, shape, slab: int = 1 << 25) -> np.ndarray:
-    """bf16 bits of fp32 N(0,1) draws, drawn in slabs to bound the fp32 temporaries."""
+_SLAB = 1 << 22
+
+
+def _normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
+    """bf16 bits of fp32 N(0,1) draws.  Slab k of 2^22 values comes from its own
+    PCG64 stream (spawned from ``rng``), so the result does not depend on how
+    many threads fill the slabs."""
     n = int(np.prod(shape))
     out = np.empty(n, dtype=np.uint16)
-    for s in range(0, n, slab):
-        e = min(n, s + slab)
-        out[s:e] = f32_to_bf16_bits(rng.standard_normal(e - s, dtype=np.float32))
+    nslab = (n + _SLAB - 1) // _SLAB
+    seeds = rng.bit_generator.seed_seq.spawn(nslab) if nslab else []
+
+    def fill(k):
+        s, e = k * _SLAB, min(n, (k + 1) * _SLAB)
+        g = np.random.Generator(np.random.PCG64(seeds[k]))
+        out[s:e] = f32_to_bf16_bits(g.standard_normal(e - s, dtype=np.float32))
+
+    if nslab > 1:
+        workers = max(1, min(16, len(os.sched_getaffinity(0))))
+        with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+            list(ex.map(fill, range(nslab)))
+    elif nslab == 1:
+        fill(0)
     return out.reshape(shape)
 
 

@@ -129,7 +129,7 @@ def test_plan_partitions_every_output_key_range(case):
     check_plan_covers_batch(hq, hkv, d, np.array(q_len, np.int32), np.array(ctx_len, np.int32))
 
 
-@pytest.mark.parametrize("tile", [64, 128, 256])
+@pytest.mark.parametrize("tile", [32, 64, 128])
 @pytest.mark.parametrize("csplit", [0, 1024, 4096])
 def test_plan_partitions_under_tuning(tile, csplit):
     q_len = np.array([700, 33, 1, 1], np.int32)
@@ -196,6 +196,7 @@ def plan_rc(shape, q_len, ctx_len, tuning=None, cap=None):
 @pytest.mark.parametrize("mutate,code", [
     (dict(num_q_heads=0), -2), (dict(num_kv_heads=3), -2), (dict(num_q_heads=34, num_kv_heads=2), -2),
     (dict(head_dim=96), -3), (dict(page_size=8), -4), (dict(softmax_scale=float("inf")), -11),
+    (dict(softmax_scale=-0.5), -11),
     (dict(num_pages=0), -6), (dict(max_pages_per_req=0), -6),
 ])
 def test_bad_shape_codes(mutate, code):

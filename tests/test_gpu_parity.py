@@ -100,8 +100,8 @@ def test_llama8b_mixed_full_parity(torch_dev):
     full_parity(workload.make_workload("l8b", seed=0))
 
 
-@pytest.mark.parametrize("tile,csplit,dsplit", [(64, 0, 0), (128, 1024, 256), (256, 512, 128),
-                                                (256, 0, 4096)])
+@pytest.mark.parametrize("tile,csplit,dsplit", [(32, 0, 0), (64, 1024, 256), (128, 512, 128),
+                                                (128, 0, 4096)])
 def test_tuning_variants_match_oracle(torch_dev, tile, csplit, dsplit):
     from paper_2606_05933_amd import ssa
     b = small(32, 8, 128, [(300, 1500), (1, 3000), (1, 100), (45, 0)], seed=11, name="tuned")
