@@ -14,9 +14,14 @@
  * Call sequence for one iteration (all on one stream):
  *   ssa_plan_size   -> sizes of the plan blob and the workspace      (host)
  *   ssa_plan        -> fills the plan blob from (q_len, ctx_len)      (host)
- *   caller copies the plan blob to device memory (same bytes)
  *   ssa_kv_append   -> writes the new K/V rows into their pages      (1 kernel)
  *   ssa_mixed_attention -> outputs of every new token                (1 kernel)
+ *
+ * The kernels read the plan blob through plan_dev: either a device copy of
+ * it, or the host buffer itself when that buffer is pinned, device-mapped host
+ * memory (hipHostMalloc); the blob is small and each workgroup reads one record
+ * of it.  Either way the caller must not change those bytes until the launches
+ * that use them have completed (alternate two buffers between iterations).
  *
  * Conventions shared by every call:
  *   - Every function returns SSA_OK (0) or a negative SSA_ERR_* code.  All
@@ -94,12 +99,21 @@ typedef struct ssa_shape {
  *   decode_split_keys keys per decode work item (multiple of 32); default:
  *                    chosen by the planner
  *   num_cus          compute units the planner balances for (default 256)
+ *   num_xcds         if > 1, die-aware placement: workgroups are taken to be
+ *                    dealt to num_xcds dies round-robin (workgroup b on die
+ *                    b mod num_xcds), and work items that read the same K/V
+ *                    (one request and kv head of a chunk) go to one die
+ *                    (default 1: off; on MI355X it measured no faster)
+ *   mix_order        1 = all chunk items (longest first) before the decode
+ *                    items (default), 2 = the two kinds interleaved
  */
 typedef struct ssa_tuning {
   int32_t chunk_tile_cols;
   int32_t chunk_split_keys;
   int32_t decode_split_keys;
   int32_t num_cus;
+  int32_t num_xcds;
+  int32_t mix_order;
 } ssa_tuning;
 
 /*
@@ -153,7 +167,9 @@ int ssa_plan(const ssa_shape* shape, const int32_t* q_len_host, const int32_t* c
  * is copied bit for bit from k_new/v_new row (q_start_i + j) into page
  * block_table[i][t / P], slot t % P, of k_cache / v_cache.  No other pool
  * byte is written.  plan_host is the plan blob on the host (read for the
- * launch size and checked against shape), plan_dev its device copy.
+ * launch size and checked against shape); plan_dev is the same bytes where the
+ * device can read them (a device copy, or plan_host itself if it is pinned
+ * device-mapped host memory).
  * Errors: NULL, the shape errors, PLAN_MISMATCH, HIP.
  */
 int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* plan_dev,

@@ -86,6 +86,8 @@ struct Cfg {
 struct AttnArgs {
   const uint8_t* plan;
   uint64_t hash;
+  int32_t off_items, off_groups;
+  int64_t ws_partials_off;
   const uint16_t* q;
   const uint16_t* kc;
   const uint16_t* vc;
@@ -126,20 +128,45 @@ __device__ __forceinline__ u32x4 keep_first(u32x4 v, int keep) {
   return r;
 }
 
-// XOR swizzle of the 16-byte chunk index of key row `key` in the LDS K block, so
-// that the 8 rows a ds_read_b128 lane octet touches (keys 8*(r/4)+4h+r%4) fall
-// in distinct bank groups.
-__device__ __forceinline__ int kswz(int key) { return (key & 3) | ((key & 8) >> 1); }
+// XOR swizzle of the 16-byte chunk index of key row `key` in the LDS K block.
+// One ds_read_b128 of a K operand reads the same chunk of 16 rows, keys
+// 8*(r/4) + r%4 (+4 for the second half), r = 0..15; the swizzle sends them to
+// 16 distinct 16-byte bank slots (D = 128: 256-byte rows), and in particular
+// to 8 distinct ones within each lane octet.  It ignores key bit 2, so both key
+// halves share it.  For D = 64 (128-byte rows) it separates each octet.
+template <int D>
+__device__ __forceinline__ int kswz(int key) {
+  if (D == 128) return (key & 3) | ((key >> 1) & 12);
+  return (key & 3) | ((key & 8) >> 1);
+}
 
+// Bit casts go through named scalars: applied directly to an element of a
+// vector value, __builtin_bit_cast has been seen to read element 0.
+__device__ __forceinline__ float as_f32(unsigned u) { return __builtin_bit_cast(float, u); }
+__device__ __forceinline__ unsigned as_u32(float f) { return __builtin_bit_cast(unsigned, f); }
+
+// Reductions over the four 16-lane groups of a wave (the lanes that hold one
+// column of an MFMA output tile), with the gfx950 row-swap permutes.  With
+// both operands holding x, a 16-lane swap returns rows {0,0,2,2} and {1,1,3,3}
+// of x, a 32-lane swap halves {0,0} and {1,1}; combining the two results
+// reduces over row pairs.
 __device__ __forceinline__ float wave_max_cols(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16));
-  x = fmaxf(x, __shfl_xor(x, 32));
-  return x;
+  const unsigned u = as_u32(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const unsigned a0 = a[0], a1 = a[1];
+  const unsigned v = as_u32(fmaxf(as_f32(a0), as_f32(a1)));
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  const unsigned b0 = b[0], b1 = b[1];
+  return fmaxf(as_f32(b0), as_f32(b1));
 }
 __device__ __forceinline__ float wave_sum_cols(float x) {
-  x += __shfl_xor(x, 16);
-  x += __shfl_xor(x, 32);
-  return x;
+  const unsigned u = as_u32(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const unsigned a0 = a[0], a1 = a[1];
+  const unsigned v = as_u32(as_f32(a0) + as_f32(a1));
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  const unsigned b0 = b[0], b1 = b[1];
+  return as_f32(b0) + as_f32(b1);
 }
 
 // Online-softmax step for one 16-column tile and one 32-key block.
@@ -151,7 +178,7 @@ __device__ __forceinline__ float wave_sum_cols(float x) {
 // block's maximum exceeds it by more than kRescaleThreshold (or while it is
 // still -inf); the O accumulators and l_run are rescaled only then, in a
 // wave-uniform branch.  Returns P in bf16 (the PV operand); l_run accumulates
-// the fp32 probabilities.
+// the same rounded values, so the normalisation matches the product.
 template <int MT, bool MASKED>
 __device__ __forceinline__ bf16x8 softmax_step(const float (&s)[8], unsigned valid, float c,
                                                float& m_run, float& l_run, f32x4 (&o)[MT]) {
@@ -181,9 +208,16 @@ __device__ __forceinline__ bf16x8 softmax_step(const float (&s)[8], unsigned val
     p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, nm));
     if (MASKED) p[e] = ((valid >> e) & 1) ? p[e] : 0.f;
   }
+  // l accumulates the bf16-rounded probabilities, the values the PV product uses
+  const bf16x8 pk = pack8(p);
+  const u32x4 w = __builtin_bit_cast(u32x4, pk);
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-  for (int e = 0; e < 8; ++e) l_run += p[e];
-  return pack8(p);
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t pair = w[i];
+    l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pair), one, l_run, false);
+  }
+  return pk;
 }
 
 __device__ __forceinline__ void store_bf16x4(uint16_t* dst, float a, float b, float c, float d) {
@@ -223,8 +257,7 @@ __device__ __forceinline__ void wait_vm_stores() { __builtin_amdgcn_s_waitcnt(0x
 template <int D>
 __device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
                             const MergeGroup& grp) {
-  const float* base = reinterpret_cast<const float*>(
-      a.ws + reinterpret_cast<const PlanHeader*>(a.plan)->ws_partials_off) + grp.ws_off;
+  const float* base = reinterpret_cast<const float*>(a.ws + a.ws_partials_off) + grp.ws_off;
   const int C = grp.ncols;
   const int64_t rec = (int64_t)C * (D + 2);
   for (int idx = threadIdx.x; idx < C * (D / 4); idx += kThreads) {
@@ -257,8 +290,7 @@ __device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntr
 template <int D>
 __device__ void finish_split(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq) {
   __shared__ int s_last;
-  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
-  const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + hdr->off_groups)[it.group];
+  const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + a.off_groups)[it.group];
   int* tickets = reinterpret_cast<int*>(a.ws);
   wait_vm_stores();
   __syncthreads();
@@ -332,7 +364,7 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   // is key 8*(r16/4) + 4h + r16%4; the XOR swizzle of its 16-byte chunks does
   // not depend on h, so half 1 sits 4 rows after half 0.
   const int key0 = 8 * (r16 >> 2) + (r16 & 3);
-  const int sw = kswz(key0);
+  const int sw = kswz<D>(key0);
   int kaddr[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) kaddr[kk] = key0 * C::K_ROW + (((kk * 4 + g) ^ sw) << 4);
@@ -353,8 +385,10 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     const int slot = within / C::CPR, c = within % C::CPR;
     const int key = page * 16 + slot;
     kgo[r] = slot * D + c * 8;
-    kso[r] = key * C::K_ROW + ((c ^ kswz(key)) << 4);
-    const int d = within >> 1, half = within & 1;
+    kso[r] = key * C::K_ROW + ((c ^ kswz<D>(key)) << 4);
+    // value chunks: consecutive threads take consecutive rows d, so that the
+    // LDS writes (row stride 80 bytes) fall in distinct bank slots
+    const int d = within % D, half = within / D;
     vgo[r] = d * 16 + half * 8;
     vso[r] = C::K_STAGE + d * C::V_ROW + (page * 2 + half) * 16;
     vkb[r] = page * 16 + half * 8;
@@ -467,10 +501,9 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
                      o[nt][mt][2] * inv, o[nt][mt][3] * inv);
     }
   } else {
-    const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
-    const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + hdr->off_groups)[it.group];
+    const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + a.off_groups)[it.group];
     const int Cn = grp.ncols;
-    float* rec = reinterpret_cast<float*>(a.ws + hdr->ws_partials_off) + grp.ws_off +
+    float* rec = reinterpret_cast<float*>(a.ws + a.ws_partials_off) + grp.ws_off +
                  (int64_t)it.split * Cn * (D + 2);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -606,9 +639,8 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
 
   float* rec = nullptr;
   if (it.group >= 0) {
-    const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
-    const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + hdr->off_groups)[it.group];
-    rec = reinterpret_cast<float*>(a.ws + hdr->ws_partials_off) + grp.ws_off +
+    const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + a.off_groups)[it.group];
+    rec = reinterpret_cast<float*>(a.ws + a.ws_partials_off) + grp.ws_off +
           (int64_t)it.split * G * (D + 2);
   }
   for (int idx = tid; idx < G * (D / 4); idx += kThreads) {
@@ -646,10 +678,16 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void mixed_attention_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[Cfg<D>::LDS];
+  // The plan may live in device-mapped host memory: read the header check and
+  // this workgroup's item, which are independent loads, and nothing else.
   const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
+  const WorkItem it = reinterpret_cast<const WorkItem*>(a.plan + a.off_items)[blockIdx.x];
   if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
-  const WorkItem it = reinterpret_cast<const WorkItem*>(a.plan + hdr->off_items)[blockIdx.x];
-  const ReqEntry rq = reinterpret_cast<const ReqEntry*>(a.plan + hdr->off_reqs)[it.req];
+  ReqEntry rq;
+  rq.q_start = it.q_start;
+  rq.ctx_len = it.ctx_len;
+  rq.q_len = it.nvalid - it.ctx_len;
+  rq.n_pages = (it.nvalid + 15) >> 4;
   if (it.kind == kItemChunk)
     chunk_item<D>(a, it, rq, lds);
   else
@@ -660,13 +698,14 @@ __global__ __launch_bounds__(kThreads, 2) void mixed_attention_kernel(AttnArgs a
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint8_t* plan, uint64_t hash,
+                                                             int32_t off_segments,
                                                              const uint16_t* k_new,
                                                              const uint16_t* v_new, uint16_t* kc,
                                                              uint16_t* vc, const int32_t* bt,
                                                              int hkv, int maxp) {
   const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(plan);
+  const AppendSeg sg = reinterpret_cast<const AppendSeg*>(plan + off_segments)[blockIdx.x];
   if (hdr->magic != kPlanMagic || hdr->hash != hash) return;
-  const AppendSeg sg = reinterpret_cast<const AppendSeg*>(plan + hdr->off_segments)[blockIdx.x];
   const int h = blockIdx.y;
   const int slot0 = sg.pos0 % 16;
   const size_t pb = (size_t)bt[(size_t)sg.req * maxp + sg.pos0 / 16] * hkv * 16 * D + (size_t)h * 16 * D;
@@ -715,10 +754,12 @@ int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* pla
   hipStream_t st = static_cast<hipStream_t>(stream);
   const uint8_t* p = static_cast<const uint8_t*>(plan_dev);
   if (h->head_dim == 128)
-    kv_append_kernel<128><<<grid, kThreads, 0, st>>>(p, h->hash, k_new, v_new, k_cache, v_cache,
+    kv_append_kernel<128><<<grid, kThreads, 0, st>>>(p, h->hash, h->off_segments, k_new, v_new,
+                                                     k_cache, v_cache,
                                                      block_table, h->hkv, h->max_pages_per_req);
   else
-    kv_append_kernel<64><<<grid, kThreads, 0, st>>>(p, h->hash, k_new, v_new, k_cache, v_cache,
+    kv_append_kernel<64><<<grid, kThreads, 0, st>>>(p, h->hash, h->off_segments, k_new, v_new,
+                                                    k_cache, v_cache,
                                                     block_table, h->hkv, h->max_pages_per_req);
   return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
 }
@@ -738,6 +779,9 @@ int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const voi
   AttnArgs a;
   a.plan = static_cast<const uint8_t*>(plan_dev);
   a.hash = h->hash;
+  a.off_items = h->off_items;
+  a.off_groups = h->off_groups;
+  a.ws_partials_off = h->ws_partials_off;
   a.q = q;
   a.kc = k_cache;
   a.vc = v_cache;

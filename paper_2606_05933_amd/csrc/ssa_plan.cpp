@@ -38,8 +38,12 @@ constexpr int kMaxChunkSplits = 16;
 constexpr int kMinDecodeSplitBlocks = 128;
 constexpr int kDecodeItemsPerCu = 1;
 
+constexpr int kDefaultXcds = 1;
+constexpr int kOrderChunkFirst = 1;
+constexpr int kOrderInterleave = 2;
+
 struct Tuning {
-  int tile_cols, chunk_split_keys, decode_split_keys, num_cus;
+  int tile_cols, chunk_split_keys, decode_split_keys, num_cus, num_xcds, mix_order;
 };
 
 int check_shape(const ssa_shape* s) {
@@ -55,7 +59,7 @@ int check_shape(const ssa_shape* s) {
 }
 
 int resolve_tuning(const ssa_tuning* t, Tuning* out) {
-  Tuning r{kDefaultTileCols, 0, 0, kDefaultCus};
+  Tuning r{kDefaultTileCols, 0, 0, kDefaultCus, kDefaultXcds, kOrderChunkFirst};
   if (t) {
     if (t->chunk_tile_cols) {
       if (t->chunk_tile_cols != 32 && t->chunk_tile_cols != 64 && t->chunk_tile_cols != 128)
@@ -65,9 +69,13 @@ int resolve_tuning(const ssa_tuning* t, Tuning* out) {
     if (t->chunk_split_keys < 0 || t->chunk_split_keys % kBlockKeys) return SSA_ERR_TUNING;
     if (t->decode_split_keys < 0 || t->decode_split_keys % kBlockKeys) return SSA_ERR_TUNING;
     if (t->num_cus < 0 || t->num_cus > 4096) return SSA_ERR_TUNING;
+    if (t->num_xcds < 0 || t->num_xcds > 64) return SSA_ERR_TUNING;
+    if (t->mix_order < 0 || t->mix_order > 2) return SSA_ERR_TUNING;
     r.chunk_split_keys = t->chunk_split_keys;
     r.decode_split_keys = t->decode_split_keys;
     if (t->num_cus) r.num_cus = t->num_cus;
+    if (t->num_xcds) r.num_xcds = t->num_xcds;
+    if (t->mix_order) r.mix_order = t->mix_order;
   }
   *out = r;
   return SSA_OK;
@@ -92,6 +100,132 @@ struct Plan {
 };
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Coarse log-scale bucket of an item's estimated duration (16 buckets per
+// factor of two): ordering only needs to be approximate.
+constexpr int kTimeBuckets = 1024;
+int time_bucket(double t) {
+  // t in units of 1/1024 ns, as an integer: 16 * floor(log2) + the next 4 bits
+  const double x = t * 1.024e12;
+  const uint64_t v = x < 1.0 ? 1 : (x > 9.0e18 ? (uint64_t)9.0e18 : (uint64_t)x);
+  const int msb = 63 - __builtin_clzll(v);
+  const int frac = msb >= 4 ? (int)((v >> (msb - 4)) & 15) : (int)((v << (4 - msb)) & 15);
+  return std::min(kTimeBuckets - 1, msb * 16 + frac);
+}
+
+// Indices of the items of one kind (kind < 0: all), longest first: a counting
+// sort on the time bucket, stable, hence deterministic.
+void longest_first(const std::vector<WorkItem>& items, const std::vector<uint16_t>& bucket,
+                   int kind, std::vector<uint32_t>* out) {
+  static thread_local std::vector<int> count;
+  count.assign(kTimeBuckets + 1, 0);
+  size_t n = 0;
+  for (size_t k = 0; k < items.size(); ++k)
+    if (kind < 0 || items[k].kind == kind) {
+      count[kTimeBuckets - 1 - bucket[k]]++;
+      ++n;
+    }
+  int acc = 0;
+  for (int b = 0; b <= kTimeBuckets; ++b) {
+    const int c = count[b];
+    count[b] = acc;
+    acc += c;
+  }
+  const size_t base = out->size();
+  out->resize(base + n);
+  for (size_t k = 0; k < items.size(); ++k)
+    if (kind < 0 || items[k].kind == kind) (*out)[base + count[kTimeBuckets - 1 - bucket[k]]++] = (uint32_t)k;
+}
+
+// Chunk and decode index lists of one queue: all chunk items then the decode
+// items, or the two merged in proportion.
+void mix(const std::vector<uint32_t>& a, const std::vector<uint32_t>& b, int order,
+         std::vector<uint32_t>* out) {
+  if (order == kOrderChunkFirst) {
+    out->insert(out->end(), a.begin(), a.end());
+    out->insert(out->end(), b.begin(), b.end());
+    return;
+  }
+  size_t i = 0, j = 0;
+  while (i < a.size() || j < b.size()) {
+    // take from the list that is behind in the fraction of its items emitted
+    const bool take_a =
+        j >= b.size() || (i < a.size() && (double)i * b.size() <= (double)j * a.size());
+    out->push_back(take_a ? a[i++] : b[j++]);
+  }
+}
+
+// Launch order of the work items (indices into `items`).  The dispatcher hands
+// out workgroups in index order, so long items go first: by default all chunk
+// items, longest first, then the decode items, longest first.  With die-aware
+// placement (num_xcds > 1; workgroup b is taken to run on die b mod X), chunk
+// items that read the same K/V (one request and kv head) go to one die, dies
+// get equal item counts (decode items balance the estimated time), and the
+// dies' queues are interleaved so that position b belongs to die b mod X.
+void order_items(const std::vector<WorkItem>& items, const std::vector<double>& t,
+                 const std::vector<uint16_t>& bucket, const Tuning& tu, int Hkv,
+                 std::vector<uint32_t>* seq) {
+  const size_t N = items.size();
+  seq->clear();
+  seq->reserve(N);
+  std::vector<uint32_t> ch, de;
+  longest_first(items, bucket, kItemChunk, &ch);
+  longest_first(items, bucket, kItemDecode, &de);
+  const int X = tu.num_xcds;
+  if (X > 1 && N > 0) {
+    std::vector<std::vector<uint32_t>> sch(X), sde(X);
+    std::vector<double> load(X, 0.0);
+    std::vector<size_t> cap(X);
+    for (int x = 0; x < X; ++x) cap[x] = N / X + ((size_t)x < N % X ? 1 : 0);
+    // chunk streams (request, kv head) to dies, largest first onto the least loaded
+    std::vector<int64_t> ids;
+    std::vector<double> stime;
+    std::vector<size_t> sid_of(N, 0);
+    for (uint32_t k : ch) {
+      const int64_t sid = (int64_t)items[k].req * Hkv + items[k].kvh;
+      size_t q = 0;
+      while (q < ids.size() && ids[q] != sid) ++q;
+      if (q == ids.size()) {
+        ids.push_back(sid);
+        stime.push_back(0.0);
+      }
+      stime[q] += t[k];
+      sid_of[k] = q;
+    }
+    std::vector<size_t> sorder(ids.size());
+    for (size_t q = 0; q < sorder.size(); ++q) sorder[q] = q;
+    std::stable_sort(sorder.begin(), sorder.end(),
+                     [&](size_t a, size_t b) { return stime[a] > stime[b]; });
+    std::vector<int> sx(ids.size(), 0);
+    for (size_t q : sorder) {
+      int best = 0;
+      for (int x = 1; x < X; ++x)
+        if (load[x] < load[best]) best = x;
+      sx[q] = best;
+      load[best] += stime[q];
+    }
+    for (uint32_t k : ch) sch[sx[sid_of[k]]].push_back(k);
+    bool fits = true;
+    for (int x = 0; x < X; ++x) fits = fits && sch[x].size() <= cap[x];
+    if (fits) {
+      for (uint32_t k : de) {  // longest first onto the least loaded die with room
+        int best = -1;
+        for (int x = 0; x < X; ++x)
+          if (sch[x].size() + sde[x].size() < cap[x] && (best < 0 || load[x] < load[best]))
+            best = x;
+        sde[best].push_back(k);
+        load[best] += t[k];
+      }
+      std::vector<std::vector<uint32_t>> q(X);
+      for (int x = 0; x < X; ++x) mix(sch[x], sde[x], tu.mix_order, &q[x]);
+      for (size_t r = 0; seq->size() < N; ++r)
+        for (int x = 0; x < X; ++x)
+          if (r < q[x].size()) seq->push_back(q[x][r]);
+      return;
+    }
+  }
+  mix(ch, de, tu.mix_order, seq);
+}
 
 int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int32_t n,
           const ssa_tuning* tuning, Plan* p) {
@@ -156,6 +290,7 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
 
   // append segments: runs of new tokens inside one page
   p->segs.clear();
+  p->segs.reserve((size_t)n + (size_t)(T / P) + 1);
   for (int i = 0; i < n; ++i) {
     int64_t pos = ctx_len[i], end = (int64_t)ctx_len[i] + q_len[i], row = p->reqs[i].q_start;
     while (pos < end) {
@@ -186,12 +321,12 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
     dec_split = (int)std::min<int64_t>(blocks * kBlockKeys, kMaxLen);
   }
 
-  struct Est {
-    WorkItem it;
-    double t;
-  };
-  std::vector<Est> est;
+  std::vector<WorkItem> raw;
+  std::vector<double> est_t;
+  raw.reserve(1024);
+  est_t.reserve(1024);
   p->groups.clear();
+  p->groups.reserve(256);
   int64_t ws_floats = 0;
   auto add_group = [&](int nsplit, int ncols) {
     MergeGroup g{nsplit, ncols, ws_floats};
@@ -232,7 +367,8 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
             it.key1 = std::min(kend, (sp + 1) * piece);
             it.group = grp;
             it.split = sp;
-            est.push_back({it, 4.0 * D * (double)tu.tile_cols * (it.key1 - it.key0) / kMfmaRatePerCu});
+            raw.push_back(it);
+            est_t.push_back(4.0 * D * (double)tu.tile_cols * (it.key1 - it.key0) / kMfmaRatePerCu);
           }
         }
       }
@@ -252,15 +388,25 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
           it.key1 = std::min(keys, (sp + 1) * dec_split);
           it.group = grp;
           it.split = sp;
-          est.push_back({it, (double)(it.key1 - it.key0) * D * 4.0 * ncu / kHbmRate});
+          raw.push_back(it);
+          est_t.push_back((double)(it.key1 - it.key0) * D * 4.0 * ncu / kHbmRate);
         }
       }
     }
   }
-  // longest first: the dispatcher hands out workgroups in index order
-  std::stable_sort(est.begin(), est.end(), [](const Est& a, const Est& b) { return a.t > b.t; });
-  p->items.resize(est.size());
-  for (size_t k = 0; k < est.size(); ++k) p->items[k] = est[k].it;
+  std::vector<uint16_t> bucket(raw.size());
+  for (size_t k = 0; k < raw.size(); ++k) bucket[k] = (uint16_t)time_bucket(est_t[k]);
+  std::vector<uint32_t> seq;
+  order_items(raw, est_t, bucket, tu, Hkv, &seq);
+  p->items.resize(raw.size());
+  for (size_t k = 0; k < seq.size(); ++k) {
+    WorkItem it = raw[seq[k]];
+    const ReqEntry& r = p->reqs[it.req];
+    it.q_start = r.q_start;
+    it.ctx_len = r.ctx_len;
+    it.nvalid = r.ctx_len + r.q_len;
+    p->items[k] = it;
+  }
   for (const WorkItem& it : p->items) {
     if (it.kind == kItemChunk) in.num_chunk_items++;
     else in.num_decode_items++;

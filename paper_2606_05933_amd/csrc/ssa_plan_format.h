@@ -54,7 +54,8 @@ struct ReqEntry {
 //     (ncols = G), keys [key0, key1).
 // group < 0: the item writes the final output; otherwise it writes partial
 // record `split` of merge group `group`, and the last of the group's items to
-// finish merges them.
+// finish merges them.  The request fields a workgroup needs are copied into the
+// item, so that a workgroup reads one record of the plan before it starts.
 struct WorkItem {
   int32_t kind;
   int32_t req;
@@ -65,7 +66,9 @@ struct WorkItem {
   int32_t key1;
   int32_t group;
   int32_t split;
-  int32_t reserved[3];
+  int32_t q_start;  // the request's first token row (copied from its ReqEntry)
+  int32_t ctx_len;  // u_i
+  int32_t nvalid;   // u_i + c_i: keys that hold data after the append
 };
 static_assert(sizeof(WorkItem) == 48, "work item size");
 

@@ -1,9 +1,10 @@
 """A batch resident in device memory, with its plan, output and workspace.
 
 Marshalling around the C ABI for tests, the benchmark and the smoke check:
-uploads the arrays of a generated batch once, plans on the host, copies the
-plan blob to the device through a pinned buffer, and calls ``ssa_kv_append``
-and ``ssa_mixed_attention`` on the current stream.
+uploads the arrays of a generated batch once, plans on the host into pinned,
+device-mapped buffers that the kernels read in place (or, optionally, copies
+the plan to device memory), and calls ``ssa_kv_append`` and
+``ssa_mixed_attention`` on the current stream.
 """
 from __future__ import annotations
 
@@ -34,8 +35,10 @@ def check_block_table(block_table: np.ndarray, q_len, ctx_len, num_pages: int, p
 
 
 class DeviceBatch:
-    def __init__(self, b, tuning: ssa.SsaTuning | None = None, device="cuda"):
+    def __init__(self, b, tuning: ssa.SsaTuning | None = None, device="cuda",
+                 plan_on_device: bool = False):
         self.b = b
+        self.plan_on_device = plan_on_device
         self.device = torch.device(device)
         s = b.shape
         check_block_table(b.block_table, b.q_len, b.ctx_len, b.num_pages, s.page)
@@ -53,49 +56,77 @@ class DeviceBatch:
         self.plan()
 
     def plan(self, tuning: ssa.SsaTuning | None = None):
-        """(Re)build the plan on the host and copy it to the device."""
+        """(Re)build the plan on the host.
+
+        Two plan slots alternate between iterations.  Each is a pinned,
+        device-mapped host buffer that the kernels read directly (no copy), or,
+        with ``plan_on_device``, a pinned buffer plus a device copy."""
         if tuning is not None:
             self.tuning = tuning
         b = self.b
+        torch.cuda.synchronize(self.device)
         nbytes, ws_bytes = ssa.ssa_plan_size(self.shape, b.q_len, b.ctx_len, self.tuning)
-        # two pinned host buffers: the host plans into one while the copy out of
-        # the other may still be queued on the stream
-        self._ring = [torch.zeros(max(nbytes, 128), dtype=torch.uint8).pin_memory()
-                      for _ in range(2)]
-        self._ring_ev = [None, None]
+        nbytes = max(nbytes, 128)
+        self._host = [torch.zeros(nbytes, dtype=torch.uint8).pin_memory() for _ in range(2)]
+        if self.plan_on_device:
+            self._dev = [torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+                         for _ in range(2)]
+        else:
+            self._dev = self._host  # device-mapped pinned memory, read in place
+        self._done = [torch.cuda.Event(), torch.cuda.Event()]  # slot's kernels done
+        self._used = [False, False]
         self._slot = 0
-        self.plan_host = self._ring[0]
         _, self.info = ssa.ssa_plan(self.shape, b.q_len, b.ctx_len, self.tuning,
-                                    out=self.plan_host)
-        self.plan_dev = torch.empty_like(self.plan_host, device=self.device)
-        self.plan_dev.copy_(self.plan_host, non_blocking=True)
-        self._ring_ev[0] = torch.cuda.Event()
-        self._ring_ev[0].record()
+                                    out=self._host[0])
+        if self.plan_on_device:
+            self._dev[0].copy_(self._host[0])
+        self.plan_host, self.plan_dev = self._host[0], self._dev[0]
         if not hasattr(self, "workspace") or self.workspace.numel() < ws_bytes:
             self.workspace = torch.zeros(max(ws_bytes, 256), dtype=torch.uint8, device=self.device)
+        # calls bound once per slot (on the stream current now): an iteration
+        # only crosses into the library
+        self._info_scratch = ssa.SsaPlanInfo()
+        self._bound = []
+        for hb, db in zip(self._host, self._dev):
+            self._bound.append((
+                ssa.bind_plan(self.shape, b.q_len, b.ctx_len, self.tuning, hb, self._info_scratch),
+                ssa.bind_kv_append(self.shape, hb, db, self.k_new, self.v_new, self.k_cache,
+                                   self.v_cache, self.block_table),
+                ssa.bind_mixed_attention(self.shape, hb, db, self.q, self.k_cache, self.v_cache,
+                                         self.block_table, self.out, self.workspace)))
+        torch.cuda.synchronize(self.device)
         return self.info
 
     def replan_host(self):
-        """Host planning of the same batch into a pinned buffer (what a serving
-        loop does every iteration), followed by the async copy to the device."""
-        self._slot ^= 1
-        buf, ev = self._ring[self._slot], self._ring_ev[self._slot]
-        if ev is not None:
-            ev.synchronize()  # the copy that last read this buffer has run
-        ssa.ssa_plan(self.shape, self.b.q_len, self.b.ctx_len, self.tuning, out=buf)
-        self.plan_host = buf
-        self.plan_dev.copy_(buf, non_blocking=True)
-        if ev is None:
-            ev = self._ring_ev[self._slot] = torch.cuda.Event()
-        ev.record()
+        """Plan the (same) batch again on the host into the other slot, as a
+        serving loop does every iteration: wait until the kernels that last read
+        that slot have finished, plan into it, and (only with plan_on_device)
+        copy it to its device buffer on the current stream."""
+        slot = self._slot ^ 1
+        if self._used[slot]:
+            self._done[slot].synchronize()
+        self._bound[slot][0]()
+        if self.plan_on_device:
+            self._dev[slot].copy_(self._host[slot], non_blocking=True)
+        self._used[slot] = True
+        self._slot = slot
+        self.plan_host, self.plan_dev = self._host[slot], self._dev[slot]
 
     def kv_append(self, stream=None):
-        ssa.ssa_kv_append(self.shape, self.plan_host, self.plan_dev, self.k_new, self.v_new,
-                          self.k_cache, self.v_cache, self.block_table, stream)
+        if stream is None:
+            self._bound[self._slot][1]()
+        else:
+            ssa.ssa_kv_append(self.shape, self.plan_host, self.plan_dev, self.k_new, self.v_new,
+                              self.k_cache, self.v_cache, self.block_table, stream)
 
     def attention(self, stream=None):
-        ssa.ssa_mixed_attention(self.shape, self.plan_host, self.plan_dev, self.q, self.k_cache,
-                                self.v_cache, self.block_table, self.out, self.workspace, stream)
+        if stream is None:
+            self._bound[self._slot][2]()
+            self._done[self._slot].record()
+        else:
+            ssa.ssa_mixed_attention(self.shape, self.plan_host, self.plan_dev, self.q,
+                                    self.k_cache, self.v_cache, self.block_table, self.out,
+                                    self.workspace, stream)
 
     def step(self, stream=None):
         self.kv_append(stream)

@@ -39,7 +39,8 @@ class SsaShape(ctypes.Structure):
 
 class SsaTuning(ctypes.Structure):
     _fields_ = [("chunk_tile_cols", ctypes.c_int32), ("chunk_split_keys", ctypes.c_int32),
-                ("decode_split_keys", ctypes.c_int32), ("num_cus", ctypes.c_int32)]
+                ("decode_split_keys", ctypes.c_int32), ("num_cus", ctypes.c_int32),
+                ("num_xcds", ctypes.c_int32), ("mix_order", ctypes.c_int32)]
 
 
 class SsaPlanInfo(ctypes.Structure):
@@ -93,9 +94,10 @@ def make_shape(hq, hkv, d, num_pages, max_pages_per_req, scale, page_size=16) ->
                     int(max_pages_per_req), float(np.float32(scale)))
 
 
-def make_tuning(chunk_tile_cols=0, chunk_split_keys=0, decode_split_keys=0, num_cus=0):
+def make_tuning(chunk_tile_cols=0, chunk_split_keys=0, decode_split_keys=0, num_cus=0,
+                num_xcds=0, mix_order=0):
     return SsaTuning(int(chunk_tile_cols), int(chunk_split_keys), int(decode_split_keys),
-                     int(num_cus))
+                     int(num_cus), int(num_xcds), int(mix_order))
 
 
 def _lens(a):
@@ -213,3 +215,71 @@ def ssa_mixed_attention(shape: SsaShape, plan_host, plan_dev, q, k_cache, v_cach
                                  _ptr(workspace), ws_bytes, _stream(stream))
     if rc != SSA_OK:
         raise SsaError(rc, "ssa_mixed_attention")
+
+
+class BoundCall:
+    """A C entry point with its arguments checked and marshalled once, for a
+    serving loop that repeats the same call (same buffers, same plan buffer)
+    every iteration.  Calling it only crosses into the library."""
+
+    def __init__(self, fn, name, args):
+        self._fn, self._name, self._args = fn, name, args
+
+    def __call__(self):
+        rc = self._fn(*self._args)
+        if rc != SSA_OK:
+            raise SsaError(rc, self._name)
+
+
+def bind_kv_append(shape: SsaShape, plan_host, plan_dev, k_new, v_new, k_cache, v_cache,
+                   block_table, stream=None) -> BoundCall:
+    h = _plan_header(plan_host)
+    T, n = h["num_tokens"], h["num_reqs"]
+    row = shape.num_kv_heads * shape.head_dim
+    pool = shape.num_pages * shape.num_kv_heads * shape.page_size * shape.head_dim
+    _check_dev("k_new", k_new, T * row, 2)
+    _check_dev("v_new", v_new, T * row, 2)
+    _check_dev("k_cache", k_cache, pool, 2)
+    _check_dev("v_cache", v_cache, pool, 2)
+    _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+    vp = ctypes.c_void_p
+    args = (ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)), vp(_ptr(k_new)),
+            vp(_ptr(v_new)), vp(_ptr(k_cache)), vp(_ptr(v_cache)), vp(_ptr(block_table)),
+            vp(_stream(stream)))
+    return BoundCall(LIB.ssa_kv_append, "ssa_kv_append", args)
+
+
+def bind_mixed_attention(shape: SsaShape, plan_host, plan_dev, q, k_cache, v_cache, block_table,
+                         out, workspace, stream=None) -> BoundCall:
+    h = _plan_header(plan_host)
+    T, n = h["num_tokens"], h["num_reqs"]
+    qrow = shape.num_q_heads * shape.head_dim
+    pool = shape.num_pages * shape.num_kv_heads * shape.page_size * shape.head_dim
+    _check_dev("q", q, T * qrow, 2)
+    _check_dev("out", out, T * qrow, 2)
+    _check_dev("k_cache", k_cache, pool, 2)
+    _check_dev("v_cache", v_cache, pool, 2)
+    _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    vp = ctypes.c_void_p
+    args = (ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)), vp(_ptr(q)),
+            vp(_ptr(k_cache)), vp(_ptr(v_cache)), vp(_ptr(block_table)), vp(_ptr(out)),
+            vp(_ptr(workspace)), ctypes.c_size_t(ws_bytes), vp(_stream(stream)))
+    return BoundCall(LIB.ssa_mixed_attention, "ssa_mixed_attention", args)
+
+
+def bind_plan(shape: SsaShape, q_len, ctx_len, tuning, out, info: SsaPlanInfo) -> BoundCall:
+    """ssa_plan into a fixed host buffer (numpy array or pinned tensor)."""
+    ql, pq = _lens(q_len)
+    cl, pc = _lens(ctx_len)
+    if isinstance(out, np.ndarray):
+        ptr, cap = out.ctypes.data, out.nbytes
+    else:
+        ptr, cap = out.data_ptr(), out.numel() * out.element_size()
+    vp = ctypes.c_void_p
+    args = (ctypes.byref(shape), vp(pq), vp(pc), ctypes.c_int32(ql.shape[0]),
+            ctypes.byref(tuning) if tuning is not None else None, vp(ptr), ctypes.c_size_t(cap),
+            ctypes.byref(info))
+    call = BoundCall(LIB.ssa_plan, "ssa_plan", args)
+    call._keep = (ql, cl)  # the length arrays must outlive the call
+    return call

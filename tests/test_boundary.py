@@ -23,7 +23,7 @@ HDR = np.dtype([("magic", "<u4"), ("version", "<u4"), ("hash", "<u8"), ("num_req
 REQ = np.dtype([("q_start", "<i4"), ("q_len", "<i4"), ("ctx_len", "<i4"), ("n_pages", "<i4")])
 ITEM = np.dtype([("kind", "<i4"), ("req", "<i4"), ("kvh", "<i4"), ("col0", "<i4"),
                  ("ncols", "<i4"), ("key0", "<i4"), ("key1", "<i4"), ("group", "<i4"),
-                 ("split", "<i4"), ("reserved", "<i4", 3)])
+                 ("split", "<i4"), ("q_start", "<i4"), ("ctx_len", "<i4"), ("nvalid", "<i4")])
 GROUP = np.dtype([("nsplit", "<i4"), ("ncols", "<i4"), ("ws_off", "<i8")])
 SEG = np.dtype([("req", "<i4"), ("row0", "<i4"), ("pos0", "<i4"), ("n", "<i4")])
 
@@ -69,6 +69,7 @@ def check_plan_covers_batch(hq, hkv, d, q_len, ctx_len, tuning=None):
     for it in items:
         i = it["req"]
         c, u = int(q_len[i]), int(ctx_len[i])
+        assert (it["q_start"], it["ctx_len"], it["nvalid"]) == (int(reqs["q_start"][i]), u, u + c)
         if it["kind"] == 1:
             assert c == 1 and it["ncols"] == G
             cols = [(int(reqs["q_start"][i]), it["kvh"] * G + hg, u) for hg in range(G)]

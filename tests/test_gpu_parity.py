@@ -30,12 +30,12 @@ def torch_dev():
     return torch
 
 
-def run(b, tuning=None):
+def run(b, tuning=None, plan_on_device=False):
     import torch
     from paper_2606_05933_amd.device import DeviceBatch
     say(f"[gpu] {b.name} reqs={b.num_reqs} T={b.num_tokens} hq/hkv/d={b.shape.hq}/{b.shape.hkv}/"
-        f"{b.shape.d} seed={b.seed}")
-    db = DeviceBatch(b, tuning)
+        f"{b.shape.d} seed={b.seed} plan_on_device={plan_on_device}")
+    db = DeviceBatch(b, tuning, plan_on_device=plan_on_device)
     db.step()
     torch.cuda.synchronize()
     return db
@@ -51,10 +51,10 @@ def assert_close(got, ref, what=""):
         assert err.mean() <= MEAN_ABS, f"{what}: mean abs {err.mean()}"
 
 
-def full_parity(b, tuning=None):
+def full_parity(b, tuning=None, plan_on_device=False):
     from oracle import oracle
     from paper_2606_05933_amd.device import bits_of
-    db = run(b, tuning)
+    db = run(b, tuning, plan_on_device)
     kc, vc = oracle.batch_kv_append(b)
     assert np.array_equal(bits_of(db.k_cache).reshape(kc.shape), kc), "K pool image differs"
     assert np.array_equal(bits_of(db.v_cache).reshape(vc.shape), vc), "V pool image differs"
@@ -95,9 +95,27 @@ def test_tiny_workload_matches_oracle(torch_dev):
     full_parity(workload.make_workload("tiny", seed=0))
 
 
-def test_llama8b_mixed_full_parity(torch_dev):
+@pytest.mark.parametrize("plan_on_device", [False, True])
+def test_llama8b_mixed_full_parity(torch_dev, plan_on_device):
     from paper_2606_05933_amd import workload
-    full_parity(workload.make_workload("l8b", seed=0))
+    full_parity(workload.make_workload("l8b", seed=0), plan_on_device=plan_on_device)
+
+
+def test_replanned_iterations_alternate_plan_slots(torch_dev):
+    """Several iterations in a row, each re-planned into the other plan slot
+    while the previous one may still run: every output matches the oracle."""
+    import torch
+    from oracle import oracle
+    from paper_2606_05933_amd import workload
+    b = workload.make_workload("l8b", seed=2)
+    db = run(b)
+    for _ in range(5):
+        db.replan_host()
+        db.step()
+    torch.cuda.synchronize()
+    kc, vc = oracle.batch_kv_append(b)
+    ref, _ = oracle.batch_attention(b, kc, vc)
+    assert_close(db.out_f32(), ref, "l8b replanned")
 
 
 @pytest.mark.parametrize("tile,csplit,dsplit", [(32, 0, 0), (64, 1024, 256), (128, 512, 128),
