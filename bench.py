@@ -196,7 +196,7 @@ def main_bench(args):
                 "kernel_us": round(attn_s * 1e6, 2)}
 
     extra = {}
-    if not args.quick:
+    if args.extras:
         flush = Flusher()
         extra["attention_cold_us"] = round(time_kernel_events(db.attention, 20, flush) * 1e6, 2)
         dec = workload.sub_batch(b, b.q_len == 1)
@@ -351,7 +351,9 @@ def main():
     ap.add_argument("--prefix", type=int, default=None)
     ap.add_argument("--scene", choices=["mixed", "decode", "prefill"], default="mixed")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--quick", action="store_true", help="skip the cold and per-segment timings")
+    ap.add_argument("--extras", action="store_true",
+                    help="also time the attention launch with a cold cache and each segment alone "
+                         "(extra launches of the same kernels on other batches)")
     ap.add_argument("--sweep", metavar="OUT", default=None)
     ap.add_argument("--sweep-workloads", default=None)
     ap.add_argument("--copy-probe", action="store_true")
