@@ -58,11 +58,37 @@ class SsaPlanInfo(ctypes.Structure):
         return d
 
 
+def hip_runtimes_loaded() -> list[str]:
+    """Distinct files of the HIP runtime (libamdhip64) mapped into this process."""
+    paths = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                path = line.split()[-1] if line.strip() else ""
+                if "libamdhip64" in os.path.basename(path):
+                    paths.add(os.path.realpath(path))
+    except OSError:
+        pass
+    return sorted(paths)
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run paper_2606_05933_amd.build.build() "
                           "(there is no non-HIP fallback)")
+    # The library must share torch's HIP runtime: torch owns the device
+    # memory and the streams it is called with.  torch loads its own copy of
+    # libamdhip64 by file name; the library asks for the runtime by soname,
+    # which resolves to torch's copy only if that is loaded first.  Loaded the
+    # other way round, the process holds two runtimes, and a stream handle of
+    # one is not valid in the other (every launch fails).
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
+    runtimes = hip_runtimes_loaded()
+    if len(runtimes) > 1:
+        raise ImportError("more than one HIP runtime is loaded in this process: "
+                          + ", ".join(runtimes)
+                          + "; load libssa.so only after torch (import torch first)")
     vp, sz = ctypes.c_void_p, ctypes.c_size_t
     P = ctypes.POINTER
     lib.ssa_status_string.argtypes = [ctypes.c_int]

@@ -290,3 +290,30 @@ def test_generator_is_deterministic_and_poisons_unwritten_slots():
     x = np.float32([1.0, 1.00390625, 1.01171875, -2.5, 3.1415926])
     assert np.array_equal(workload.bf16_bits_to_f32(workload.f32_to_bf16_bits(x)),
                           np.float32([1.0, 1.0, 1.015625, -2.5, 3.140625]))
+
+
+def _fresh_python(code):
+    import subprocess
+    import sys
+    return subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                          timeout=300, cwd=ROOT)
+
+
+def test_binding_shares_torchs_hip_runtime_whatever_is_imported_first():
+    """The binding loaded before anything imported torch still ends up with a
+    single HIP runtime in the process (torch's): torch's streams and memory are
+    only valid in the runtime that made them."""
+    r = _fresh_python("from paper_2606_05933_amd import ssa\n"
+                      "import torch\n"
+                      "rt = ssa.hip_runtimes_loaded()\n"
+                      "print(len(rt), rt)\n"
+                      "assert len(rt) == 1, rt\n")
+    assert r.returncode == 0, r.stdout + r.stderr
+
+
+def test_binding_refuses_a_process_with_two_hip_runtimes():
+    r = _fresh_python("import ctypes\n"
+                      "ctypes.CDLL('paper_2606_05933_amd/libssa.so')\n"
+                      "from paper_2606_05933_amd import ssa\n")
+    assert r.returncode != 0
+    assert "more than one HIP runtime" in r.stderr
