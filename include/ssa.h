@@ -192,6 +192,27 @@ int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const voi
                         const int32_t* block_table, uint16_t* out, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/*
+ * The two launches above with kernel timing: identical work and errors, plus
+ * two optional HIP events (hipEvent_t as void*, created by the caller with
+ * timing enabled; NULL = not recorded).  start_event takes the time the kernel
+ * starts and stop_event the time it ends, stamped from the kernel's own
+ * dispatch (hipExtLaunchKernel), so timing adds no packet to the stream and no
+ * gap between the kernel and its neighbours.  Per-iteration kernel latencies
+ * are what the paper's batch latency predictor is fitted on (Sec. 3.2, Eq. 5).
+ * When the batch has no work (no launch), the events are not recorded.
+ */
+int ssa_kv_append_timed(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                        const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache,
+                        uint16_t* v_cache, const int32_t* block_table, void* stream,
+                        void* start_event, void* stop_event);
+
+int ssa_mixed_attention_timed(const ssa_shape* shape, const void* plan_host,
+                              const void* plan_dev, const uint16_t* q, const uint16_t* k_cache,
+                              const uint16_t* v_cache, const int32_t* block_table, uint16_t* out,
+                              void* workspace, size_t workspace_bytes, void* stream,
+                              void* start_event, void* stop_event);
+
 #ifdef __cplusplus
 }
 #endif

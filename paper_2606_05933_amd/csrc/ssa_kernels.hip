@@ -34,6 +34,7 @@
 // operand of the PV MFMA, whose A operand (V^T) is then 8 consecutive slots of
 // one value-page row: a single 16-byte load.  That is why value pages are
 // stored dim-major ([D][16 slots]).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -740,9 +741,10 @@ hipError_t clear_and_check() { return hipGetLastError(); }
 
 extern "C" {
 
-int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
-                  const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache,
-                  uint16_t* v_cache, const int32_t* block_table, void* stream) {
+int ssa_kv_append_timed(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                        const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache,
+                        uint16_t* v_cache, const int32_t* block_table, void* stream,
+                        void* start_event, void* stop_event) {
   const PlanHeader* h = nullptr;
   int rc = check_plan(shape, plan_host, &h);
   if (rc) return rc;
@@ -750,24 +752,32 @@ int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* pla
   if (h->num_segments == 0) return SSA_OK;
   if (!k_new || !v_new || !k_cache || !v_cache || !block_table) return SSA_ERR_NULL;
   (void)clear_and_check();
-  dim3 grid(h->num_segments, h->hkv);
-  hipStream_t st = static_cast<hipStream_t>(stream);
   const uint8_t* p = static_cast<const uint8_t*>(plan_dev);
-  if (h->head_dim == 128)
-    kv_append_kernel<128><<<grid, kThreads, 0, st>>>(p, h->hash, h->off_segments, k_new, v_new,
-                                                     k_cache, v_cache,
-                                                     block_table, h->hkv, h->max_pages_per_req);
-  else
-    kv_append_kernel<64><<<grid, kThreads, 0, st>>>(p, h->hash, h->off_segments, k_new, v_new,
-                                                    k_cache, v_cache,
-                                                    block_table, h->hkv, h->max_pages_per_req);
-  return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+  uint64_t hash = h->hash;
+  int32_t off_segments = h->off_segments, hkv = h->hkv, maxp = h->max_pages_per_req;
+  void* args[] = {&p, &hash, &off_segments, &k_new, &v_new, &k_cache, &v_cache, &block_table,
+                  &hkv, &maxp};
+  const void* fn = h->head_dim == 128 ? reinterpret_cast<const void*>(&kv_append_kernel<128>)
+                                      : reinterpret_cast<const void*>(&kv_append_kernel<64>);
+  hipError_t e = hipExtLaunchKernel(fn, dim3(h->num_segments, h->hkv), dim3(kThreads), args, 0,
+                                    static_cast<hipStream_t>(stream),
+                                    static_cast<hipEvent_t>(start_event),
+                                    static_cast<hipEvent_t>(stop_event), 0);
+  return e == hipSuccess && hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
 }
 
-int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
-                        const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
-                        const int32_t* block_table, uint16_t* out, void* workspace,
-                        size_t workspace_bytes, void* stream) {
+int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                  const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache,
+                  uint16_t* v_cache, const int32_t* block_table, void* stream) {
+  return ssa_kv_append_timed(shape, plan_host, plan_dev, k_new, v_new, k_cache, v_cache,
+                             block_table, stream, nullptr, nullptr);
+}
+
+int ssa_mixed_attention_timed(const ssa_shape* shape, const void* plan_host,
+                              const void* plan_dev, const uint16_t* q, const uint16_t* k_cache,
+                              const uint16_t* v_cache, const int32_t* block_table, uint16_t* out,
+                              void* workspace, size_t workspace_bytes, void* stream,
+                              void* start_event, void* stop_event) {
   const PlanHeader* h = nullptr;
   int rc = check_plan(shape, plan_host, &h);
   if (rc) return rc;
@@ -794,12 +804,24 @@ int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const voi
   a.G = h->hq / h->hkv;
   a.maxp = h->max_pages_per_req;
   (void)clear_and_check();
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  if (h->head_dim == 128)
-    mixed_attention_kernel<128><<<h->num_items, kThreads, 0, st>>>(a);
-  else
-    mixed_attention_kernel<64><<<h->num_items, kThreads, 0, st>>>(a);
-  return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+  void* args[] = {&a};
+  const void* fn = h->head_dim == 128
+                       ? reinterpret_cast<const void*>(&mixed_attention_kernel<128>)
+                       : reinterpret_cast<const void*>(&mixed_attention_kernel<64>);
+  hipError_t e = hipExtLaunchKernel(fn, dim3(h->num_items), dim3(kThreads), args, 0,
+                                    static_cast<hipStream_t>(stream),
+                                    static_cast<hipEvent_t>(start_event),
+                                    static_cast<hipEvent_t>(stop_event), 0);
+  return e == hipSuccess && hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
 }
+
+int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                        const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                        const int32_t* block_table, uint16_t* out, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  return ssa_mixed_attention_timed(shape, plan_host, plan_dev, q, k_cache, v_cache, block_table,
+                                   out, workspace, workspace_bytes, stream, nullptr, nullptr);
+}
+
 
 }  // extern "C"

@@ -73,7 +73,12 @@ class DeviceBatch:
                          for _ in range(2)]
         else:
             self._dev = self._host  # device-mapped pinned memory, read in place
-        self._done = [torch.cuda.Event(), torch.cuda.Event()]  # slot's kernels done
+        # "the slot's kernels are done": the attention launch of the slot stamps
+        # its own end into one of these (no extra packet on the stream)
+        self._own_done = [torch.cuda.Event(), torch.cuda.Event()]
+        for ev in self._own_done:
+            ev.record()  # creates the HIP event
+        self._done = list(self._own_done)
         self._used = [False, False]
         self._slot = 0
         _, self.info = ssa.ssa_plan(self.shape, b.q_len, b.ctx_len, self.tuning,
@@ -112,17 +117,24 @@ class DeviceBatch:
         self._slot = slot
         self.plan_host, self.plan_dev = self._host[slot], self._dev[slot]
 
-    def kv_append(self, stream=None):
+    def kv_append(self, stream=None, events=(None, None)):
+        """events: optional (start, stop) torch.cuda.Event pair stamped with the
+        kernel's own start and end (current stream only)."""
         if stream is None:
-            self._bound[self._slot][1]()
+            self._bound[self._slot][1](*events)
         else:
             ssa.ssa_kv_append(self.shape, self.plan_host, self.plan_dev, self.k_new, self.v_new,
                               self.k_cache, self.v_cache, self.block_table, stream)
 
-    def attention(self, stream=None):
+    def attention(self, stream=None, events=(None, None)):
+        """events: optional (start, stop) pair stamped by the kernel; the stop
+        event then also marks the slot's kernels done."""
         if stream is None:
-            self._bound[self._slot][2]()
-            self._done[self._slot].record()
+            start, stop = events
+            if stop is None:
+                stop = self._own_done[self._slot]
+            self._bound[self._slot][2](start, stop)
+            self._done[self._slot] = stop
         else:
             ssa.ssa_mixed_attention(self.shape, self.plan_host, self.plan_dev, self.q,
                                     self.k_cache, self.v_cache, self.block_table, self.out,

@@ -102,13 +102,18 @@ def _load():
     lib.ssa_kv_append.restype = ctypes.c_int
     lib.ssa_mixed_attention.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.ssa_mixed_attention.restype = ctypes.c_int
+    lib.ssa_kv_append_timed.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.ssa_kv_append_timed.restype = ctypes.c_int
+    lib.ssa_mixed_attention_timed.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp,
+                                              vp, vp]
+    lib.ssa_mixed_attention_timed.restype = ctypes.c_int
     return lib
 
 
 LIB = _load()
 
 EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
-            "ssa_mixed_attention")
+            "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed")
 
 
 def ssa_status_string(code: int) -> str:
@@ -248,13 +253,29 @@ class BoundCall:
     serving loop that repeats the same call (same buffers, same plan buffer)
     every iteration.  Calling it only crosses into the library."""
 
-    def __init__(self, fn, name, args):
+    def __init__(self, fn, name, args, timed=False):
         self._fn, self._name, self._args = fn, name, args
+        self._untimed = args + (None, None) if timed else args
 
-    def __call__(self):
-        rc = self._fn(*self._args)
+    def __call__(self, start_event=None, stop_event=None):
+        """start_event / stop_event (timed entry points only): torch.cuda.Event
+        objects (timing enabled, recorded at least once so that the HIP event
+        exists) that receive the kernel's own start and end times."""
+        if start_event is None and stop_event is None:
+            rc = self._fn(*self._untimed)
+        else:
+            rc = self._fn(*self._args, _event(start_event), _event(stop_event))
         if rc != SSA_OK:
             raise SsaError(rc, self._name)
+
+
+def _event(ev):
+    if ev is None:
+        return None
+    handle = ev.cuda_event
+    if not handle:
+        raise ValueError("the event has no HIP event yet: record it once before timing")
+    return ctypes.c_void_p(handle)
 
 
 def bind_kv_append(shape: SsaShape, plan_host, plan_dev, k_new, v_new, k_cache, v_cache,
@@ -272,7 +293,7 @@ def bind_kv_append(shape: SsaShape, plan_host, plan_dev, k_new, v_new, k_cache, 
     args = (ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)), vp(_ptr(k_new)),
             vp(_ptr(v_new)), vp(_ptr(k_cache)), vp(_ptr(v_cache)), vp(_ptr(block_table)),
             vp(_stream(stream)))
-    return BoundCall(LIB.ssa_kv_append, "ssa_kv_append", args)
+    return BoundCall(LIB.ssa_kv_append_timed, "ssa_kv_append", args, timed=True)
 
 
 def bind_mixed_attention(shape: SsaShape, plan_host, plan_dev, q, k_cache, v_cache, block_table,
@@ -291,7 +312,7 @@ def bind_mixed_attention(shape: SsaShape, plan_host, plan_dev, q, k_cache, v_cac
     args = (ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)), vp(_ptr(q)),
             vp(_ptr(k_cache)), vp(_ptr(v_cache)), vp(_ptr(block_table)), vp(_ptr(out)),
             vp(_ptr(workspace)), ctypes.c_size_t(ws_bytes), vp(_stream(stream)))
-    return BoundCall(LIB.ssa_mixed_attention, "ssa_mixed_attention", args)
+    return BoundCall(LIB.ssa_mixed_attention_timed, "ssa_mixed_attention", args, timed=True)
 
 
 def bind_plan(shape: SsaShape, q_len, ctx_len, tuning, out, info: SsaPlanInfo) -> BoundCall:

@@ -257,6 +257,15 @@ def test_launchers_validate_before_any_hip_call():
     junk = np.zeros(256, np.uint8)
     assert L.ssa_kv_append(ctypes.byref(shape), junk.ctypes.data, fake, fake, fake, fake, fake,
                            fake, None) == -9
+    # the timed entry points validate the same way (events are never touched)
+    assert L.ssa_kv_append_timed(ctypes.byref(shape), p, None, fake, fake, fake, fake, fake, None,
+                                 fake, fake) == -1
+    assert L.ssa_kv_append_timed(ctypes.byref(other), p, fake, fake, fake, fake, fake, fake, None,
+                                 fake, fake) == -9
+    assert L.ssa_mixed_attention_timed(ctypes.byref(shape), p, fake, fake, fake, fake, fake, fake,
+                                       fake, ws - 1, None, fake, fake) == -8
+    assert L.ssa_mixed_attention_timed(ctypes.byref(other), p, fake, fake, fake, fake, fake, fake,
+                                       fake, ws, None, fake, fake) == -9
 
 
 def test_empty_batch_launches_nothing():

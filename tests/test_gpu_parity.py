@@ -199,3 +199,26 @@ def test_repeat_launches_are_bitwise_identical_and_reset_tickets(torch_dev):
     ng = db.info.num_merge_groups
     tickets = db.workspace[: 4 * ng].view(torch.int32)
     assert int(tickets.abs().sum()) == 0
+
+
+def test_timed_launches_stamp_the_kernels_and_match_untimed(torch_dev):
+    """The timed entry points do the same work (bitwise) and stamp both events
+    with a positive kernel duration."""
+    import torch
+    from paper_2606_05933_amd import workload
+    b = workload.make_workload("l8b", seed=3)
+    db = run(b)
+    ref = db.out.clone()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in evs:
+        e.record()  # creates the HIP events
+    torch.cuda.synchronize()
+    db.out.zero_()
+    db.kv_append(events=(evs[0], evs[1]))
+    db.attention(events=(evs[2], evs[3]))
+    torch.cuda.synchronize()
+    assert torch.equal(db.out.view(torch.int16), ref.view(torch.int16))
+    t_app, t_att = evs[0].elapsed_time(evs[1]), evs[2].elapsed_time(evs[3])
+    say(f"    kv_append {t_app * 1e3:.1f} us, attention {t_att * 1e3:.1f} us")
+    assert 0 < t_app < 1000 and 0 < t_att < 1000
+    assert evs[1].elapsed_time(evs[2]) >= 0
