@@ -38,6 +38,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "../../include/ssa.h"
 #include "ssa_plan_format.h"
 
@@ -60,6 +62,19 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // which are not ordered with the vector loads of K/V pages.
 typedef const __attribute__((address_space(4))) int32_t cint32;
 
+// One wave-wide global -> LDS copy of 16 bytes per lane (gfx950
+// global_load_lds_dwordx4): lane i's 16 bytes from g land at LDS address
+// l + 16 i.  It is issued as inline assembly so that the compiler's memory
+// counter tracking does not make later reads of *other* LDS stages wait for
+// it; every reader of the destination waits explicitly (lds_dma_wait before
+// the barrier that publishes the stage).
+__device__ __forceinline__ void dma16(const void* g, const char* l) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)l;
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(a) : "memory");
+}
+// s_waitcnt vmcnt(0): this wave's LDS copies (and loads) have landed.
+__device__ __forceinline__ void lds_dma_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 constexpr float kLog2e = 1.4426950408889634f;
 // The running maximum of a column is raised only when a block's logit exceeds
 // it by more than this (base 2): probabilities then stay below 2^8, and the
@@ -75,13 +90,14 @@ struct Cfg {
   static constexpr int CPR = D / 8;          // 16-byte chunks per key row
   static constexpr int K_ROW = D * 2;        // LDS bytes per key row (chunks XOR-swizzled)
   static constexpr int K_STAGE = 32 * K_ROW; // one 32-key block of K
-  static constexpr int V_ROW = 80;           // LDS bytes per value row: 32 slots + 16 pad
-  static constexpr int V_STAGE = D * V_ROW;
+  static constexpr int V_PAGE = D * 32;      // LDS bytes of one value page: D rows of 16 slots
+  static constexpr int V_STAGE = 2 * V_PAGE;
   static constexpr int STAGE = K_STAGE + V_STAGE;
-  static constexpr int LDS_CHUNK = 2 * STAGE;
+  static constexpr int LDS_CHUNK = 3 * STAGE;  // three stages (chunk pipeline)
   static constexpr int LDS_DECODE = kWaves * (32 + 16 * D) * 4;
   static constexpr int LDS = LDS_CHUNK > LDS_DECODE ? LDS_CHUNK : LDS_DECODE;
   static constexpr int LOADS = D / 64;       // 16-byte K (and V) chunks per thread per block
+  static constexpr int KROWS_PER_LOAD = 64 / CPR;  // key rows one wave-wide 1 KB load fills
 };
 
 struct AttnArgs {
@@ -155,10 +171,10 @@ __device__ __forceinline__ float wave_max_cols(float x) {
   const unsigned u = as_u32(x);
   const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
   const unsigned a0 = a[0], a1 = a[1];
-  const unsigned v = as_u32(fmaxf(as_f32(a0), as_f32(a1)));
+  const unsigned v = as_u32(__builtin_elementwise_maximum(as_f32(a0), as_f32(a1)));
   const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
   const unsigned b0 = b[0], b1 = b[1];
-  return fmaxf(as_f32(b0), as_f32(b1));
+  return __builtin_elementwise_maximum(as_f32(b0), as_f32(b1));
 }
 __device__ __forceinline__ float wave_sum_cols(float x) {
   const unsigned u = as_u32(x);
@@ -309,12 +325,134 @@ __device__ void finish_split(const AttnArgs& a, const WorkItem& it, const ReqEnt
 
 // ---------------------------------------------------------------- chunk tiles
 
+// Per-column online-softmax state of one 16-column tile (one lane's column).
+//   m    reference in base-2 units (probabilities are exp2(c*s - m))
+//   thr  raw logit above which a block raises the reference:
+//        (m + kRescaleThreshold) / c, -inf while nothing was seen
+//   l    sum of the bf16-rounded probabilities
+struct ColState {
+  float m, thr, l;
+};
+
+// One 32-key block of a 16-column tile, in compute-then-correct form: the
+// probabilities are formed against the current reference right away (no
+// cross-lane step; softmax_begin), and only if some lane sees a logit above
+// `thr` does a wave-uniform branch (softmax_end) take the column maxima, raise
+// the reference of those columns, rescale their O and l, and form the block
+// again.  After the first block of a column that branch is rare, so the common
+// path is the 8-way maximum, 8 FMA + 8 exp2, packing and the l sum, none of
+// which depends on the MFMAs of the other tile: the caller interleaves them.
+//   s0, s1 the QK^T outputs of the block's two key halves (this lane: keys
+//          8g .. 8g+7 of the block for column r16)
+//   lim    (MASKED) key e of the lane is visible iff e <= lim
+//   c      softmax_scale * log2(e) >= 0, inv_c = 1 / c (inf for c = 0)
+// Maximum of 8 logits with the NaN-propagating maximum (v_maximum3_f32 on
+// gfx950): unlike fmaxf it needs no quieting of its MFMA-produced operands.
+// Every operand is a finite logit or -inf (masked), never NaN.
+__device__ __forceinline__ float max8(const float (&s)[8]) {
+  auto mx = [](float a, float b) { return __builtin_elementwise_maximum(a, b); };
+  return mx(mx(mx(s[0], s[1]), mx(s[2], s[3])), mx(mx(s[4], s[5]), mx(s[6], s[7])));
+}
+
+struct SmBlock {
+  float s[8];
+  float lmax, lb;
+  u32x4 pk;
+};
+
+template <bool MASKED>
+__device__ __forceinline__ u32x4 sm_form(const float (&s)[8], int lim, float c, float m,
+                                         float& lb) {
+  float p[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c, -m));
+    if (MASKED) p[e] = (e <= lim) ? p[e] : 0.f;
+  }
+  const u32x4 w = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
+  const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3];
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  float acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), one, 0.f, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), one, acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w2), one, acc, false);
+  lb = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w3), one, acc, false);
+  return w;
+}
+
+template <bool MASKED>
+__device__ __forceinline__ SmBlock softmax_begin(f32x4 s0, f32x4 s1, int lim, float c,
+                                                 const ColState& st) {
+  SmBlock b;
+  b.s[0] = s0[0]; b.s[1] = s0[1]; b.s[2] = s0[2]; b.s[3] = s0[3];
+  b.s[4] = s1[0]; b.s[5] = s1[1]; b.s[6] = s1[2]; b.s[7] = s1[3];
+  if (MASKED) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) b.s[e] = (e <= lim) ? b.s[e] : kNegInf;
+  }
+  b.lmax = max8(b.s);
+  b.pk = sm_form<MASKED>(b.s, lim, c, st.m, b.lb);
+  return b;
+}
+
+template <int MT, bool MASKED>
+__device__ __forceinline__ bf16x8 softmax_end(SmBlock& b, int lim, float c, float inv_c,
+                                              ColState& st, f32x4 (&o)[MT]) {
+  if (__builtin_amdgcn_ballot_w64(b.lmax > st.thr)) {
+    const float cmax = wave_max_cols(b.lmax);
+    const bool raise = cmax > st.thr;  // the same for every lane of a column
+    const float m_new = raise ? cmax * c : st.m;
+    const float alpha = raise ? __builtin_amdgcn_exp2f(st.m - m_new) : 1.f;
+    st.l *= alpha;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) o[mt] *= alpha;
+    st.m = m_new;
+    st.thr = raise ? (m_new + kRescaleThreshold) * inv_c : st.thr;
+    float lb2;
+    const u32x4 pk2 = sm_form<MASKED>(b.s, lim, c, m_new, lb2);
+    // columns that did not raise keep the block as first formed (the same values)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t x = pk2[i], y = b.pk[i];
+      b.pk[i] = raise ? x : y;
+    }
+    b.lb = raise ? lb2 : b.lb;
+  }
+  st.l += b.lb;
+  return as_bf16x8(b.pk);
+}
+
+// Scheduling hints for one pipeline step (one basic block) of READS operand
+// fragments, each feeding two MFMAs: two reads ahead, then per fragment its
+// two MFMAs with VALU instructions (the softmax of the other tile) between
+// them and the next read, so the matrix core and the vector ALU both stay busy
+// while few fragments are live.
+constexpr int kMaskMfma = 0x008, kMaskValu = 0x002 | 0x400, kMaskDsRead = 0x100;
+
+template <int READS, int VALU_PER_MFMA>
+__device__ __forceinline__ void interleave_stream() {
+  __builtin_amdgcn_sched_group_barrier(kMaskDsRead, 2, 0);
+  __builtin_amdgcn_sched_group_barrier(kMaskValu, 4, 0);
+#pragma unroll
+  for (int i = 0; i < READS; ++i) {
+    __builtin_amdgcn_sched_group_barrier(kMaskMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kMaskValu, VALU_PER_MFMA, 0);
+    if (i + 2 < READS) __builtin_amdgcn_sched_group_barrier(kMaskDsRead, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kMaskMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kMaskValu, VALU_PER_MFMA, 0);
+  }
+}
+
+template <int S>
+using Stage = std::integral_constant<int, S>;
+
 template <int D>
 __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
                            char* lds) {
   using C = Cfg<D>;
   constexpr int KK = C::KK, MT = C::MT, NT = kChunkWaveCols / 16;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  static_assert(NT == 2, "the chunk pipeline alternates two 16-column tiles");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int g = lane >> 4, r16 = lane & 15;
   const int G = a.G;
   const int u = rq.ctx_len;
@@ -323,6 +461,8 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   const size_t page_stride = (size_t)a.hkv * 16 * D;
   const uint16_t* kbase = a.kc + (size_t)it.kvh * 16 * D;
   const uint16_t* vbase = a.vc + (size_t)it.kvh * 16 * D;
+  const float c = a.scale_log2;
+  const float inv_c = 1.f / c;
 
   // this wave's columns: [wc0, wc1)
   const int colend = it.col0 + it.ncols;
@@ -331,6 +471,8 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   const bool wave_has = wc0 < colend;
   const int wpmin = wave_has ? u + wc0 / G : 0;                     // smallest position
   const int wkend = wave_has ? min(it.key1, u + (wc1 - 1) / G + 1) : it.key0;
+  const int nb = (it.key1 - it.key0 + 31) / 32;                     // blocks of the item
+  const int nbw = (wkend - it.key0 + 31) / 32;                      // blocks this wave uses
 
   bf16x8 qop[NT][KK];
   int pos[NT];
@@ -351,12 +493,11 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     }
   }
 
-  float m_run[NT], l_run[NT];
+  ColState cs[NT];
   f32x4 o[NT][MT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    m_run[nt] = kNegInf;
-    l_run[nt] = 0.f;
+    cs[nt] = ColState{kNegInf, kNegInf, 0.f};
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) o[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
@@ -369,124 +510,186 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   int kaddr[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) kaddr[kk] = key0 * C::K_ROW + (((kk * 4 + g) ^ sw) << 4);
-  const int vaddr = C::K_STAGE + r16 * C::V_ROW + g * 16;
+  // Value pages sit in LDS page-major, as in HBM: page half h of the block,
+  // row d, 16 slots (32 bytes).  The two 16-byte halves of a row are swapped
+  // when vswz(d) is set, so that the A-operand reads of one MFMA (16 rows,
+  // one half each) hit distinct bank slots.
+  auto vswz = [](int d) { return ((d >> 2) ^ (d >> 3)) & 1; };
+  const int vaddr = C::K_STAGE + (g >> 1) * C::V_PAGE + r16 * 32 + (((g & 1) ^ vswz(r16)) << 4);
 
-  // Cooperative staging of one 32-key block: each thread moves LOADS 16-byte
-  // chunks of K and of V.  The two page indices of a block are wave-uniform
-  // scalar loads; a page past the request's last one is read from the first
-  // page instead (in bounds): its keys are beyond every position and its
-  // values are zeroed at store time together with the unwritten tail slots.
-  int kgo[C::LOADS], vgo[C::LOADS], kso[C::LOADS], vso[C::LOADS], vkb[C::LOADS];
-  bool second[C::LOADS];
+  // Staging of one 32-key block, global -> LDS without registers
+  // (global_load_lds_dwordx4): load r of wave w fills 1 KB of the stage,
+  // 16 bytes per lane in lane order, so each lane fetches the global chunk
+  // that belongs at its LDS slot.  Load r of every wave reads one page of the
+  // block (page r for D = 128; page w / 2 for D = 64), whose index is a
+  // wave-uniform scalar load.  A page past the request's last one is read
+  // from the first page instead (in bounds): its keys are beyond every
+  // position, and the values of unwritten slots are zeroed in LDS before use
+  // (a zero probability times a NaN would not be zero).
+  int kgo[C::LOADS], vgo[C::LOADS];
 #pragma unroll
   for (int r = 0; r < C::LOADS; ++r) {
-    const int ci = tid + r * kThreads;
-    const int page = __builtin_amdgcn_readfirstlane(ci / (2 * D));
-    const int within = ci % (2 * D);
-    const int slot = within / C::CPR, c = within % C::CPR;
-    const int key = page * 16 + slot;
-    kgo[r] = slot * D + c * 8;
-    kso[r] = key * C::K_ROW + ((c ^ kswz<D>(key)) << 4);
-    // value chunks: consecutive threads take consecutive rows d, so that the
-    // LDS writes (row stride 80 bytes) fall in distinct bank slots
-    const int d = within % D, half = within / D;
-    vgo[r] = d * 16 + half * 8;
-    vso[r] = C::K_STAGE + d * C::V_ROW + (page * 2 + half) * 16;
-    vkb[r] = page * 16 + half * 8;
-    second[r] = page != 0;
+    const int m = r * kWaves + w;  // which 1 KB of the stage
+    const int key = m * C::KROWS_PER_LOAD + lane / C::CPR;
+    const int ch = (lane % C::CPR) ^ kswz<D>(key);
+    kgo[r] = (key & 15) * D + ch * 8;
+    const int d = (m * 32) % D + (lane >> 1);
+    vgo[r] = d * 16 + (((lane & 1) ^ vswz(d)) << 3);
   }
-  u32x4 kreg[C::LOADS], vreg[C::LOADS];
-  int vkeep[C::LOADS];
-  auto gload = [&](int kb) {
+  auto dma = [&](int kb, char* stage) {
     const int lp0 = kb >> 4;
     const int pg0 = bt[lp0];
     const int pg1 = (lp0 + 1 < rq.n_pages) ? bt[lp0 + 1] : pg0;
 #pragma unroll
     for (int r = 0; r < C::LOADS; ++r) {
-      const size_t pb = (size_t)(second[r] ? pg1 : pg0) * page_stride;
-      kreg[r] = ld16(kbase + pb + kgo[r]);
-      vreg[r] = ld16(vbase + pb + vgo[r]);
-      vkeep[r] = nvalid - (kb + vkb[r]);
+      const int m = r * kWaves + w;
+      const bool second = (D == 128) ? (r != 0) : (w >= 2);
+      const size_t pb = (size_t)(second ? pg1 : pg0) * page_stride;
+      dma16(kbase + pb + kgo[r], stage + m * 1024);
+      dma16(vbase + pb + vgo[r], stage + C::K_STAGE + m * 1024);
     }
   };
-  auto lstore = [&](char* stage) {
+  // Zero the values of key slots >= nvalid of the block at kb (the block that
+  // holds the request's end), in a stage whose loads have completed.
+  auto zero_tail = [&](int kb, char* stage) {
+    const int nv = nvalid - kb;
 #pragma unroll
-    for (int r = 0; r < C::LOADS; ++r) {
-      st16(stage + kso[r], kreg[r]);
-      st16(stage + vso[r], vkeep[r] >= 8 ? vreg[r] : keep_first(vreg[r], vkeep[r]));
+    for (int k = 0; k < D / 64; ++k) {
+      const int idx = tid + k * kThreads;  // (page half, row, 16-byte half)
+      const int h = idx / (2 * D), d = (idx >> 1) % D, j = idx & 1;
+      const int keep = nv - (h * 16 + ((j ^ vswz(d)) << 3));
+      char* p = stage + C::K_STAGE + h * C::V_PAGE + d * 32 + j * 16;
+      if (keep < 8) st16(p, keep <= 0 ? u32x4{0, 0, 0, 0} : keep_first(ld16(p), keep));
     }
   };
-  auto compute = [&](const char* stage, int kb) {
-    if (kb >= wkend) return;
-    bf16x8 kop[2][KK];
+
+  // Software pipeline over (block, tile) steps.  QK(b,t) is S^T of key
+  // block b for tile t, SM(b,t) its softmax and PV(b,t) its O update.
+  // Iteration b of a wave runs two steps, each 16 MFMAs next to the softmax
+  // of one tile that they do not depend on:
+  //   step A: K(b+1) from LDS; MFMA QK(b+1,0), QK(b+1,1) | VALU SM(b,1)
+  //   step B: V(b) from LDS;   MFMA PV(b,0), PV(b,1)     | VALU SM(b+1,0)
+  // Operands stream: each 16-byte K or V fragment read from LDS feeds the
+  // MFMAs of both tiles and is dropped, so few are live at a time.  Blocks
+  // live in three LDS stages (block b in stage b % 3): iteration b reads
+  // stages (b+1)%3 and b%3 while block b+2 is fetched into the third, so one
+  // barrier per block suffices.
+  f32x4 s0[2], s1[2];  // QK outputs of tile 0 and tile 1 (two key halves each)
+  bf16x8 p0, p1;
+
+  // QK(b+1, 0..1) from stage stk into n0, n1
+  auto qk2 = [&](const char* stk, f32x4 (&n0)[2], f32x4 (&n1)[2]) {
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      kop[0][kk] = as_bf16x8(ld16(stage + kaddr[kk]));
-      kop[1][kk] = as_bf16x8(ld16(stage + kaddr[kk] + 4 * C::K_ROW));
-    }
-    f32x4 s0[NT], s1[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      s0[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      s1[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int h = 0; h < 2; ++h) {
+      n0[h] = f32x4{0.f, 0.f, 0.f, 0.f};
+      n1[h] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        s0[nt] = mfma(kop[0][kk], qop[nt][kk], s0[nt]);
-        s1[nt] = mfma(kop[1][kk], qop[nt][kk], s1[nt]);
+      for (int h = 0; h < 2; ++h) {
+        const bf16x8 k = as_bf16x8(ld16(stk + kaddr[kk] + h * 4 * C::K_ROW));
+        n0[h] = mfma(k, qop[0][kk], n0[h]);
+        n1[h] = mfma(k, qop[1][kk], n1[h]);
       }
-    bf16x8 pop[NT];
-    const bool need_mask = kb + 31 > wpmin;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const float sv[8] = {s0[nt][0], s0[nt][1], s0[nt][2], s0[nt][3],
-                           s1[nt][0], s1[nt][1], s1[nt][2], s1[nt][3]};
-      if (need_mask) {
-        const int lim = pos[nt] - (kb + 8 * g);  // key e visible iff e <= lim
-        const unsigned valid = lim < 0 ? 0u : (lim >= 7 ? 0xFFu : (2u << lim) - 1u);
-        pop[nt] = softmax_step<MT, true>(sv, valid, a.scale_log2, m_run[nt], l_run[nt], o[nt]);
-      } else {
-        pop[nt] = softmax_step<MT, false>(sv, 0xFFu, a.scale_log2, m_run[nt], l_run[nt], o[nt]);
-      }
-    }
+  };
+  // PV(b, 0..1) from stage stv
+  auto pv2 = [&](const char* stv) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const bf16x8 vop = as_bf16x8(ld16(stage + vaddr + mt * 16 * C::V_ROW));
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) o[nt][mt] = mfma(vop, pop[nt], o[nt][mt]);
+      const bf16x8 v = as_bf16x8(ld16(stv + vaddr + mt * 16 * 32));
+      o[0][mt] = mfma(v, p0, o[0][mt]);
+      o[1][mt] = mfma(v, p1, o[1][mt]);
     }
   };
+  auto lim_of = [&](int nt, int kb) { return pos[nt] - (kb + 8 * g); };
+  auto masked = [&](int kb) { return kb + 31 > wpmin; };
+  // SM(b,0) as one unit (prologue)
+  auto softmax_tile0 = [&](auto masked_t, int kb) {
+    constexpr bool M = decltype(masked_t)::value;
+    const int lim = lim_of(0, kb);
+    SmBlock sb = softmax_begin<M>(s0[0], s0[1], lim, c, cs[0]);
+    return softmax_end<MT, M>(sb, lim, c, inv_c, cs[0], o[0]);
+  };
+  auto step_a = [&](auto masked_t, const char* stk, int kb) {
+    constexpr bool M = decltype(masked_t)::value;
+    const int lim = lim_of(1, kb);
+    f32x4 n0[2], n1[2];
+    qk2(stk, n0, n1);
+    SmBlock sb = softmax_begin<M>(s1[0], s1[1], lim, c, cs[1]);
+    interleave_stream<2 * KK, 2>();
+    p1 = softmax_end<MT, M>(sb, lim, c, inv_c, cs[1], o[1]);
+    s0[0] = n0[0]; s0[1] = n0[1];
+    s1[0] = n1[0]; s1[1] = n1[1];
+  };
+  auto step_b = [&](auto masked_t, const char* stv, int kb_next) {
+    constexpr bool M = decltype(masked_t)::value;
+    const int lim = lim_of(0, kb_next);
+    pv2(stv);
+    SmBlock sb = softmax_begin<M>(s0[0], s0[1], lim, c, cs[0]);
+    interleave_stream<MT, 2>();
+    p0 = softmax_end<MT, M>(sb, lim, c, inv_c, cs[0], o[0]);
+  };
+  auto iteration = [&](auto sv_t, int b) {
+    constexpr int SV = decltype(sv_t)::value;
+    const char* stv = lds + SV * C::STAGE;
+    const char* stk = lds + ((SV + 1) % 3) * C::STAGE;
+    const int kb = it.key0 + b * 32;
+    if (masked(kb))
+      step_a(std::true_type{}, stk, kb);
+    else
+      step_a(std::false_type{}, stk, kb);
+    if (b + 1 < nbw) {
+      if (masked(kb + 32))
+        step_b(std::true_type{}, stv, kb + 32);
+      else
+        step_b(std::false_type{}, stv, kb + 32);
+    } else {
+      pv2(stv);  // the wave's last block
+    }
+  };
+  // Block b+2 is fetched at the start of iteration b into the stage that
+  // held block b-1; the barrier that ends the iteration waits for it.  The
+  // block after the current one is zeroed past the request's end if needed.
+  auto block = [&](auto sv_t, int b) {
+    constexpr int SV = decltype(sv_t)::value;
+    dma(it.key0 + min(b + 2, nb - 1) * 32, lds + ((SV + 2) % 3) * C::STAGE);
+    const int kn = it.key0 + (b + 1) * 32;
+    if (b + 1 < nb && kn + 32 > nvalid) zero_tail(kn, lds + ((SV + 1) % 3) * C::STAGE);
+    if (b < nbw) iteration(sv_t, b);
+    lds_dma_wait();
+    __syncthreads();
+  };
 
-  // Two LDS stages, loop unrolled by two so that stage offsets are constants.
-  // The next block's global loads are issued before the current block is
-  // computed and stored to the other stage after it; they are unconditional
-  // (the last block is loaded again at the end) so that the loop body is
-  // straight code with exact memory-counter waits.
-  const int nb = (it.key1 - it.key0 + 31) / 32;
-  char* st0 = lds;
-  char* st1 = lds + C::STAGE;
   if (nb > 0) {
-    gload(it.key0);
-    lstore(st0);
+    dma(it.key0, lds);
+    dma(it.key0 + min(1, nb - 1) * 32, lds + C::STAGE);
   }
+  lds_dma_wait();
   __syncthreads();
-  for (int b = 0; b < nb; b += 2) {
-    gload(it.key0 + min(b + 1, nb - 1) * 32);
-    compute(st0, it.key0 + b * 32);
-    lstore(st1);
+  if (nb > 0 && it.key0 + 32 > nvalid) {
+    zero_tail(it.key0, lds);
     __syncthreads();
-    if (b + 1 >= nb) break;
-    gload(it.key0 + min(b + 2, nb - 1) * 32);
-    compute(st1, it.key0 + (b + 1) * 32);
-    lstore(st0);
-    __syncthreads();
+  }
+  if (nbw > 0) {  // QK(0,0), QK(0,1), SM(0,0)
+    qk2(lds, s0, s1);
+    if (masked(it.key0))
+      p0 = softmax_tile0(std::true_type{}, it.key0);
+    else
+      p0 = softmax_tile0(std::false_type{}, it.key0);
+  }
+  for (int b = 0; b < nb;) {
+    block(Stage<0>{}, b);
+    if (++b >= nb) break;
+    block(Stage<1>{}, b);
+    if (++b >= nb) break;
+    block(Stage<2>{}, b);
+    ++b;
   }
 
   // epilogue
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) l_run[nt] = wave_sum_cols(l_run[nt]);
+  for (int nt = 0; nt < NT; ++nt) cs[nt].l = wave_sum_cols(cs[nt].l);
   if (it.group < 0) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -495,7 +698,7 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
       const int j = col / G;
       const int hg = col - j * G;
       uint16_t* orow = a.out + ((size_t)(rq.q_start + j) * a.hq + it.kvh * G + hg) * D;
-      const float inv = 1.f / l_run[nt];
+      const float inv = 1.f / cs[nt].l;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
         store_bf16x4(orow + mt * 16 + 4 * g, o[nt][mt][0] * inv, o[nt][mt][1] * inv,
@@ -512,8 +715,8 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
       if (col >= colend) continue;
       const int cl = col - it.col0;
       if (g == 0) {
-        st_dev(rec + cl, m_run[nt]);
-        st_dev(rec + Cn + cl, l_run[nt]);
+        st_dev(rec + cl, cs[nt].m);
+        st_dev(rec + Cn + cl, cs[nt].l);
       }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
