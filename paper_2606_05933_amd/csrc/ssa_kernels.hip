@@ -72,8 +72,14 @@ __device__ __forceinline__ void dma16(const void* g, const char* l) {
   const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)l;
   asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(a) : "memory");
 }
-// s_waitcnt vmcnt(0): this wave's LDS copies (and loads) have landed.
-__device__ __forceinline__ void lds_dma_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// s_waitcnt vmcnt(N): all but this wave's N most recent vector-memory
+// operations (LDS copies included) have completed.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+__device__ __forceinline__ void lds_dma_wait() { vm_wait<0>(); }
 
 constexpr float kLog2e = 1.4426950408889634f;
 // The running maximum of a column is raised only when a block's logit exceeds
@@ -82,6 +88,11 @@ constexpr float kLog2e = 1.4426950408889634f;
 // reference, so the result does not depend on it.
 constexpr float kRescaleThreshold = 8.0f;
 constexpr float kNegInf = -__builtin_inff();
+// LDS stages of the chunk pipeline: key block b lives in stage b % kChunkStages
+// and is fetched kChunkStages - 1 blocks ahead.
+constexpr int kChunkStages = 4;
+// LDS operand fragments the chunk steps keep in flight ahead of their MFMAs.
+constexpr int kReadAhead = 2;
 
 template <int D>
 struct Cfg {
@@ -93,9 +104,9 @@ struct Cfg {
   static constexpr int V_PAGE = D * 32;      // LDS bytes of one value page: D rows of 16 slots
   static constexpr int V_STAGE = 2 * V_PAGE;
   static constexpr int STAGE = K_STAGE + V_STAGE;
-  static constexpr int LDS_CHUNK = 3 * STAGE;  // three stages (chunk pipeline)
+  static constexpr int LDS_CHUNK = kChunkStages * STAGE;
   static constexpr int LDS_DECODE = kWaves * (32 + 16 * D) * 4;
-  static constexpr int LDS = LDS_CHUNK > LDS_DECODE ? LDS_CHUNK : LDS_DECODE;
+  static constexpr int LDS = (LDS_CHUNK > LDS_DECODE + 16 ? LDS_CHUNK : LDS_DECODE + 16);
   static constexpr int LOADS = D / 64;       // 16-byte K (and V) chunks per thread per block
   static constexpr int KROWS_PER_LOAD = 64 / CPR;  // key rows one wave-wide 1 KB load fills
 };
@@ -305,8 +316,10 @@ __device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntr
 // the stores, take a ticket; the last of the group's items merges and resets
 // the ticket for the next launch.
 template <int D>
-__device__ void finish_split(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq) {
-  __shared__ int s_last;
+__device__ void finish_split(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
+                             char* lds) {
+  // a word of the kernel's LDS buffer past both items' working areas
+  int& s_last = *reinterpret_cast<int*>(lds + Cfg<D>::LDS - 16);
   const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + a.off_groups)[it.group];
   int* tickets = reinterpret_cast<int*>(a.ws);
   wait_vm_stores();
@@ -428,15 +441,15 @@ __device__ __forceinline__ bf16x8 softmax_end(SmBlock& b, int lim, float c, floa
 // while few fragments are live.
 constexpr int kMaskMfma = 0x008, kMaskValu = 0x002 | 0x400, kMaskDsRead = 0x100;
 
-template <int READS, int VALU_PER_MFMA>
+template <int READS, int VALU_PER_MFMA, int AHEAD = 2>
 __device__ __forceinline__ void interleave_stream() {
-  __builtin_amdgcn_sched_group_barrier(kMaskDsRead, 2, 0);
+  __builtin_amdgcn_sched_group_barrier(kMaskDsRead, AHEAD, 0);
   __builtin_amdgcn_sched_group_barrier(kMaskValu, 4, 0);
 #pragma unroll
   for (int i = 0; i < READS; ++i) {
     __builtin_amdgcn_sched_group_barrier(kMaskMfma, 1, 0);
     __builtin_amdgcn_sched_group_barrier(kMaskValu, VALU_PER_MFMA, 0);
-    if (i + 2 < READS) __builtin_amdgcn_sched_group_barrier(kMaskDsRead, 1, 0);
+    if (i + AHEAD < READS) __builtin_amdgcn_sched_group_barrier(kMaskDsRead, 1, 0);
     __builtin_amdgcn_sched_group_barrier(kMaskMfma, 1, 0);
     __builtin_amdgcn_sched_group_barrier(kMaskValu, VALU_PER_MFMA, 0);
   }
@@ -571,9 +584,10 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   //   step B: V(b) from LDS;   MFMA PV(b,0), PV(b,1)     | VALU SM(b+1,0)
   // Operands stream: each 16-byte K or V fragment read from LDS feeds the
   // MFMAs of both tiles and is dropped, so few are live at a time.  Blocks
-  // live in three LDS stages (block b in stage b % 3): iteration b reads
-  // stages (b+1)%3 and b%3 while block b+2 is fetched into the third, so one
-  // barrier per block suffices.
+  // live in kChunkStages LDS stages (block b in stage b % S): iteration b
+  // reads stages b%S and (b+1)%S, and fetches block b+S-1 into the stage of
+  // block b-1, which every wave finished reading before the barrier that
+  // ended iteration b-1; one barrier per block suffices.
   f32x4 s0[2], s1[2];  // QK outputs of tile 0 and tile 1 (two key halves each)
   bf16x8 p0, p1;
 
@@ -617,7 +631,7 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     f32x4 n0[2], n1[2];
     qk2(stk, n0, n1);
     SmBlock sb = softmax_begin<M>(s1[0], s1[1], lim, c, cs[1]);
-    interleave_stream<2 * KK, 2>();
+    interleave_stream<2 * KK, 2, kReadAhead>();
     p1 = softmax_end<MT, M>(sb, lim, c, inv_c, cs[1], o[1]);
     s0[0] = n0[0]; s0[1] = n0[1];
     s1[0] = n1[0]; s1[1] = n1[1];
@@ -627,13 +641,13 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     const int lim = lim_of(0, kb_next);
     pv2(stv);
     SmBlock sb = softmax_begin<M>(s0[0], s0[1], lim, c, cs[0]);
-    interleave_stream<MT, 2>();
+    interleave_stream<MT, 2, kReadAhead>();
     p0 = softmax_end<MT, M>(sb, lim, c, inv_c, cs[0], o[0]);
   };
   auto iteration = [&](auto sv_t, int b) {
     constexpr int SV = decltype(sv_t)::value;
     const char* stv = lds + SV * C::STAGE;
-    const char* stk = lds + ((SV + 1) % 3) * C::STAGE;
+    const char* stk = lds + ((SV + 1) % kChunkStages) * C::STAGE;
     const int kb = it.key0 + b * 32;
     if (masked(kb))
       step_a(std::true_type{}, stk, kb);
@@ -648,24 +662,34 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
       pv2(stv);  // the wave's last block
     }
   };
-  // Block b+2 is fetched at the start of iteration b into the stage that
-  // held block b-1; the barrier that ends the iteration waits for it.  The
-  // block after the current one is zeroed past the request's end if needed.
+  // Every iteration issues the same number of LDS copies per thread (the
+  // fetch is clamped to the last block), so the copies still allowed in
+  // flight at a barrier are an exact count: the barrier ending iteration b
+  // needs blocks up to b+2 (read by iteration b+1) and leaves the fetches of
+  // the S-3 most recent iterations outstanding.  The block after the current
+  // one is zeroed past the request's end if needed (it has landed).
+  constexpr int kInFlight = (kChunkStages - 3) * 2 * C::LOADS;
   auto block = [&](auto sv_t, int b) {
     constexpr int SV = decltype(sv_t)::value;
-    dma(it.key0 + min(b + 2, nb - 1) * 32, lds + ((SV + 2) % 3) * C::STAGE);
+    constexpr int S = kChunkStages;
+    dma(it.key0 + min(b + S - 1, nb - 1) * 32, lds + ((SV + S - 1) % S) * C::STAGE);
     const int kn = it.key0 + (b + 1) * 32;
-    if (b + 1 < nb && kn + 32 > nvalid) zero_tail(kn, lds + ((SV + 1) % 3) * C::STAGE);
+    if (b + 1 < nb && kn + 32 > nvalid) zero_tail(kn, lds + ((SV + 1) % S) * C::STAGE);
     if (b < nbw) iteration(sv_t, b);
-    lds_dma_wait();
+    vm_wait<kInFlight>();
     __syncthreads();
   };
 
-  if (nb > 0) {
-    dma(it.key0, lds);
-    dma(it.key0 + min(1, nb - 1) * 32, lds + C::STAGE);
-  }
+  // The query fragments have landed before the first copy is issued: the
+  // compiler's own waits for them would otherwise count the copies (which it
+  // does not see) and stall on them inside the loop.
   lds_dma_wait();
+  if (nb > 0) {
+#pragma unroll
+    for (int k = 0; k < kChunkStages - 1; ++k)
+      dma(it.key0 + min(k, nb - 1) * 32, lds + k * C::STAGE);
+  }
+  vm_wait<kInFlight>();  // blocks 0 and 1 have landed
   __syncthreads();
   if (nb > 0 && it.key0 + 32 > nvalid) {
     zero_tail(it.key0, lds);
@@ -678,14 +702,24 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     else
       p0 = softmax_tile0(std::false_type{}, it.key0);
   }
+  static_assert(kChunkStages >= 3 && kChunkStages <= 5, "pipeline depth");
   for (int b = 0; b < nb;) {
     block(Stage<0>{}, b);
     if (++b >= nb) break;
     block(Stage<1>{}, b);
     if (++b >= nb) break;
     block(Stage<2>{}, b);
-    ++b;
+    if (++b >= nb) break;
+    if (kChunkStages >= 4) {
+      block(Stage<(kChunkStages >= 4 ? 3 : 0)>{}, b);
+      if (++b >= nb) break;
+    }
+    if (kChunkStages >= 5) {
+      block(Stage<(kChunkStages >= 5 ? 4 : 0)>{}, b);
+      ++b;
+    }
   }
+  lds_dma_wait();  // no copy may land after this workgroup has left
 
   // epilogue
 #pragma unroll
@@ -724,7 +758,7 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
         for (int jj = 0; jj < 4; ++jj)
           st_dev(rec + 2 * Cn + (int64_t)cl * D + mt * 16 + 4 * g + jj, o[nt][mt][jj]);
     }
-    finish_split<D>(a, it, rq);
+    finish_split<D>(a, it, rq, lds);
   }
 }
 
@@ -876,7 +910,7 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
                    acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
     }
   }
-  if (rec) finish_split<D>(a, it, rq);
+  if (rec) finish_split<D>(a, it, rq, lds);
 }
 
 template <int D>
