@@ -18,6 +18,9 @@ Other modes (all single GPU):
   --sweep OUT        latency-vs-chunk-size table of every workload (JSON lines)
   --copy-probe       plain 1 GiB device copies (the scale of the traffic counters)
   --only-attention   time the attention launch alone (for counter runs)
+  --traffic-json OUT --traffic-json-inputs F W CF CW
+                     HBM traffic summary from rocprofv3 FETCH_SIZE / WRITE_SIZE CSVs
+  --sweep-md JSONL   markdown tables of a --sweep file
 """
 from __future__ import annotations
 
@@ -341,6 +344,80 @@ def main_only_attention(args):
                       "chunk_flops": info.chunk_flops, "launches": args.steps}), flush=True)
 
 
+def _pmc_rows(path, counter):
+    import csv
+    rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+    return rows
+
+
+def main_traffic_json(args):
+    """HBM traffic of the attention launch from rocprofv3 --pmc runs: FETCH_SIZE
+    and WRITE_SIZE (KiB per dispatch) of mixed_attention_kernel, each scaled by
+    what the same counter reads for a plain 1 GiB device copy."""
+    fetch, write, cfetch, cwrite = args.traffic_json_inputs
+    def kernel_avg(path, counter, name):
+        v = [float(r["Counter_Value"]) for r in _pmc_rows(path, counter) if name in r["Kernel_Name"]]
+        if not v:
+            raise SystemExit(f"no {counter} rows for {name} in {path}")
+        return statistics.mean(v), len(v)
+    f_kib, n_f = kernel_avg(fetch, "FETCH_SIZE", "mixed_attention_kernel")
+    w_kib, n_w = kernel_avg(write, "WRITE_SIZE", "mixed_attention_kernel")
+    copy_kib = float(1 << 20)  # the copy probe moves 1 GiB
+    cf, _ = kernel_avg(cfetch, "FETCH_SIZE", "copyBuffer")
+    cw, _ = kernel_avg(cwrite, "WRITE_SIZE", "copyBuffer")
+    out = {"kernel": "mixed_attention_kernel", "workload": DESCR[args.workload],
+           "kernel_source_sha256": sha256_file(KERNEL_SRC),
+           "fetch_kib": round(f_kib, 1), "write_kib": round(w_kib, 1), "dispatches": [n_f, n_w],
+           "copy_fetch_factor": round(cf / copy_kib, 4), "copy_write_factor": round(cw / copy_kib, 4),
+           "commands": ["rocprofv3 --pmc FETCH_SIZE --output-format csv -- python3 bench.py --no-cpu-baseline",
+                        "rocprofv3 --pmc WRITE_SIZE --output-format csv -- python3 bench.py --no-cpu-baseline",
+                        "rocprofv3 --pmc FETCH_SIZE --output-format csv -- python3 bench.py --copy-probe --steps 3",
+                        "rocprofv3 --pmc WRITE_SIZE --output-format csv -- python3 bench.py --copy-probe --steps 3"]}
+    out["traffic_bytes"] = round((out["fetch_kib"] / out["copy_fetch_factor"]
+                                  + out["write_kib"] / out["copy_write_factor"]) * 1024)
+    json.dump(out, open(args.traffic_json, "w"), indent=1)
+    print(json.dumps(out))
+
+
+def main_sweep_md(args):
+    """Markdown tables of a --sweep JSON-lines file, one per workload."""
+    rows = [json.loads(l) for l in open(args.sweep_md) if l.strip()]
+    # the row that is the workload's own configuration (multi: chunks scaled by c / 512)
+    own = {"tiny": (64, 192), "l8b": (512, 2048), "l70b": (1024, 32768), "multi": (512, None)}
+    lines = []
+    for name in workload_names_in(rows):
+        lines.append(f"### {name}: {DESCR.get(name, name)}\n")
+        lines.append("| chunk c | prefix u | scene | tokens | attention us (cold) | attention us (warm) | "
+                     "kv_append us | plan us | step us | tokens/s | decode-only us | chunk-only us | "
+                     "HBM GB/s (% of 8 TB/s) | MFMA TFLOP/s (% of 2.5 PF) |")
+        lines.append("|---|---|---|---|---|---|---|---|---|---|---|---|---|---|")
+        for r in rows:
+            if r["workload"] != name:
+                continue
+            segs = r.get("segments", {})
+            dec = segs.get("decode", {}).get("us", "")
+            chk = segs.get("chunk", {}).get("us", "")
+            mark = " (config)" if own.get(name) == (r["chunk"], r["prefix"]) else ""
+            hbm = r["hbm_GBps"]
+            tf = r["mfma_TFLOPs"]
+            lines.append(
+                f"| {r['chunk']}{mark} | "
+                f"{r['prefix'] if r['prefix'] is not None else 'drawn'} | {r['scene']} | {r['tokens']} | "
+                f"{r['attention_us']} | {r['attention_warm_us']} | {r['kv_append_us']} | {r['plan_us']} | "
+                f"{r['step_us']} | {r['tokens_per_s']:.3g} | {dec} | {chk} | "
+                f"{hbm} ({hbm / HBM_PEAK_GBS:.0%}) | {tf} ({tf / MFMA_BF16_PEAK_TFLOPS:.0%}) |")
+        lines.append("")
+    print("\n".join(lines))
+
+
+def workload_names_in(rows):
+    seen = []
+    for r in rows:
+        if r["workload"] not in seen:
+            seen.append(r["workload"])
+    return seen
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__,
                                  formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -360,7 +437,17 @@ def main():
     ap.add_argument("--sweep-workloads", default=None)
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--only-attention", action="store_true")
+    ap.add_argument("--traffic-json", metavar="OUT", default=None,
+                    help="write the HBM traffic summary from four rocprofv3 counter CSVs")
+    ap.add_argument("--traffic-json-inputs", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH",
+                                                               "COPY_WRITE"))
+    ap.add_argument("--sweep-md", metavar="JSONL", default=None,
+                    help="print the latency-vs-chunk tables of a --sweep file")
     args = ap.parse_args()
+    if args.traffic_json:
+        return main_traffic_json(args)
+    if args.sweep_md:
+        return main_sweep_md(args)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU: this attention path has no multi-GPU mode "
