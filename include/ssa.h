@@ -96,8 +96,9 @@ typedef struct ssa_shape {
  *                    item: 32, 64 or 128 (default 128)
  *   chunk_split_keys if > 0, a chunk tile's key range is cut into pieces of this
  *                    many keys (multiple of 32); default: chosen by the planner
- *   decode_split_keys keys per decode work item (multiple of 32); default:
- *                    chosen by the planner
+ *   decode_split_keys a decode key range of k keys is cut into
+ *                    max(1, round(k / decode_split_keys)) equal pieces, each a
+ *                    multiple of 32 keys (multiple of 32; default 4096)
  *   num_cus          compute units the planner balances for (default 256)
  *   num_xcds         if > 1, die-aware placement: workgroups are taken to be
  *                    dealt to num_xcds dies round-robin (workgroup b on die
@@ -105,7 +106,11 @@ typedef struct ssa_shape {
  *                    (one request and kv head of a chunk) go to one die
  *                    (default 1: off; on MI355X it measured no faster)
  *   mix_order        1 = all chunk items (longest first) before the decode
- *                    items (default), 2 = the two kinds interleaved
+ *                    items (default), 2 = the two kinds interleaved, 3 = paired:
+ *                    the first num_cus chunk items, then decode items for the
+ *                    second slot of every compute unit, then the rest
+ *                    interleaved (workgroups 0 .. num_cus-1 are taken to land on
+ *                    distinct units, the next num_cus on their second slots)
  */
 typedef struct ssa_tuning {
   int32_t chunk_tile_cols;

@@ -32,15 +32,16 @@ constexpr double kHbmRate = 8.0e12 * 0.7;
 // each piece costs a partial record of ncols*(D+2) floats written and read back.
 constexpr int kMinChunkSplitKeys = 1024;
 constexpr int kMaxChunkSplits = 16;
-// Decode key ranges are cut into items of at least kMinDecodeSplitBlocks blocks,
-// aiming at about kDecodeItemsPerCu items per compute unit: enough to balance
-// contexts of different lengths, few enough that merging partials stays cheap.
-constexpr int kMinDecodeSplitBlocks = 128;
-constexpr int kDecodeItemsPerCu = 1;
+// Decode key ranges are cut into equal pieces of about this many keys: long
+// enough that the load latency at the start of an item is amortised over 32
+// blocks per wave, short enough that long and short contexts balance over the
+// compute units; partial records cost G*(D+2) floats per piece.
+constexpr int kDefaultDecodeSplitKeys = 4096;
 
 constexpr int kDefaultXcds = 1;
 constexpr int kOrderChunkFirst = 1;
 constexpr int kOrderInterleave = 2;
+constexpr int kOrderPaired = 3;
 
 struct Tuning {
   int tile_cols, chunk_split_keys, decode_split_keys, num_cus, num_xcds, mix_order;
@@ -70,7 +71,7 @@ int resolve_tuning(const ssa_tuning* t, Tuning* out) {
     if (t->decode_split_keys < 0 || t->decode_split_keys % kBlockKeys) return SSA_ERR_TUNING;
     if (t->num_cus < 0 || t->num_cus > 4096) return SSA_ERR_TUNING;
     if (t->num_xcds < 0 || t->num_xcds > 64) return SSA_ERR_TUNING;
-    if (t->mix_order < 0 || t->mix_order > 2) return SSA_ERR_TUNING;
+    if (t->mix_order < 0 || t->mix_order > 3) return SSA_ERR_TUNING;
     r.chunk_split_keys = t->chunk_split_keys;
     r.decode_split_keys = t->decode_split_keys;
     if (t->num_cus) r.num_cus = t->num_cus;
@@ -138,8 +139,13 @@ void longest_first(const std::vector<WorkItem>& items, const std::vector<uint16_
 }
 
 // Chunk and decode index lists of one queue: all chunk items then the decode
-// items, or the two merged in proportion.
-void mix(const std::vector<uint32_t>& a, const std::vector<uint32_t>& b, int order,
+// items, the two merged in proportion, or paired: the dispatcher gives the
+// first `cus` workgroups one compute unit each and the next `cus` the second
+// slot of the same units, so the first min(cus, chunk items) chunk items are
+// followed by enough decode items to fill the second slots (every unit then
+// runs one MFMA-bound and one HBM-bound item side by side), and the rest
+// follows merged in proportion.
+void mix(const std::vector<uint32_t>& a, const std::vector<uint32_t>& b, int order, int cus,
          std::vector<uint32_t>* out) {
   if (order == kOrderChunkFirst) {
     out->insert(out->end(), a.begin(), a.end());
@@ -147,10 +153,17 @@ void mix(const std::vector<uint32_t>& a, const std::vector<uint32_t>& b, int ord
     return;
   }
   size_t i = 0, j = 0;
+  if (order == kOrderPaired) {
+    i = std::min(a.size(), (size_t)cus);
+    j = std::min(b.size(), 2 * (size_t)cus - i);
+    out->insert(out->end(), a.begin(), a.begin() + i);
+    out->insert(out->end(), b.begin(), b.begin() + j);
+  }
+  const size_t i0 = i, j0 = j;
   while (i < a.size() || j < b.size()) {
     // take from the list that is behind in the fraction of its items emitted
-    const bool take_a =
-        j >= b.size() || (i < a.size() && (double)i * b.size() <= (double)j * a.size());
+    const bool take_a = j >= b.size() || (i < a.size() && (double)(i - i0) * (b.size() - j0) <=
+                                                                (double)(j - j0) * (a.size() - i0));
     out->push_back(take_a ? a[i++] : b[j++]);
   }
 }
@@ -217,14 +230,14 @@ void order_items(const std::vector<WorkItem>& items, const std::vector<double>& 
         load[best] += t[k];
       }
       std::vector<std::vector<uint32_t>> q(X);
-      for (int x = 0; x < X; ++x) mix(sch[x], sde[x], tu.mix_order, &q[x]);
+      for (int x = 0; x < X; ++x) mix(sch[x], sde[x], tu.mix_order, tu.num_cus / X, &q[x]);
       for (size_t r = 0; seq->size() < N; ++r)
         for (int x = 0; x < X; ++x)
           if (r < q[x].size()) seq->push_back(q[x][r]);
       return;
     }
   }
-  mix(ch, de, tu.mix_order, seq);
+  mix(ch, de, tu.mix_order, tu.num_cus, seq);
 }
 
 int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int32_t n,
@@ -314,12 +327,7 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   const double makespan =
       chunk_time_total / ncu + decode_blocks * kBlockKeys * D * 4.0 / kHbmRate;
 
-  int dec_split = tu.decode_split_keys;
-  if (dec_split == 0) {
-    int64_t blocks = (int64_t)std::ceil(decode_blocks / (double)(ncu * kDecodeItemsPerCu));
-    blocks = std::max<int64_t>(kMinDecodeSplitBlocks, ceil_div(blocks, kWaves) * kWaves);
-    dec_split = (int)std::min<int64_t>(blocks * kBlockKeys, kMaxLen);
-  }
+  const int dec_split = tu.decode_split_keys > 0 ? tu.decode_split_keys : kDefaultDecodeSplitKeys;
 
   std::vector<WorkItem> raw;
   std::vector<double> est_t;
@@ -374,7 +382,10 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
       }
     } else if (c == 1) {
       const int keys = u + 1;
-      const int nsplit = (int)ceil_div(keys, dec_split);
+      // round(keys / dec_split) equal pieces (at least one), block aligned
+      int nsplit = std::max(1, (int)(((int64_t)keys + dec_split / 2) / dec_split));
+      const int piece = (int)ceil_div(ceil_div(keys, nsplit), kBlockKeys) * kBlockKeys;
+      nsplit = (int)ceil_div(keys, piece);
       for (int h = 0; h < Hkv; ++h) {
         const int32_t grp = nsplit > 1 ? add_group(nsplit, G) : -1;
         for (int sp = 0; sp < nsplit; ++sp) {
@@ -384,8 +395,8 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
           it.kvh = h;
           it.col0 = 0;
           it.ncols = G;
-          it.key0 = sp * dec_split;
-          it.key1 = std::min(keys, (sp + 1) * dec_split);
+          it.key0 = sp * piece;
+          it.key1 = std::min(keys, (sp + 1) * piece);
           it.group = grp;
           it.split = sp;
           raw.push_back(it);

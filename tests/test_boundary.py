@@ -140,6 +140,24 @@ def test_plan_partitions_under_tuning(tile, csplit):
     assert info.num_items == len(items)
 
 
+@pytest.mark.parametrize("order", [1, 2, 3])
+@pytest.mark.parametrize("cus", [4, 256])
+def test_plan_partitions_under_every_launch_order(order, cus):
+    shape, q_len, ctx_len = workload.workload_lengths("multi", seed=5)
+    tu = ssa.make_tuning(mix_order=order, num_cus=cus)
+    info, items = check_plan_covers_batch(shape.hq, shape.hkv, shape.d, q_len, ctx_len, tu)
+    is_chunk = items["kind"] == 0
+    nc, nd = int(is_chunk.sum()), int((~is_chunk).sum())
+    assert nc > 0 and nd > 0
+    if order == 1:  # all chunk items first
+        assert is_chunk[:nc].all()
+    if order == 3:  # min(cus, chunk items) chunk items, then decode items up to 2 * cus
+        first = min(cus, nc)
+        second = min(nd, 2 * cus - first)
+        assert is_chunk[:first].all()
+        assert not is_chunk[first:first + second].any()
+
+
 def test_plan_on_generated_workloads():
     for name in workload.WORKLOADS:
         shape, q_len, ctx_len = workload.workload_lengths(name, seed=3)
