@@ -8,11 +8,13 @@
 //    128 columns = (token, q head of the kv group) pairs of one request and kv
 //    head; each of the 4 waves owns 32 columns as two 16-wide MFMA N tiles, so
 //    that a wave fits in 256 registers and two workgroups share a CU.
-//    Key blocks of 32 keys (two 16-slot pages) are staged through LDS, double
-//    buffered, and shared by the 4 waves.  S^T = K Q^T and O^T += V^T P run on
-//    v_mfma_f32_16x16x32_bf16 with fp32 accumulation; softmax is online, in
-//    base 2, fp32.  Causal masking is applied only on blocks that cross the
-//    diagonal.
+//    Key blocks of 32 keys (two 16-slot pages) are copied global -> LDS
+//    (global_load_lds_dwordx4) into four stages, three blocks ahead, and shared
+//    by the 4 waves.  S^T = K Q^T and O^T += V^T P run on
+//    v_mfma_f32_16x16x32_bf16 with fp32 accumulation; each wave alternates the
+//    two tiles so that a tile's softmax (online, base 2, fp32) sits beside the
+//    other tile's MFMAs.  Causal masking is applied only on blocks that cross
+//    the diagonal.
 //
 //  * decode split (c_i == 1; Tab. 1 x4/x5): the G q heads of one kv head are the
 //    N columns of the same MFMA formulation, so each K/V byte read from HBM is
