@@ -110,7 +110,9 @@ typedef struct ssa_shape {
  *                    the first num_cus chunk items, then decode items for the
  *                    second slot of every compute unit, then the rest
  *                    interleaved (workgroups 0 .. num_cus-1 are taken to land on
- *                    distinct units, the next num_cus on their second slots)
+ *                    distinct units, the next num_cus on their second slots),
+ *                    4 = as 3, then the other decode items, then the other
+ *                    chunk items
  */
 typedef struct ssa_tuning {
   int32_t chunk_tile_cols;

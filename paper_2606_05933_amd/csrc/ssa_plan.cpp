@@ -42,6 +42,7 @@ constexpr int kDefaultXcds = 1;
 constexpr int kOrderChunkFirst = 1;
 constexpr int kOrderInterleave = 2;
 constexpr int kOrderPaired = 3;
+constexpr int kOrderPairedDecodeFirst = 4;
 
 struct Tuning {
   int tile_cols, chunk_split_keys, decode_split_keys, num_cus, num_xcds, mix_order;
@@ -71,7 +72,7 @@ int resolve_tuning(const ssa_tuning* t, Tuning* out) {
     if (t->decode_split_keys < 0 || t->decode_split_keys % kBlockKeys) return SSA_ERR_TUNING;
     if (t->num_cus < 0 || t->num_cus > 4096) return SSA_ERR_TUNING;
     if (t->num_xcds < 0 || t->num_xcds > 64) return SSA_ERR_TUNING;
-    if (t->mix_order < 0 || t->mix_order > 3) return SSA_ERR_TUNING;
+    if (t->mix_order < 0 || t->mix_order > 4) return SSA_ERR_TUNING;
     r.chunk_split_keys = t->chunk_split_keys;
     r.decode_split_keys = t->decode_split_keys;
     if (t->num_cus) r.num_cus = t->num_cus;
@@ -144,7 +145,9 @@ void longest_first(const std::vector<WorkItem>& items, const std::vector<uint16_
 // slot of the same units, so the first min(cus, chunk items) chunk items are
 // followed by enough decode items to fill the second slots (every unit then
 // runs one MFMA-bound and one HBM-bound item side by side), and the rest
-// follows merged in proportion.
+// follows merged in proportion or, for order 4, the rest of the decode items
+// before the rest of the chunk items (units go back to two chunk tiles each
+// once the decode work is gone).
 void mix(const std::vector<uint32_t>& a, const std::vector<uint32_t>& b, int order, int cus,
          std::vector<uint32_t>* out) {
   if (order == kOrderChunkFirst) {
@@ -153,11 +156,16 @@ void mix(const std::vector<uint32_t>& a, const std::vector<uint32_t>& b, int ord
     return;
   }
   size_t i = 0, j = 0;
-  if (order == kOrderPaired) {
+  if (order == kOrderPaired || order == kOrderPairedDecodeFirst) {
     i = std::min(a.size(), (size_t)cus);
     j = std::min(b.size(), 2 * (size_t)cus - i);
     out->insert(out->end(), a.begin(), a.begin() + i);
     out->insert(out->end(), b.begin(), b.begin() + j);
+    if (order == kOrderPairedDecodeFirst) {  // then the other decode items, then the chunk items
+      out->insert(out->end(), b.begin() + j, b.end());
+      out->insert(out->end(), a.begin() + i, a.end());
+      return;
+    }
   }
   const size_t i0 = i, j0 = j;
   while (i < a.size() || j < b.size()) {

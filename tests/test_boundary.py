@@ -140,7 +140,7 @@ def test_plan_partitions_under_tuning(tile, csplit):
     assert info.num_items == len(items)
 
 
-@pytest.mark.parametrize("order", [1, 2, 3])
+@pytest.mark.parametrize("order", [1, 2, 3, 4])
 @pytest.mark.parametrize("cus", [4, 256])
 def test_plan_partitions_under_every_launch_order(order, cus):
     shape, q_len, ctx_len = workload.workload_lengths("multi", seed=5)
@@ -151,11 +151,14 @@ def test_plan_partitions_under_every_launch_order(order, cus):
     assert nc > 0 and nd > 0
     if order == 1:  # all chunk items first
         assert is_chunk[:nc].all()
-    if order == 3:  # min(cus, chunk items) chunk items, then decode items up to 2 * cus
+    if order in (3, 4):  # min(cus, chunk items) chunk items, then decode items up to 2 * cus
         first = min(cus, nc)
         second = min(nd, 2 * cus - first)
         assert is_chunk[:first].all()
         assert not is_chunk[first:first + second].any()
+    if order == 4:  # then every other decode item, then the other chunk items
+        assert not is_chunk[first:first + nd].any()
+        assert is_chunk[first + nd:].all()
 
 
 def test_plan_on_generated_workloads():
