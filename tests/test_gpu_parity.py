@@ -81,6 +81,9 @@ SMALL = [
     (16, 1, 64, [(40, 60), (1, 500)]),                               # G = 16
     (4, 4, 128, [(300, 77), (1, 129)]),                               # G = 1, D = 128
     (12, 4, 64, [(2, 0), (3, 1), (65, 1023), (1, 0)]),                # G = 3, D = 64
+    (64, 4, 128, [(129, 0), (1, 0), (3, 700)]),                       # G = 16, D = 128
+    (8, 8, 64, [(2048, 0), (1, 1)]),                                  # long chunk from empty
+    (32, 8, 128, [(1, 65535), (1, 12287), (40, 20000)]),              # many decode pieces
 ]
 
 
@@ -125,6 +128,23 @@ def test_tuning_variants_match_oracle(torch_dev, tile, csplit, dsplit):
     b = small(32, 8, 128, [(300, 1500), (1, 3000), (1, 100), (45, 0)], seed=11, name="tuned")
     full_parity(b, ssa.make_tuning(chunk_tile_cols=tile, chunk_split_keys=csplit,
                                    decode_split_keys=dsplit))
+
+
+def test_launch_orders_give_bitwise_identical_outputs(torch_dev):
+    """The launch order only changes which workgroup runs when: every order
+    gives the same bytes (splits merge in split order)."""
+    import torch
+    from paper_2606_05933_amd import ssa, workload
+    b = workload.make_workload("multi", seed=4)
+    db = run(b)
+    ref = db.out.clone()
+    for order in (2, 3, 4):
+        for cus in (256, 7):
+            db.plan(ssa.make_tuning(mix_order=order, num_cus=cus))
+            db.out.zero_()
+            db.attention()
+            torch.cuda.synchronize()
+            assert torch.equal(db.out.view(torch.int16), ref.view(torch.int16)), (order, cus)
 
 
 def test_scenes_pure_decode_and_pure_prefill(torch_dev):
@@ -174,6 +194,8 @@ def sampled_parity(b, n_chunk_rows=24, heads_per_row=4, seed=0):
 @pytest.mark.parametrize("name,chunk,prefix", [
     ("multi", None, None), ("l70b", None, None),
     ("l8b_sweep", 2048, 6144), ("l8b_sweep", 128, 0), ("l8b_sweep", 1024, 2048),
+    ("l8b_sweep", 2048, 0), ("l8b_sweep", 256, 6144), ("multi", 1024, None),
+    ("l70b", 2048, None), ("l8b", 2048, None),
 ])
 def test_full_size_sampled_parity(torch_dev, name, chunk, prefix):
     from paper_2606_05933_amd import workload
