@@ -3,16 +3,18 @@
 
 A step is the whole path for one batch B = {(c_i, u_i)} (SlidingServe Sec. 3.2):
 host planning (routing by Eq. 2, work items) into a pinned device-mapped plan
-buffer, ``ssa_kv_append`` and the single ``ssa_mixed_attention`` launch.  The default
+buffer and one ``ssa_append_attention`` launch (kv_append and the mixed
+attention of all requests in one kernel; the same results, bit for bit, as
+``ssa_kv_append`` followed by ``ssa_mixed_attention``).  The default
 workload is the Llama-3-8B-shaped mixed batch (32 q / 8 kv heads, D = 128, page
 16; one 512-token chunk on a 2048-token prefix plus 64 decodes with contexts
 uniform in [512, 4096]), synthetic and seeded; inputs are resident in HBM before
 the timed region starts.
 
 Printed on stdout, as the last line: one JSON object with the metric (µs per
-iteration), the dominant kernel's roofline (live HIP-event timing of the
-attention launch against MI355X's 8 TB/s HBM peak), and the CPU oracle timed on
-this host (a reported baseline, not the target).
+iteration), the dominant kernel's roofline (live timing of the fused launch,
+from events the kernel stamps itself, against MI355X's 8 TB/s HBM peak), and
+the CPU oracle timed on this host (a reported baseline, not the target).
 
 Other modes (all single GPU):
   --sweep OUT        latency-vs-chunk-size table of every workload (JSON lines)
@@ -39,7 +41,7 @@ METRIC = "mixed prefill+decode attention µs/iter vs chunk size; % HBM / MFMA ro
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_05933_amd", "csrc", "ssa_kernels.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_mixed_attention_l8b.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_append_attention_l8b.json")
 
 DESCR = {
     "tiny": "tiny mixed: 8q/8kv/D64, 1 chunk (u=192,c=64) + 4 decodes u in {128,256,384,512}",
@@ -130,8 +132,8 @@ def cpu_baseline(b, min_seconds=10.0, max_reps=30):
 
 
 def traffic_bytes():
-    """HBM bytes per attention launch from committed rocprofv3 counter runs, if
-    they were taken on the current kernel source."""
+    """HBM bytes per fused launch from committed rocprofv3 counter runs, if they
+    were taken on the current kernel source."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     t = json.load(open(TRAFFIC_FILE))
@@ -155,16 +157,15 @@ def main_bench(args):
 
     def step():
         db.replan_host()
-        db.kv_append()
-        db.attention()
+        db.step_fused()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    # The kernels stamp these events themselves (start and end of each launch),
-    # so timing adds no packet to the stream: the timed loop is the serving loop.
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    # The kernel stamps these events itself (start and end of the launch), so
+    # timing adds no packet to the stream: the timed loop is the serving loop.
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     for step_evs in evs:
         for e in step_evs:
             e.record()  # creates the HIP events
@@ -174,31 +175,34 @@ def main_bench(args):
     for i in range(args.steps):
         tp = time.perf_counter()
         db.replan_host()   # host plan into the other (device-mapped) plan slot
-        db.kv_append(events=(evs[i][0], evs[i][1]))
-        db.attention(events=(evs[i][2], evs[i][3]))
+        db.step_fused(events=(evs[i][0], evs[i][1]))
         host_s.append(time.perf_counter() - tp)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall / args.steps * 1e3
-    attn_s = statistics.mean(e[2].elapsed_time(e[3]) for e in evs) / 1e3
-    app_s = statistics.mean(e[0].elapsed_time(e[1]) for e in evs) / 1e3
+    fused_s = statistics.mean(e[0].elapsed_time(e[1]) for e in evs) / 1e3
+    # context, after the timed region: the same iteration as two launches
+    app_s = time_kernel_events(db.kv_append, 20)
+    attn_s = time_kernel_events(db.attention, 20)
     # host cost of planning alone (no copy, no launch)
     tp = time.perf_counter()
     for _ in range(200):
         db._bound[0][0]()
     plan_s = (time.perf_counter() - tp) / 200
-    log(f"[bench] step {ms_per_step * 1e3:.1f} us, attention {attn_s * 1e6:.1f} us, "
-        f"kv_append {app_s * 1e6:.1f} us, "
+    log(f"[bench] step {ms_per_step * 1e3:.1f} us, fused launch {fused_s * 1e6:.1f} us "
+        f"(as two launches: kv_append {app_s * 1e6:.1f} us, attention {attn_s * 1e6:.1f} us), "
         f"host per step {statistics.mean(host_s) * 1e6:.1f} us, plan {plan_s * 1e6:.1f} us")
 
-    alg_bytes = info.decode_bytes + info.chunk_bytes
-    achieved = alg_bytes / attn_s / 1e9
+    # algorithmic bytes: every K/V byte attention reads once, plus the append
+    # (new rows read once and written once)
+    alg_bytes = info.decode_bytes + info.chunk_bytes + info.append_bytes
+    achieved = alg_bytes / fused_s / 1e9
     tb = traffic_bytes()
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": None if tb is None else round(tb),
-                "kernel": "mixed_attention", "algorithmic_bytes": round(alg_bytes),
-                "kernel_us": round(attn_s * 1e6, 2)}
+                "kernel": "append_attention", "algorithmic_bytes": round(alg_bytes),
+                "kernel_us": round(fused_s * 1e6, 2)}
 
     extra = {}
     if args.extras:
@@ -226,7 +230,8 @@ def main_bench(args):
                    "chunk_tokens": int(b.q_len[b.q_len > 1].sum()),
                    "decode_reqs": int((b.q_len == 1).sum())},
         "tokens_per_s": round(b.num_tokens / (ms_per_step / 1e3), 1),
-        "attention_us": round(attn_s * 1e6, 2), "kv_append_us": round(app_s * 1e6, 2),
+        "fused_us": round(fused_s * 1e6, 2),
+        "two_launch": {"kv_append_us": round(app_s * 1e6, 2), "attention_us": round(attn_s * 1e6, 2)},
         "plan_us": round(plan_s * 1e6, 2),
         "host_us_per_step": round(statistics.mean(host_s) * 1e6, 2),
         "roofline": roofline,
@@ -278,6 +283,7 @@ def main_sweep(args):
             n = args.steps
             app = time_kernel_events(db.kv_append, n, flush) * 1e6
             attn = time_kernel_events(db.attention, n, flush) * 1e6
+            fused = time_kernel_events(db.step_fused, n, flush) * 1e6
             warm = time_kernel_events(db.attention, n) * 1e6
             tp = time.perf_counter()
             for _ in range(n):
@@ -292,11 +298,12 @@ def main_sweep(args):
                     segs[label] = segment_stats(sb, n, flush)
                     del sb
             info = db.info
-            step_us = plan + app + attn
+            step_us = plan + fused
             row = {"workload": name, "chunk": chunk, "prefix": prefix, "seed": args.seed,
                    "scene": info.scene, "tokens": b.num_tokens,
                    "attention_us": round(attn, 2), "attention_warm_us": round(warm, 2),
-                   "kv_append_us": round(app, 2), "plan_us": round(plan, 2),
+                   "kv_append_us": round(app, 2), "fused_us": round(fused, 2),
+                   "plan_us": round(plan, 2),
                    "step_us": round(step_us, 2),
                    "tokens_per_s": round(b.num_tokens / step_us * 1e6, 1),
                    "hbm_GBps": round((info.decode_bytes + info.chunk_bytes) / attn / 1e3, 1),
@@ -351,8 +358,8 @@ def _pmc_rows(path, counter):
 
 
 def main_traffic_json(args):
-    """HBM traffic of the attention launch from rocprofv3 --pmc runs: FETCH_SIZE
-    and WRITE_SIZE (KiB per dispatch) of mixed_attention_kernel, each scaled by
+    """HBM traffic of the fused launch from rocprofv3 --pmc runs: FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch) of append_attention_kernel, each scaled by
     what the same counter reads for a plain 1 GiB device copy."""
     fetch, write, cfetch, cwrite = args.traffic_json_inputs
     def kernel_avg(path, counter, name):
@@ -360,12 +367,12 @@ def main_traffic_json(args):
         if not v:
             raise SystemExit(f"no {counter} rows for {name} in {path}")
         return statistics.mean(v), len(v)
-    f_kib, n_f = kernel_avg(fetch, "FETCH_SIZE", "mixed_attention_kernel")
-    w_kib, n_w = kernel_avg(write, "WRITE_SIZE", "mixed_attention_kernel")
+    f_kib, n_f = kernel_avg(fetch, "FETCH_SIZE", "append_attention_kernel")
+    w_kib, n_w = kernel_avg(write, "WRITE_SIZE", "append_attention_kernel")
     copy_kib = float(1 << 20)  # the copy probe moves 1 GiB
     cf, _ = kernel_avg(cfetch, "FETCH_SIZE", "copyBuffer")
     cw, _ = kernel_avg(cwrite, "WRITE_SIZE", "copyBuffer")
-    out = {"kernel": "mixed_attention_kernel", "workload": DESCR[args.workload],
+    out = {"kernel": "append_attention_kernel", "workload": DESCR[args.workload],
            "kernel_source_sha256": sha256_file(KERNEL_SRC),
            "fetch_kib": round(f_kib, 1), "write_kib": round(w_kib, 1), "dispatches": [n_f, n_w],
            "copy_fetch_factor": round(cf / copy_kib, 4), "copy_write_factor": round(cw / copy_kib, 4),
@@ -388,9 +395,9 @@ def main_sweep_md(args):
     for name in workload_names_in(rows):
         lines.append(f"### {name}: {DESCR.get(name, name)}\n")
         lines.append("| chunk c | prefix u | scene | tokens | attention us (cold) | attention us (warm) | "
-                     "kv_append us | plan us | step us | tokens/s | decode-only us | chunk-only us | "
-                     "HBM GB/s (% of 8 TB/s) | MFMA TFLOP/s (% of 2.5 PF) |")
-        lines.append("|---|---|---|---|---|---|---|---|---|---|---|---|---|---|")
+                     "kv_append us | fused us | plan us | step us | tokens/s | decode-only us | "
+                     "chunk-only us | HBM GB/s (% of 8 TB/s) | MFMA TFLOP/s (% of 2.5 PF) |")
+        lines.append("|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|")
         for r in rows:
             if r["workload"] != name:
                 continue
@@ -403,7 +410,8 @@ def main_sweep_md(args):
             lines.append(
                 f"| {r['chunk']}{mark} | "
                 f"{r['prefix'] if r['prefix'] is not None else 'drawn'} | {r['scene']} | {r['tokens']} | "
-                f"{r['attention_us']} | {r['attention_warm_us']} | {r['kv_append_us']} | {r['plan_us']} | "
+                f"{r['attention_us']} | {r['attention_warm_us']} | {r['kv_append_us']} | "
+                f"{r.get('fused_us', '')} | {r['plan_us']} | "
                 f"{r['step_us']} | {r['tokens_per_s']:.3g} | {dec} | {chk} | "
                 f"{hbm} ({hbm / HBM_PEAK_GBS:.0%}) | {tf} ({tf / MFMA_BF16_PEAK_TFLOPS:.0%}) |")
         lines.append("")

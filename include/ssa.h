@@ -189,9 +189,10 @@ int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* pla
  * request i (kv head floor(h / G)), for every new token and q head, in bf16
  * (fp32 accumulation).  Reads the chunk's own keys from the pools, so
  * ssa_kv_append of the same plan must have run before it on the stream.
- * workspace: device memory of at least the plan's workspace size, zero-filled
- * by the caller once before its first use; each call leaves its counters at
- * zero again.  Calls that share a workspace must not overlap in time.
+ * workspace: device memory of at least the plan's workspace size (never less
+ * than 256 bytes), zero-filled by the caller once before its first use; each
+ * call leaves its counters at zero again.  Calls that share a workspace must
+ * not overlap in time.
  * Errors: NULL, the shape errors, PLAN_MISMATCH, WORKSPACE, HIP.
  */
 int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
@@ -219,6 +220,33 @@ int ssa_mixed_attention_timed(const ssa_shape* shape, const void* plan_host,
                               const uint16_t* v_cache, const int32_t* block_table, uint16_t* out,
                               void* workspace, size_t workspace_bytes, void* stream,
                               void* start_event, void* stop_event);
+
+/*
+ * ssa_kv_append followed by ssa_mixed_attention of the same plan, in ONE
+ * kernel launch (one iteration, Sec. 3.2: the new K/V rows of B = {(c_i, u_i)}
+ * enter their pages and every new token's output is computed).  Results are
+ * the same as the two calls in sequence (the same pool image, bit for bit; the
+ * same outputs, bit for bit).  Saves the second launch and the gap between two
+ * dependent kernels.
+ *   Arguments: as ssa_kv_append and ssa_mixed_attention; the workspace is
+ *   required (its first words are the launch's counters, zero at rest and
+ *   zero again after each call); events as in the _timed calls (NULL: none).
+ *   Inside the launch, the rows of chunk requests (c_i > 1) are appended by
+ *   workgroups of their own that come first in the grid and never wait; a
+ *   chunk work item waits for them (device-scope counter, once) before it
+ *   copies the first key block holding rows appended by this launch, and
+ *   copies the blocks from there on at device scope.  This relies on
+ *   workgroups being dispatched in index order, as the hardware does for one
+ *   launch.  A decode request's single new row is read by its decode item
+ *   from k_new / v_new and appended by that item itself (no other workgroup
+ *   reads that slot), so decode work never waits.
+ * Errors: those of ssa_kv_append and ssa_mixed_attention.
+ */
+int ssa_append_attention(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                         const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+                         uint16_t* k_cache, uint16_t* v_cache, const int32_t* block_table,
+                         uint16_t* out, void* workspace, size_t workspace_bytes, void* stream,
+                         void* start_event, void* stop_event);
 
 #ifdef __cplusplus
 }

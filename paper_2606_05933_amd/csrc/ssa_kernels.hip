@@ -70,9 +70,14 @@ typedef const __attribute__((address_space(4))) int32_t cint32;
 // counter tracking does not make later reads of *other* LDS stages wait for
 // it; every reader of the destination waits explicitly (lds_dma_wait before
 // the barrier that publishes the stage).
+// COHERENT reads at device scope (sc1): rows appended in the same launch.
+template <bool COHERENT = false>
 __device__ __forceinline__ void dma16(const void* g, const char* l) {
   const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)l;
-  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(a) : "memory");
+  if (COHERENT)
+    asm volatile("global_load_lds_dwordx4 %0, off sc1" ::"v"(g), "{m0}"(a) : "memory");
+  else
+    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(a) : "memory");
 }
 // s_waitcnt vmcnt(N): all but this wave's N most recent vector-memory
 // operations (LDS copies included) have completed.
@@ -126,10 +131,53 @@ struct AttnArgs {
   uint8_t* ws;
   float scale_log2;
   int hq, hkv, G, maxp;
+  // fused launch (append workgroups first in the grid): their number, and the
+  // attention items in the grid; 0 for a plain attention launch
+  int append_wgs, num_items;
+  // fused launch: this iteration's new key / value rows ([T, Hkv, D])
+  const uint16_t* k_new;
+  const uint16_t* v_new;
 };
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// 16-byte load / store at device scope (bypassing stale copies in another
+// die's L2): two 8-byte device-scope atomics.  Used where one launch both
+// writes and reads the same pool slots.
+__device__ __forceinline__ u32x4 ld16_dev(const void* p) {
+  uint64_t* q = reinterpret_cast<uint64_t*>(const_cast<void*>(p));
+  const uint64_t lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return u32x4{(uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32)};
+}
+__device__ __forceinline__ void st16_dev(void* p, u32x4 v) {
+  uint64_t* q = reinterpret_cast<uint64_t*>(p);
+  const uint32_t v0 = v[0], v1 = v[1], v2 = v[2], v3 = v[3];
+  __hip_atomic_store(q, (uint64_t)v0 | ((uint64_t)v1 << 32), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(q + 1, (uint64_t)v2 | ((uint64_t)v3 << 32), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Workspace words of a fused launch (ahead of the merge tickets): appending
+// workgroups that have finished, attention workgroups that have finished.
+// Both are zero at rest; the last attention workgroup resets them.
+constexpr int kCounterAppended = 0, kCounterAttended = 1;
+
+// Wait (a fused launch) until every appending workgroup has published its
+// rows.  They come first in the grid and never wait, and workgroups are
+// dispatched in index order, so the wait ends; the bound is a safety exit.
+__device__ __forceinline__ void wait_appended(const AttnArgs& a) {
+  if (a.append_wgs == 0) return;
+  int* counters = reinterpret_cast<int*>(a.ws);
+  for (int spin = 0; spin < (1 << 24); ++spin) {
+    if (__hip_atomic_load(&counters[kCounterAppended], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >=
+        a.append_wgs)
+      break;
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 __device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
@@ -323,7 +371,7 @@ __device__ void finish_split(const AttnArgs& a, const WorkItem& it, const ReqEnt
   // a word of the kernel's LDS buffer past both items' working areas
   int& s_last = *reinterpret_cast<int*>(lds + Cfg<D>::LDS - 16);
   const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + a.off_groups)[it.group];
-  int* tickets = reinterpret_cast<int*>(a.ws);
+  int* tickets = reinterpret_cast<int*>(a.ws) + kLaunchCounters;
   wait_vm_stores();
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -460,7 +508,7 @@ __device__ __forceinline__ void interleave_stream() {
 template <int S>
 using Stage = std::integral_constant<int, S>;
 
-template <int D>
+template <int D, bool FUSED>
 __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
                            char* lds) {
   using C = Cfg<D>;
@@ -551,18 +599,33 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     const int d = (m * 32) % D + (lane >> 1);
     vgo[r] = d * 16 + (((lane & 1) ^ vswz(d)) << 3);
   }
-  auto dma = [&](int kb, char* stage) {
+  // In a fused launch the blocks from the first one holding keys >= u on are
+  // copied at device scope (COH), after a wait, once, for the appending
+  // workgroups.
+  bool appended = !FUSED;
+  auto dma = [&](auto coh_t, int kb, char* stage) {
+    constexpr bool COH = decltype(coh_t)::value;
     const int lp0 = kb >> 4;
     const int pg0 = bt[lp0];
     const int pg1 = (lp0 + 1 < rq.n_pages) ? bt[lp0 + 1] : pg0;
+    auto issue = [&](auto coherent_t) {
+      constexpr bool COH = decltype(coherent_t)::value;
 #pragma unroll
-    for (int r = 0; r < C::LOADS; ++r) {
-      const int m = r * kWaves + w;
-      const bool second = (D == 128) ? (r != 0) : (w >= 2);
-      const size_t pb = (size_t)(second ? pg1 : pg0) * page_stride;
-      dma16(kbase + pb + kgo[r], stage + m * 1024);
-      dma16(vbase + pb + vgo[r], stage + C::K_STAGE + m * 1024);
+      for (int r = 0; r < C::LOADS; ++r) {
+        const int m = r * kWaves + w;
+        const bool second = (D == 128) ? (r != 0) : (w >= 2);
+        const size_t pb = (size_t)(second ? pg1 : pg0) * page_stride;
+        dma16<COH>(kbase + pb + kgo[r], stage + m * 1024);
+        dma16<COH>(vbase + pb + vgo[r], stage + C::K_STAGE + m * 1024);
+      }
+    };
+    if constexpr (COH) {
+      if (!appended) {
+        wait_appended(a);
+        appended = true;
+      }
     }
+    issue(coh_t);
   };
   // Zero the values of key slots >= nvalid of the block at kb (the block that
   // holds the request's end), in a stage whose loads have completed.
@@ -671,10 +734,10 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   // the S-3 most recent iterations outstanding.  The block after the current
   // one is zeroed past the request's end if needed (it has landed).
   constexpr int kInFlight = (kChunkStages - 3) * 2 * C::LOADS;
-  auto block = [&](auto sv_t, int b) {
+  auto block = [&](auto coh_t, auto sv_t, int b) {
     constexpr int SV = decltype(sv_t)::value;
     constexpr int S = kChunkStages;
-    dma(it.key0 + min(b + S - 1, nb - 1) * 32, lds + ((SV + S - 1) % S) * C::STAGE);
+    dma(coh_t, it.key0 + min(b + S - 1, nb - 1) * 32, lds + ((SV + S - 1) % S) * C::STAGE);
     const int kn = it.key0 + (b + 1) * 32;
     if (b + 1 < nb && kn + 32 > nvalid) zero_tail(kn, lds + ((SV + 1) % S) * C::STAGE);
     if (b < nbw) iteration(sv_t, b);
@@ -686,10 +749,23 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   // compiler's own waits for them would otherwise count the copies (which it
   // does not see) and stall on them inside the loop.
   lds_dma_wait();
+  // Block index of the first block holding keys >= u, and the first loop
+  // step (a multiple of the stage count, so that both loops below start at
+  // stage 0) from which the copies are device-scope: at or before the step
+  // that fetches that block.
+  constexpr int S = kChunkStages;
+  const int first_new = u > it.key0 ? (u - it.key0) / 32 : 0;
+  const int b_coh = FUSED ? min(nb, max(0, first_new - (S - 1)) / S * S) : nb;
   if (nb > 0) {
+    if (FUSED && first_new <= S - 2) {
 #pragma unroll
-    for (int k = 0; k < kChunkStages - 1; ++k)
-      dma(it.key0 + min(k, nb - 1) * 32, lds + k * C::STAGE);
+      for (int k = 0; k < S - 1; ++k)
+        dma(std::true_type{}, it.key0 + min(k, nb - 1) * 32, lds + k * C::STAGE);
+    } else {
+#pragma unroll
+      for (int k = 0; k < S - 1; ++k)
+        dma(std::false_type{}, it.key0 + min(k, nb - 1) * 32, lds + k * C::STAGE);
+    }
   }
   vm_wait<kInFlight>();  // blocks 0 and 1 have landed
   __syncthreads();
@@ -705,22 +781,28 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
       p0 = softmax_tile0(std::false_type{}, it.key0);
   }
   static_assert(kChunkStages >= 3 && kChunkStages <= 5, "pipeline depth");
-  for (int b = 0; b < nb;) {
-    block(Stage<0>{}, b);
-    if (++b >= nb) break;
-    block(Stage<1>{}, b);
-    if (++b >= nb) break;
-    block(Stage<2>{}, b);
-    if (++b >= nb) break;
-    if (kChunkStages >= 4) {
-      block(Stage<(kChunkStages >= 4 ? 3 : 0)>{}, b);
-      if (++b >= nb) break;
+  // steps [b, end): end is nb or a multiple of the stage count
+  int b = 0;
+  auto run = [&](auto coh_t, int end) {
+    while (b < end) {
+      block(coh_t, Stage<0>{}, b);
+      if (++b >= end) break;
+      block(coh_t, Stage<1>{}, b);
+      if (++b >= end) break;
+      block(coh_t, Stage<2>{}, b);
+      if (++b >= end) break;
+      if (kChunkStages >= 4) {
+        block(coh_t, Stage<(kChunkStages >= 4 ? 3 : 0)>{}, b);
+        if (++b >= end) break;
+      }
+      if (kChunkStages >= 5) {
+        block(coh_t, Stage<(kChunkStages >= 5 ? 4 : 0)>{}, b);
+        ++b;
+      }
     }
-    if (kChunkStages >= 5) {
-      block(Stage<(kChunkStages >= 5 ? 4 : 0)>{}, b);
-      ++b;
-    }
-  }
+  };
+  run(std::false_type{}, b_coh);
+  if constexpr (FUSED) run(std::true_type{}, nb);
   lds_dma_wait();  // no copy may land after this workgroup has left
 
   // epilogue
@@ -772,7 +854,18 @@ struct DecodeRegs {
   u32x4 v[Cfg<D>::MT];
 };
 
-template <int D>
+// v with its 16-bit element j (0..7; any other j: unchanged) replaced by e.
+__device__ __forceinline__ u32x4 set_elem(u32x4 v, int j, uint32_t e) {
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = (v[i] & 0xFFFF0000u) | e, hi = (v[i] & 0x0000FFFFu) | (e << 16);
+    r[i] = j == 2 * i ? lo : (j == 2 * i + 1 ? hi : v[i]);
+  }
+  return r;
+}
+
+template <int D, bool FUSED>
 __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
                             char* lds) {
   using C = Cfg<D>;
@@ -803,15 +896,35 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   // vector-memory wait before the K/V loads).  A page past the request's last
   // one is read from the first page instead (in bounds); keys from it are at or
   // beyond key1, so their logits are masked and their values zeroed in compute.
+  // In a fused launch the row of key u is taken from the new rows instead of
+  // the pool, and this item (the one of its kv head that holds key u) also
+  // appends it to the pool: no other workgroup reads that slot in the launch,
+  // so the decode never waits.
+  const bool has_new = FUSED && rq.q_len > 0 && it.key0 <= rq.ctx_len && rq.ctx_len < key1;
+  const size_t new_off = ((size_t)rq.q_start * a.hkv + it.kvh) * D;
+  // The new row in registers, loaded by every wave without waiting for it:
+  // vpk holds value dims lane (low half) and lane + 64 (high half, D = 128);
+  // kx, in lanes below D / 8, 16 bytes of the key row.
+  uint32_t vpk = 0;
+  u32x4 kx = {0, 0, 0, 0};
+  if constexpr (FUSED) {
+    if (has_new) {
+      vpk = a.v_new[new_off + lane];
+      if (D > 64) vpk |= (uint32_t)a.v_new[new_off + 64 + lane] << 16;
+      if (lane < C::CPR) kx = ld16(a.k_new + new_off + lane * 8);
+    }
+  }
   auto load = [&](DecodeRegs<D>& R, int kb) {
     const int lp0 = kb >> 4;
     const int pg0 = bt[lp0];
     const int pg1 = (lp0 + 1 < rq.n_pages) ? bt[lp0 + 1] : pg0;
+    const bool patch = has_new && kb + 32 > rq.ctx_len;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int key = 8 * (r16 >> 2) + 4 * h + (r16 & 3);
       const uint16_t* src = a.kc + (size_t)((key >> 4) ? pg1 : pg0) * page_stride + head_off +
                             (key & 15) * D + g * 8;
+      if (FUSED && patch && kb + key == rq.ctx_len) src = a.k_new + new_off + g * 8;
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) R.k[h][kk] = as_bf16x8(ld16(src + kk * 32));
     }
@@ -829,6 +942,19 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
     }
     const float sv[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
     bf16x8 pop;
+    if constexpr (FUSED) {
+      if (has_new && kb + 32 > rq.ctx_len) {
+        // the lane's 8 value slots are keys kb + 8 g .. kb + 8 g + 7; its dims
+        // r16 + 16 mt sit in lane r16 + 16 (mt % 4), half mt / 4, of vpk
+        const int j = rq.ctx_len - (kb + 8 * g);
+        uint32_t pk[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pk[i] = __builtin_amdgcn_ds_bpermute(4 * (r16 + 16 * i), (int)vpk);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          R.v[mt] = set_elem(R.v[mt], j, mt < 4 ? pk[mt] & 0xFFFFu : pk[mt & 3] >> 16);
+      }
+    }
     if (kb + 32 > key1) {
       const int lim = key1 - (kb + 8 * g);  // key e of the lane group valid iff e < lim
 #pragma unroll
@@ -848,7 +974,8 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   // and the memory-counter waits only cover the block being computed.
   const int nb = (key1 - it.key0 + 31) / 32;
   DecodeRegs<D> R0, R1;
-  int b = __builtin_amdgcn_readfirstlane(w);
+  const int wave = __builtin_amdgcn_readfirstlane(w);
+  int b = wave;
   if (b < nb) {
     load(R0, it.key0 + b * 32);
     for (;;) {
@@ -863,6 +990,19 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
     }
   }
   l_run = wave_sum_cols(l_run);
+  if constexpr (FUSED) {
+    if (has_new && wave == 0) {
+      // append the new row: key row and the value column of slot u (a fused
+      // launch passes pools it may write)
+      const size_t pg = (size_t)bt[rq.ctx_len >> 4] * page_stride + head_off;
+      const int slot = rq.ctx_len & 15;
+      uint16_t* kp = const_cast<uint16_t*>(a.kc) + pg;
+      uint16_t* vp = const_cast<uint16_t*>(a.vc) + pg;
+      if (lane < C::CPR) st16(kp + slot * D + lane * 8, kx);
+      vp[lane * 16 + slot] = (uint16_t)vpk;
+      if (D > 64) vp[(lane + 64) * 16 + slot] = (uint16_t)(vpk >> 16);
+    }
+  }
 
   // merge the 4 waves through LDS: per wave m[16], l[16], o[D][16]
   float* sm = reinterpret_cast<float*>(lds);
@@ -915,61 +1055,173 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   if (rec) finish_split<D>(a, it, rq, lds);
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads, 2) void mixed_attention_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) char lds[Cfg<D>::LDS];
-  // The plan may live in device-mapped host memory: read the header check and
-  // this workgroup's item, which are independent loads, and nothing else.
-  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
-  const WorkItem it = reinterpret_cast<const WorkItem*>(a.plan + a.off_items)[blockIdx.x];
-  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
+// One attention work item of the plan.
+template <int D, bool FUSED>
+__device__ void attention_wg(const AttnArgs& a, const WorkItem& it, char* lds) {
   ReqEntry rq;
   rq.q_start = it.q_start;
   rq.ctx_len = it.ctx_len;
   rq.q_len = it.nvalid - it.ctx_len;
   rq.n_pages = (it.nvalid + 15) >> 4;
   if (it.kind == kItemChunk)
-    chunk_item<D>(a, it, rq, lds);
+    chunk_item<D, FUSED>(a, it, rq, lds);
   else
-    decode_item<D>(a, it, rq, lds);
+    decode_item<D, FUSED>(a, it, rq, lds);
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void mixed_attention_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) char lds[Cfg<D>::LDS];
+  // The plan may live in device-mapped host memory: the header check and this
+  // workgroup's item are independent loads.
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
+  const WorkItem it = reinterpret_cast<const WorkItem*>(a.plan + a.off_items)[blockIdx.x];
+  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
+  attention_wg<D, false>(a, it, lds);
 }
 
 // ------------------------------------------------------------------ kv_append
 
+struct AppendArgs {
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  uint16_t* kc;
+  uint16_t* vc;
+  int32_t off_segments;
+};
+
+// The rows of one append segment (consecutive new tokens of one request that
+// land in one page) for kv heads h0 .. h0 + nh - 1: key rows are copied as
+// they are; value rows are transposed into the dim-major page ([D][16 slots]),
+// as whole 16-byte half rows where a segment covers them, else slot by slot.
+// Each thread issues the loads of kUnits units before their stores, so a
+// workgroup takes few memory round trips whatever the number of heads.
+// DEVICE_SCOPE writes through to the device coherence point (for readers in
+// the same launch on other dies).
+constexpr int kUnits = 4;
+template <int D, bool DEVICE_SCOPE>
+__device__ void append_rows(const AppendArgs& ap, const AppendSeg& sg, const int32_t* bt, int h0,
+                            int nh, int hkv, int maxp) {
+  constexpr int CPR = D / 8;
+  const int slot0 = sg.pos0 % 16;
+  const size_t pb = (size_t)bt[(size_t)sg.req * maxp + sg.pos0 / 16] * hkv * 16 * D;
+  auto put16 = [](uint16_t* p, u32x4 v) {
+    if (DEVICE_SCOPE)
+      st16_dev(p, v);
+    else
+      st16(p, v);
+  };
+  // key rows: units (head, row, 16-byte chunk)
+  const int rows_c = sg.n * CPR;
+  const int nk = nh * rows_c;
+  for (int i0 = threadIdx.x; i0 < nk; i0 += kUnits * kThreads) {
+    u32x4 v[kUnits];
+#pragma unroll
+    for (int u = 0; u < kUnits; ++u) {
+      const int idx = i0 + u * kThreads;
+      if (idx < nk) {
+        const int h = h0 + idx / rows_c, r = (idx % rows_c) / CPR, c = idx % CPR;
+        v[u] = ld16(ap.k_new + ((size_t)(sg.row0 + r) * hkv + h) * D + c * 8);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnits; ++u) {
+      const int idx = i0 + u * kThreads;
+      if (idx < nk) {
+        const int h = h0 + idx / rows_c, r = (idx % rows_c) / CPR, c = idx % CPR;
+        put16(ap.kc + pb + (size_t)h * 16 * D + (size_t)(slot0 + r) * D + c * 8, v[u]);
+      }
+    }
+  }
+  // value rows: units (head, dim, half page row of 8 slots); a unit takes the
+  // slots [lo, hi) of its half that the segment covers
+  const int nv = nh * 2 * D;
+  for (int i0 = threadIdx.x; i0 < nv; i0 += kUnits * kThreads) {
+    uint32_t e[kUnits][8];
+#pragma unroll
+    for (int u = 0; u < kUnits; ++u) {
+      const int idx = i0 + u * kThreads;
+      const int h = h0 + idx / (2 * D), d = (idx >> 1) % D, half = idx & 1;
+      const int lo = max(half * 8, slot0), hi = min(half * 8 + 8, slot0 + sg.n);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int sl = half * 8 + k;
+        e[u][k] = (idx < nv && sl >= lo && sl < hi)
+                      ? ap.v_new[((size_t)(sg.row0 + sl - slot0) * hkv + h) * D + d]
+                      : 0u;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnits; ++u) {
+      const int idx = i0 + u * kThreads;
+      if (idx >= nv) continue;
+      const int h = h0 + idx / (2 * D), d = (idx >> 1) % D, half = idx & 1;
+      const int lo = max(half * 8, slot0), hi = min(half * 8 + 8, slot0 + sg.n);
+      if (lo >= hi) continue;
+      uint16_t* dst = ap.vc + pb + (size_t)h * 16 * D + (size_t)d * 16;
+      if (lo == half * 8 && hi == half * 8 + 8) {
+        put16(dst + lo, u32x4{e[u][0] | (e[u][1] << 16), e[u][2] | (e[u][3] << 16),
+                              e[u][4] | (e[u][5] << 16), e[u][6] | (e[u][7] << 16)});
+      } else {
+        for (int sl = lo; sl < hi; ++sl) {
+          const uint16_t x = (uint16_t)e[u][sl - half * 8];
+          if (DEVICE_SCOPE)
+            __hip_atomic_store(dst + sl, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          else
+            dst[sl] = x;
+        }
+      }
+    }
+  }
+}
+
+// kv_append: workgroup (segment, kv head).
 template <int D>
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint8_t* plan, uint64_t hash,
-                                                             int32_t off_segments,
-                                                             const uint16_t* k_new,
-                                                             const uint16_t* v_new, uint16_t* kc,
-                                                             uint16_t* vc, const int32_t* bt,
+                                                             AppendArgs ap, const int32_t* bt,
                                                              int hkv, int maxp) {
   const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(plan);
-  const AppendSeg sg = reinterpret_cast<const AppendSeg*>(plan + off_segments)[blockIdx.x];
+  const AppendSeg sg = reinterpret_cast<const AppendSeg*>(plan + ap.off_segments)[blockIdx.x];
   if (hdr->magic != kPlanMagic || hdr->hash != hash) return;
-  const int h = blockIdx.y;
-  const int slot0 = sg.pos0 % 16;
-  const size_t pb = (size_t)bt[(size_t)sg.req * maxp + sg.pos0 / 16] * hkv * 16 * D + (size_t)h * 16 * D;
-  constexpr int CPR = D / 8;
-  for (int idx = threadIdx.x; idx < sg.n * CPR; idx += kThreads) {
-    const int r = idx / CPR, c = idx % CPR;
-    st16(kc + pb + (size_t)(slot0 + r) * D + c * 8,
-         ld16(k_new + ((size_t)(sg.row0 + r) * hkv + h) * D + c * 8));
+  append_rows<D, false>(ap, sg, bt, blockIdx.y, 1, hkv, maxp);
+}
+
+// kv_append and mixed attention in one launch.  Workgroups 0 .. append_wgs-1
+// append one segment of a chunk request each (every kv head) with
+// device-scope stores, then count themselves done.  The others run the
+// attention work items: a chunk block that holds keys appended in this launch
+// is read, at device scope, only after every appending workgroup has counted
+// (they never wait, and workgroups are dispatched in index order, so they all
+// run); a decode item appends its request's one new row itself.  The last
+// attention workgroup resets both counters for the next launch.
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void append_attention_kernel(AttnArgs a, AppendArgs ap) {
+  __shared__ __attribute__((aligned(16))) char lds[Cfg<D>::LDS];
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
+  int* counters = reinterpret_cast<int*>(a.ws);
+  if ((int)blockIdx.x < a.append_wgs) {
+    const AppendSeg sg = reinterpret_cast<const AppendSeg*>(a.plan + ap.off_segments)[blockIdx.x];
+    if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
+    append_rows<D, true>(ap, sg, a.bt, 0, a.hkv, a.hkv, a.maxp);
+    vm_wait<0>();  // this thread's device-scope stores have completed
+    __syncthreads();
+    if (threadIdx.x == 0)
+      __hip_atomic_fetch_add(&counters[kCounterAppended], 1, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    return;
   }
-  for (int idx = threadIdx.x; idx < 2 * D; idx += kThreads) {
-    const int d = idx >> 1, half = idx & 1;
-    const int lo = max(half * 8, slot0), hi = min(half * 8 + 8, slot0 + sg.n);
-    if (lo >= hi) continue;
-    uint16_t* dst = vc + pb + (size_t)d * 16;
-    // value of slot s: token row row0 + (s - slot0), kv head h, dim d
-    auto src = [&](int s) { return v_new[((size_t)(sg.row0 + s - slot0) * hkv + h) * D + d]; };
-    if (lo == half * 8 && hi == half * 8 + 8) {
-      uint32_t wv[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        wv[i] = (uint32_t)src(lo + 2 * i) | ((uint32_t)src(lo + 2 * i + 1) << 16);
-      st16(dst + lo, u32x4{wv[0], wv[1], wv[2], wv[3]});
-    } else {
-      for (int s = lo; s < hi; ++s) dst[s] = src(s);
+  const WorkItem it =
+      reinterpret_cast<const WorkItem*>(a.plan + a.off_items)[(int)blockIdx.x - a.append_wgs];
+  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
+  attention_wg<D, true>(a, it, lds);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int prev = __hip_atomic_fetch_add(&counters[kCounterAttended], 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == a.num_items - 1) {
+      wait_appended(a);  // no appending workgroup still to count
+      __hip_atomic_store(&counters[kCounterAppended], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&counters[kCounterAttended], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -993,9 +1245,9 @@ int ssa_kv_append_timed(const ssa_shape* shape, const void* plan_host, const voi
   (void)clear_and_check();
   const uint8_t* p = static_cast<const uint8_t*>(plan_dev);
   uint64_t hash = h->hash;
-  int32_t off_segments = h->off_segments, hkv = h->hkv, maxp = h->max_pages_per_req;
-  void* args[] = {&p, &hash, &off_segments, &k_new, &v_new, &k_cache, &v_cache, &block_table,
-                  &hkv, &maxp};
+  AppendArgs ap{k_new, v_new, k_cache, v_cache, h->off_segments};
+  int32_t hkv = h->hkv, maxp = h->max_pages_per_req;
+  void* args[] = {&p, &hash, &ap, &block_table, &hkv, &maxp};
   const void* fn = h->head_dim == 128 ? reinterpret_cast<const void*>(&kv_append_kernel<128>)
                                       : reinterpret_cast<const void*>(&kv_append_kernel<64>);
   hipError_t e = hipExtLaunchKernel(fn, dim3(h->num_segments, h->hkv), dim3(kThreads), args, 0,
@@ -1012,36 +1264,58 @@ int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* pla
                              block_table, stream, nullptr, nullptr);
 }
 
+}  // extern "C"
+
+namespace {
+// Validated attention arguments of a plan (SSA_OK, or the error to return).
+int attention_args(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                   const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                   const int32_t* block_table, uint16_t* out, void* workspace,
+                   size_t workspace_bytes, const PlanHeader** hp, AttnArgs* a) {
+  const PlanHeader* h = nullptr;
+  int rc = check_plan(shape, plan_host, &h);
+  if (rc) return rc;
+  if (!plan_dev) return SSA_ERR_NULL;
+  *hp = h;
+  if (h->num_items == 0) return SSA_OK;
+  if (!q || !k_cache || !v_cache || !block_table || !out) return SSA_ERR_NULL;
+  if (!workspace || workspace_bytes < (size_t)h->ws_bytes) return SSA_ERR_WORKSPACE;
+  a->plan = static_cast<const uint8_t*>(plan_dev);
+  a->hash = h->hash;
+  a->off_items = h->off_items;
+  a->off_groups = h->off_groups;
+  a->ws_partials_off = h->ws_partials_off;
+  a->q = q;
+  a->kc = k_cache;
+  a->vc = v_cache;
+  a->bt = block_table;
+  a->out = out;
+  a->ws = static_cast<uint8_t*>(workspace);
+  a->scale_log2 = h->softmax_scale * kLog2e;
+  a->hq = h->hq;
+  a->hkv = h->hkv;
+  a->G = h->hq / h->hkv;
+  a->maxp = h->max_pages_per_req;
+  a->append_wgs = 0;
+  a->num_items = h->num_items;
+  a->k_new = nullptr;
+  a->v_new = nullptr;
+  return SSA_OK;
+}
+}  // namespace
+
+extern "C" {
+
 int ssa_mixed_attention_timed(const ssa_shape* shape, const void* plan_host,
                               const void* plan_dev, const uint16_t* q, const uint16_t* k_cache,
                               const uint16_t* v_cache, const int32_t* block_table, uint16_t* out,
                               void* workspace, size_t workspace_bytes, void* stream,
                               void* start_event, void* stop_event) {
   const PlanHeader* h = nullptr;
-  int rc = check_plan(shape, plan_host, &h);
-  if (rc) return rc;
-  if (!plan_dev) return SSA_ERR_NULL;
-  if (h->num_items == 0) return SSA_OK;
-  if (!q || !k_cache || !v_cache || !block_table || !out) return SSA_ERR_NULL;
-  if (h->ws_bytes > 0 && (!workspace || workspace_bytes < (size_t)h->ws_bytes))
-    return SSA_ERR_WORKSPACE;
   AttnArgs a;
-  a.plan = static_cast<const uint8_t*>(plan_dev);
-  a.hash = h->hash;
-  a.off_items = h->off_items;
-  a.off_groups = h->off_groups;
-  a.ws_partials_off = h->ws_partials_off;
-  a.q = q;
-  a.kc = k_cache;
-  a.vc = v_cache;
-  a.bt = block_table;
-  a.out = out;
-  a.ws = static_cast<uint8_t*>(workspace);
-  a.scale_log2 = h->softmax_scale * kLog2e;
-  a.hq = h->hq;
-  a.hkv = h->hkv;
-  a.G = h->hq / h->hkv;
-  a.maxp = h->max_pages_per_req;
+  int rc = attention_args(shape, plan_host, plan_dev, q, k_cache, v_cache, block_table, out,
+                          workspace, workspace_bytes, &h, &a);
+  if (rc || h->num_items == 0) return rc;
   (void)clear_and_check();
   void* args[] = {&a};
   const void* fn = h->head_dim == 128
@@ -1062,5 +1336,31 @@ int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const voi
                                    out, workspace, workspace_bytes, stream, nullptr, nullptr);
 }
 
+int ssa_append_attention(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                         const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+                         uint16_t* k_cache, uint16_t* v_cache, const int32_t* block_table,
+                         uint16_t* out, void* workspace, size_t workspace_bytes, void* stream,
+                         void* start_event, void* stop_event) {
+  const PlanHeader* h = nullptr;
+  AttnArgs a;
+  int rc = attention_args(shape, plan_host, plan_dev, q, k_cache, v_cache, block_table, out,
+                          workspace, workspace_bytes, &h, &a);
+  if (rc || h->num_items == 0) return rc;
+  if (h->num_segments > 0 && (!k_new || !v_new)) return SSA_ERR_NULL;
+  a.append_wgs = h->num_chunk_segments;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  AppendArgs ap{k_new, v_new, k_cache, v_cache, h->off_segments};
+  (void)clear_and_check();
+  void* args[] = {&a, &ap};
+  const void* fn = h->head_dim == 128
+                       ? reinterpret_cast<const void*>(&append_attention_kernel<128>)
+                       : reinterpret_cast<const void*>(&append_attention_kernel<64>);
+  hipError_t e = hipExtLaunchKernel(fn, dim3(a.append_wgs + h->num_items), dim3(kThreads), args,
+                                    0, static_cast<hipStream_t>(stream),
+                                    static_cast<hipEvent_t>(start_event),
+                                    static_cast<hipEvent_t>(stop_event), 0);
+  return e == hipSuccess && hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+}
 
 }  // extern "C"

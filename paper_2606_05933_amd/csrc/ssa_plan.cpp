@@ -97,6 +97,7 @@ struct Plan {
   std::vector<WorkItem> items;
   std::vector<MergeGroup> groups;
   std::vector<AppendSeg> segs;
+  int32_t num_chunk_segs = 0;
   PlanHeader hdr;
   ssa_plan_info info;
 };
@@ -309,17 +310,23 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   else if (in.num_decode_reqs == 0) in.scene = SSA_SCENE_PURE_PREFILL;
   else in.scene = SSA_SCENE_MIXED;
 
-  // append segments: runs of new tokens inside one page
+  // append segments: runs of new tokens inside one page; those of chunk
+  // requests first (a fused launch appends only them in workgroups of their
+  // own: a decode item writes its request's single new row itself)
   p->segs.clear();
   p->segs.reserve((size_t)n + (size_t)(T / P) + 1);
-  for (int i = 0; i < n; ++i) {
-    int64_t pos = ctx_len[i], end = (int64_t)ctx_len[i] + q_len[i], row = p->reqs[i].q_start;
-    while (pos < end) {
-      int64_t m = std::min<int64_t>(P - pos % P, end - pos);
-      p->segs.push_back(AppendSeg{i, (int32_t)row, (int32_t)pos, (int32_t)m});
-      pos += m;
-      row += m;
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int i = 0; i < n; ++i) {
+      if ((q_len[i] > 1) != (pass == 0)) continue;
+      int64_t pos = ctx_len[i], end = (int64_t)ctx_len[i] + q_len[i], row = p->reqs[i].q_start;
+      while (pos < end) {
+        int64_t m = std::min<int64_t>(P - pos % P, end - pos);
+        p->segs.push_back(AppendSeg{i, (int32_t)row, (int32_t)pos, (int32_t)m});
+        pos += m;
+        row += m;
+      }
     }
+    if (pass == 0) p->num_chunk_segs = (int32_t)p->segs.size();
   }
 
   // balancing estimates (seconds): chunk work per CU at the nominal MFMA rate,
@@ -445,6 +452,7 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   h.num_decode_items = in.num_decode_items;
   h.num_groups = in.num_merge_groups;
   h.num_segments = in.num_append_segments;
+  h.num_chunk_segments = p->num_chunk_segs;
   h.hq = Hq;
   h.hkv = Hkv;
   h.head_dim = D;
@@ -463,9 +471,9 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   h.off_segments = (int32_t)off;
   off += (int64_t)sizeof(AppendSeg) * p->segs.size();
   h.plan_bytes = off;
-  const int64_t tickets = ceil_div((int64_t)p->groups.size() * 4, 256) * 256;
+  const int64_t tickets = ceil_div(((int64_t)kLaunchCounters + p->groups.size()) * 4, 256) * 256;
   h.ws_partials_off = tickets;
-  h.ws_bytes = p->groups.empty() ? 0 : tickets + ws_floats * 4;
+  h.ws_bytes = tickets + ws_floats * 4;
 
   uint64_t hv = 1469598103934665603ull;
   int32_t fields[8] = {Hq, Hkv, D, P, s->num_pages, s->max_pages_per_req, n, 0};

@@ -5,8 +5,9 @@
 //   [PlanHeader 128 B][ReqEntry x num_reqs][WorkItem x num_items]
 //   [MergeGroup x num_groups][AppendSeg x num_segments]
 //
-// The workspace of ssa_mixed_attention holds one int32 ticket per merge group
-// (zero at rest) followed, at ws_partials_off, by fp32 partial results:
+// The workspace holds kLaunchCounters int32 words for a fused launch and one
+// int32 ticket per merge group (all zero at rest), padded to 256 bytes, then,
+// at ws_partials_off, fp32 partial results:
 // for merge group g and split s, a record of ncols * (D + 2) floats at float
 // offset ws_off + s * ncols * (D + 2): m[ncols], l[ncols], o[ncols][D].
 #pragma once
@@ -15,11 +16,12 @@
 namespace ssa {
 
 constexpr uint32_t kPlanMagic = 0x31415353u;  // "SSA1"
-constexpr uint32_t kPlanVersion = 1;
+constexpr uint32_t kPlanVersion = 2;
 constexpr int kBlockKeys = 32;  // keys per attention block: two 16-slot pages
 constexpr int kWaves = 4;       // waves per workgroup
 constexpr int kThreads = 256;   // threads per workgroup
 constexpr int kChunkWaveCols = 32;  // columns a wave owns in a chunk tile
+constexpr int kLaunchCounters = 2;  // workspace words ahead of the merge tickets
 
 enum ItemKind : int32_t { kItemChunk = 0, kItemDecode = 1 };
 
@@ -33,10 +35,11 @@ struct PlanHeader {
   int32_t chunk_tile_cols;
   int32_t off_reqs, off_items, off_groups, off_segments;  // byte offsets in the blob
   int64_t ws_partials_off;  // byte offset of the partial records in the workspace
-  int64_t ws_bytes;         // workspace bytes the plan needs (0: none)
+  int64_t ws_bytes;         // workspace bytes the plan needs (at least 256)
   int64_t plan_bytes;       // total blob size
   float softmax_scale;
-  int32_t reserved[3];
+  int32_t num_chunk_segments;  // segments of chunk requests (c > 1): the first ones
+  int32_t reserved[2];
 };
 static_assert(sizeof(PlanHeader) == 128, "plan header size");
 

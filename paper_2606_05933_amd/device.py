@@ -98,7 +98,10 @@ class DeviceBatch:
                 ssa.bind_kv_append(self.shape, hb, db, self.k_new, self.v_new, self.k_cache,
                                    self.v_cache, self.block_table),
                 ssa.bind_mixed_attention(self.shape, hb, db, self.q, self.k_cache, self.v_cache,
-                                         self.block_table, self.out, self.workspace)))
+                                         self.block_table, self.out, self.workspace),
+                ssa.bind_append_attention(self.shape, hb, db, self.q, self.k_new, self.v_new,
+                                          self.k_cache, self.v_cache, self.block_table, self.out,
+                                          self.workspace)))
         torch.cuda.synchronize(self.device)
         return self.info
 
@@ -143,6 +146,15 @@ class DeviceBatch:
     def step(self, stream=None):
         self.kv_append(stream)
         self.attention(stream)
+
+    def step_fused(self, events=(None, None)):
+        """kv_append and attention in one launch (ssa_append_attention) on the
+        current stream; its stop event marks the slot's kernels done."""
+        start, stop = events
+        if stop is None:
+            stop = self._own_done[self._slot]
+        self._bound[self._slot][3](start, stop)
+        self._done[self._slot] = stop
 
     def out_f32(self) -> np.ndarray:
         return self.out.float().cpu().numpy()

@@ -107,13 +107,17 @@ def _load():
     lib.ssa_mixed_attention_timed.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp,
                                               vp, vp]
     lib.ssa_mixed_attention_timed.restype = ctypes.c_int
+    lib.ssa_append_attention.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                         vp, vp, vp]
+    lib.ssa_append_attention.restype = ctypes.c_int
     return lib
 
 
 LIB = _load()
 
 EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
-            "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed")
+            "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed",
+            "ssa_append_attention")
 
 
 def ssa_status_string(code: int) -> str:
@@ -313,6 +317,31 @@ def bind_mixed_attention(shape: SsaShape, plan_host, plan_dev, q, k_cache, v_cac
             vp(_ptr(k_cache)), vp(_ptr(v_cache)), vp(_ptr(block_table)), vp(_ptr(out)),
             vp(_ptr(workspace)), ctypes.c_size_t(ws_bytes), vp(_stream(stream)))
     return BoundCall(LIB.ssa_mixed_attention_timed, "ssa_mixed_attention", args, timed=True)
+
+
+def bind_append_attention(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
+                          block_table, out, workspace, stream=None) -> BoundCall:
+    """ssa_append_attention (kv_append and mixed attention in one launch);
+    calling the result takes optional (start, stop) events."""
+    h = _plan_header(plan_host)
+    T, n = h["num_tokens"], h["num_reqs"]
+    qrow = shape.num_q_heads * shape.head_dim
+    row = shape.num_kv_heads * shape.head_dim
+    pool = shape.num_pages * shape.num_kv_heads * shape.page_size * shape.head_dim
+    _check_dev("q", q, T * qrow, 2)
+    _check_dev("out", out, T * qrow, 2)
+    _check_dev("k_new", k_new, T * row, 2)
+    _check_dev("v_new", v_new, T * row, 2)
+    _check_dev("k_cache", k_cache, pool, 2)
+    _check_dev("v_cache", v_cache, pool, 2)
+    _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    vp = ctypes.c_void_p
+    args = (ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)), vp(_ptr(q)),
+            vp(_ptr(k_new)), vp(_ptr(v_new)), vp(_ptr(k_cache)), vp(_ptr(v_cache)),
+            vp(_ptr(block_table)), vp(_ptr(out)), vp(_ptr(workspace)), ctypes.c_size_t(ws_bytes),
+            vp(_stream(stream)))
+    return BoundCall(LIB.ssa_append_attention, "ssa_append_attention", args, timed=True)
 
 
 def bind_plan(shape: SsaShape, q_len, ctx_len, tuning, out, info: SsaPlanInfo) -> BoundCall:

@@ -19,7 +19,8 @@ HDR = np.dtype([("magic", "<u4"), ("version", "<u4"), ("hash", "<u8"), ("num_req
                 ("max_pages_per_req", "<i4"), ("num_pages", "<i4"), ("chunk_tile_cols", "<i4"),
                 ("off_reqs", "<i4"), ("off_items", "<i4"), ("off_groups", "<i4"),
                 ("off_segments", "<i4"), ("ws_partials_off", "<i8"), ("ws_bytes", "<i8"),
-                ("plan_bytes", "<i8"), ("scale", "<f4"), ("reserved", "<i4", 3)])
+                ("plan_bytes", "<i8"), ("scale", "<f4"), ("num_chunk_segments", "<i4"),
+                ("reserved", "<i4", 2)])
 REQ = np.dtype([("q_start", "<i4"), ("q_len", "<i4"), ("ctx_len", "<i4"), ("n_pages", "<i4")])
 ITEM = np.dtype([("kind", "<i4"), ("req", "<i4"), ("kvh", "<i4"), ("col0", "<i4"),
                  ("ncols", "<i4"), ("key0", "<i4"), ("key1", "<i4"), ("group", "<i4"),
@@ -112,6 +113,10 @@ def check_plan_covers_batch(hq, hkv, d, q_len, ctx_len, tuning=None):
             seen.append((sg["row0"] + k, sg["pos0"] + k - int(ctx_len[i])))
     expect = [(int(reqs["q_start"][i]) + j, j) for i in range(n) for j in range(int(q_len[i]))]
     assert sorted(seen) == sorted(expect)
+    # those of chunk requests (c > 1) first, then one per decode request
+    nc, ql = int(h["num_chunk_segments"]), np.asarray(q_len)
+    assert (ql[segs["req"][:nc]] > 1).all() and (ql[segs["req"][nc:]] == 1).all()
+    assert len(segs) - nc == int((ql == 1).sum())
     return info, items
 
 
@@ -287,6 +292,18 @@ def test_launchers_validate_before_any_hip_call():
                                        fake, ws - 1, None, fake, fake) == -8
     assert L.ssa_mixed_attention_timed(ctypes.byref(other), p, fake, fake, fake, fake, fake, fake,
                                        fake, ws, None, fake, fake) == -9
+    # kv_append + attention in one launch: the same checks
+    args = [fake] * 8  # q, k_new, v_new, k_cache, v_cache, block_table, out, workspace
+    assert L.ssa_append_attention(ctypes.byref(shape), p, None, *args, ws, None, None, None) == -1
+    assert L.ssa_append_attention(ctypes.byref(other), p, fake, *args, ws, None, None, None) == -9
+    assert L.ssa_append_attention(ctypes.byref(shape), p, fake, *args, ws - 1, None, None,
+                                  None) == -8
+    nulls = list(args)
+    nulls[1] = None  # k_new
+    assert L.ssa_append_attention(ctypes.byref(shape), p, fake, *nulls, ws, None, None, None) == -1
+    nulls = list(args)
+    nulls[7] = None  # workspace
+    assert L.ssa_append_attention(ctypes.byref(shape), p, fake, *nulls, ws, None, None, None) == -8
 
 
 def test_empty_batch_launches_nothing():

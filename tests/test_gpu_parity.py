@@ -219,8 +219,8 @@ def test_repeat_launches_are_bitwise_identical_and_reset_tickets(torch_dev):
             assert torch.equal(db.out.view(torch.int16), first.view(torch.int16)), k
     torch.cuda.synchronize()
     ng = db.info.num_merge_groups
-    tickets = db.workspace[: 4 * ng].view(torch.int32)
-    assert int(tickets.abs().sum()) == 0
+    counters_and_tickets = db.workspace[: 4 * (2 + ng)].view(torch.int32)
+    assert int(counters_and_tickets.abs().sum()) == 0
 
 
 def test_timed_launches_stamp_the_kernels_and_match_untimed(torch_dev):
@@ -244,3 +244,71 @@ def test_timed_launches_stamp_the_kernels_and_match_untimed(torch_dev):
     say(f"    kv_append {t_app * 1e3:.1f} us, attention {t_att * 1e3:.1f} us")
     assert 0 < t_app < 1000 and 0 < t_att < 1000
     assert evs[1].elapsed_time(evs[2]) >= 0
+
+
+def fused_parity(b, tuning=None, plan_on_device=False):
+    """ssa_append_attention on a fresh batch (new slots NaN-poisoned): the pool
+    image bit for bit, outputs against the oracle, and bitwise the same as the
+    two launches."""
+    import torch
+    from oracle import oracle
+    from paper_2606_05933_amd.device import DeviceBatch, bits_of
+    say(f"[gpu fused] {b.name} reqs={b.num_reqs} T={b.num_tokens} hq/hkv/d={b.shape.hq}/"
+        f"{b.shape.hkv}/{b.shape.d} seed={b.seed}")
+    db = DeviceBatch(b, tuning, plan_on_device=plan_on_device)
+    db.step_fused()
+    torch.cuda.synchronize()
+    kc, vc = oracle.batch_kv_append(b)
+    assert np.array_equal(bits_of(db.k_cache).reshape(kc.shape), kc), "K pool image differs"
+    assert np.array_equal(bits_of(db.v_cache).reshape(vc.shape), vc), "V pool image differs"
+    ref, _ = oracle.batch_attention(b, kc, vc)
+    assert_close(db.out_f32(), ref, b.name + " fused")
+    fused = db.out.clone()
+    two = DeviceBatch(b, tuning, plan_on_device=plan_on_device)
+    two.step()
+    torch.cuda.synchronize()
+    assert torch.equal(fused.view(torch.int16), two.out.view(torch.int16)), "fused != two launches"
+    return db
+
+
+@pytest.mark.parametrize("case", range(len(SMALL)))
+def test_fused_small_batches(torch_dev, case):
+    hq, hkv, d, cu = SMALL[case]
+    fused_parity(small(hq, hkv, d, cu, seed=case, name=f"small{case}"))
+
+
+@pytest.mark.parametrize("name", ["tiny", "l8b", "multi"])
+def test_fused_workloads(torch_dev, name):
+    from paper_2606_05933_amd import workload
+    fused_parity(workload.make_workload(name, seed=1))
+
+
+def test_fused_with_splits_and_device_plan(torch_dev):
+    from paper_2606_05933_amd import ssa
+    b = small(32, 8, 128, [(300, 1500), (1, 3000), (1, 5000), (64, 0)], seed=5, name="fused-split")
+    fused_parity(b, ssa.make_tuning(chunk_split_keys=512, decode_split_keys=1024),
+                 plan_on_device=True)
+
+
+def test_fused_repeated_from_poisoned_pools(torch_dev):
+    """Every launch starts from the pools with the new slots NaN-poisoned, so a
+    read of a new row before its append shows; the counters end at zero."""
+    import torch
+    from paper_2606_05933_amd import ssa, workload
+    from paper_2606_05933_amd.device import DeviceBatch
+    b = workload.make_workload("multi", seed=6)
+    db = DeviceBatch(b, ssa.make_tuning(decode_split_keys=1024))
+    k0, v0 = db.k_cache.clone(), db.v_cache.clone()
+    db.step()
+    torch.cuda.synchronize()
+    ref = db.out.clone()
+    for k in range(20):
+        db.k_cache.copy_(k0)
+        db.v_cache.copy_(v0)
+        db.out.zero_()
+        db.replan_host()
+        db.step_fused()
+        torch.cuda.synchronize()
+        assert torch.equal(db.out.view(torch.int16), ref.view(torch.int16)), k
+    ng = db.info.num_merge_groups
+    assert int(db.workspace[: 4 * (2 + ng)].view(torch.int32).abs().sum()) == 0
