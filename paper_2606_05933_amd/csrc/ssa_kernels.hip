@@ -167,15 +167,22 @@ constexpr int kCounterAppended = 0, kCounterAttended = 1;
 
 // Wait (a fused launch) until every appending workgroup has published its
 // rows.  They come first in the grid and never wait, and workgroups are
-// dispatched in index order, so the wait ends; the bound is a safety exit.
+// dispatched in index order, so the wait ends; the bound (about half a second)
+// is a safety exit.  One lane per wave polls: hundreds of waiting workgroups
+// polling the one counter word with every lane would slow the very stores
+// they wait for.
 __device__ __forceinline__ void wait_appended(const AttnArgs& a) {
   if (a.append_wgs == 0) return;
   int* counters = reinterpret_cast<int*>(a.ws);
-  for (int spin = 0; spin < (1 << 24); ++spin) {
-    if (__hip_atomic_load(&counters[kCounterAppended], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >=
-        a.append_wgs)
-      break;
-    __builtin_amdgcn_s_sleep(2);
+  const int me = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  const int poller = __builtin_amdgcn_readfirstlane(me);
+  for (int spin = 0; spin < (1 << 21); ++spin) {
+    int done = 0;
+    if (me == poller)
+      done = __hip_atomic_load(&counters[kCounterAppended], __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+    if (__builtin_amdgcn_readfirstlane(done) >= a.append_wgs) break;
+    __builtin_amdgcn_s_sleep(8);
   }
 }
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -600,11 +607,9 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     vgo[r] = d * 16 + (((lane & 1) ^ vswz(d)) << 3);
   }
   // In a fused launch the blocks from the first one holding keys >= u on are
-  // copied at device scope (COH), after a wait, once, for the appending
-  // workgroups.
-  bool appended = !FUSED;
+  // copied at device scope (COH), after one wait for the appending workgroups
+  // (outside the loops).
   auto dma = [&](auto coh_t, int kb, char* stage) {
-    constexpr bool COH = decltype(coh_t)::value;
     const int lp0 = kb >> 4;
     const int pg0 = bt[lp0];
     const int pg1 = (lp0 + 1 < rq.n_pages) ? bt[lp0 + 1] : pg0;
@@ -619,12 +624,6 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
         dma16<COH>(vbase + pb + vgo[r], stage + C::K_STAGE + m * 1024);
       }
     };
-    if constexpr (COH) {
-      if (!appended) {
-        wait_appended(a);
-        appended = true;
-      }
-    }
     issue(coh_t);
   };
   // Zero the values of key slots >= nvalid of the block at kb (the block that
@@ -756,8 +755,10 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   constexpr int S = kChunkStages;
   const int first_new = u > it.key0 ? (u - it.key0) / 32 : 0;
   const int b_coh = FUSED ? min(nb, max(0, first_new - (S - 1)) / S * S) : nb;
+  const bool coh_prologue = FUSED && first_new <= S - 2;
+  if (coh_prologue) wait_appended(a);
   if (nb > 0) {
-    if (FUSED && first_new <= S - 2) {
+    if (coh_prologue) {
 #pragma unroll
       for (int k = 0; k < S - 1; ++k)
         dma(std::true_type{}, it.key0 + min(k, nb - 1) * 32, lds + k * C::STAGE);
@@ -802,7 +803,12 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     }
   };
   run(std::false_type{}, b_coh);
-  if constexpr (FUSED) run(std::true_type{}, nb);
+  if constexpr (FUSED) {
+    if (b < nb) {
+      if (!coh_prologue) wait_appended(a);
+      run(std::true_type{}, nb);
+    }
+  }
   lds_dma_wait();  // no copy may land after this workgroup has left
 
   // epilogue
@@ -1091,87 +1097,110 @@ struct AppendArgs {
 };
 
 // The rows of one append segment (consecutive new tokens of one request that
-// land in one page) for kv heads h0 .. h0 + nh - 1: key rows are copied as
-// they are; value rows are transposed into the dim-major page ([D][16 slots]),
-// as whole 16-byte half rows where a segment covers them, else slot by slot.
-// Each thread issues the loads of kUnits units before their stores, so a
-// workgroup takes few memory round trips whatever the number of heads.
-// DEVICE_SCOPE writes through to the device coherence point (for readers in
-// the same launch on other dies).
-constexpr int kUnits = 4;
-template <int D, bool DEVICE_SCOPE>
-__device__ void append_rows(const AppendArgs& ap, const AppendSeg& sg, const int32_t* bt, int h0,
-                            int nh, int hkv, int maxp) {
+// land in one page) for kv head h: key rows are copied as they are; value
+// rows are transposed into the dim-major page ([D][16 slots]), as whole
+// 16-byte half rows where a segment covers them, else slot by slot.  At most
+// 16 rows: one key chunk and one value half row per thread.
+template <int D>
+__device__ void append_rows(const AppendArgs& ap, const AppendSeg& sg, const int32_t* bt, int h,
+                            int hkv, int maxp) {
   constexpr int CPR = D / 8;
+  static_assert(16 * CPR <= kThreads && 2 * D <= kThreads, "one unit per thread");
   const int slot0 = sg.pos0 % 16;
-  const size_t pb = (size_t)bt[(size_t)sg.req * maxp + sg.pos0 / 16] * hkv * 16 * D;
-  auto put16 = [](uint16_t* p, u32x4 v) {
-    if (DEVICE_SCOPE)
-      st16_dev(p, v);
-    else
-      st16(p, v);
-  };
-  // key rows: units (head, row, 16-byte chunk)
-  const int rows_c = sg.n * CPR;
-  const int nk = nh * rows_c;
-  for (int i0 = threadIdx.x; i0 < nk; i0 += kUnits * kThreads) {
-    u32x4 v[kUnits];
+  const size_t pb = (size_t)bt[(size_t)sg.req * maxp + sg.pos0 / 16] * hkv * 16 * D +
+                    (size_t)h * 16 * D;
+  const int t = threadIdx.x;
+  // key rows: (row, 16-byte chunk)
+  if (t < sg.n * CPR) {
+    const int r = t / CPR, c = t % CPR;
+    st16(ap.kc + pb + (size_t)(slot0 + r) * D + c * 8,
+         ld16(ap.k_new + ((size_t)(sg.row0 + r) * hkv + h) * D + c * 8));
+  }
+  // value rows: (dim, half page row of 8 slots), slots [lo, hi) of the half
+  if (t < 2 * D) {
+    const int d = t >> 1, half = t & 1;
+    const int lo = max(half * 8, slot0), hi = min(half * 8 + 8, slot0 + sg.n);
+    if (lo < hi) {
+      uint16_t* dst = ap.vc + pb + (size_t)d * 16;
+      auto src = [&](int sl) {
+        return (uint32_t)ap.v_new[((size_t)(sg.row0 + sl - slot0) * hkv + h) * D + d];
+      };
+      if (lo == half * 8 && hi == half * 8 + 8) {
+        uint32_t w[4];
 #pragma unroll
-    for (int u = 0; u < kUnits; ++u) {
-      const int idx = i0 + u * kThreads;
-      if (idx < nk) {
-        const int h = h0 + idx / rows_c, r = (idx % rows_c) / CPR, c = idx % CPR;
-        v[u] = ld16(ap.k_new + ((size_t)(sg.row0 + r) * hkv + h) * D + c * 8);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kUnits; ++u) {
-      const int idx = i0 + u * kThreads;
-      if (idx < nk) {
-        const int h = h0 + idx / rows_c, r = (idx % rows_c) / CPR, c = idx % CPR;
-        put16(ap.kc + pb + (size_t)h * 16 * D + (size_t)(slot0 + r) * D + c * 8, v[u]);
+        for (int i = 0; i < 4; ++i) w[i] = src(lo + 2 * i) | (src(lo + 2 * i + 1) << 16);
+        st16(dst + lo, u32x4{w[0], w[1], w[2], w[3]});
+      } else {
+        for (int sl = lo; sl < hi; ++sl) dst[sl] = (uint16_t)src(sl);
       }
     }
   }
-  // value rows: units (head, dim, half page row of 8 slots); a unit takes the
-  // slots [lo, hi) of its half that the segment covers
-  const int nv = nh * 2 * D;
-  for (int i0 = threadIdx.x; i0 < nv; i0 += kUnits * kThreads) {
-    uint32_t e[kUnits][8];
+}
+
+// One append segment for every kv head, in a fused launch (device-scope
+// stores).  Latency matters more than issue here (the launch's decode traffic
+// fills the memory queues), so each pass makes one round of 16-byte loads of
+// whole key and value rows for HG heads, stores the key rows, and transposes
+// the value rows through LDS into the dim-major page.
+template <int D>
+__device__ void append_segment_staged(const AppendArgs& ap, const AppendSeg& sg,
+                                      const int32_t* bt, int hkv, int maxp, char* lds) {
+  constexpr int CPR = D / 8;
+  constexpr int HG = 128 / CPR;                    // heads per pass
+  constexpr int UK = HG * 16 * CPR / kThreads;     // 16-byte units per thread per pass and kind
+  static_assert(UK * kThreads == HG * 16 * CPR, "whole units per thread");
+  static_assert(HG * 16 * D * 2 <= Cfg<D>::LDS, "staging fits the kernel's LDS");
+  const int n = sg.n, slot0 = sg.pos0 % 16;
+  const size_t pb = (size_t)bt[(size_t)sg.req * maxp + sg.pos0 / 16] * hkv * 16 * D;
+  uint16_t* vt = reinterpret_cast<uint16_t*>(lds);  // [HG][16 rows][D], token-major
+  for (int h0 = 0; h0 < hkv; h0 += HG) {
+    u32x4 kr[UK], vr[UK];
 #pragma unroll
-    for (int u = 0; u < kUnits; ++u) {
-      const int idx = i0 + u * kThreads;
-      const int h = h0 + idx / (2 * D), d = (idx >> 1) % D, half = idx & 1;
-      const int lo = max(half * 8, slot0), hi = min(half * 8 + 8, slot0 + sg.n);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int sl = half * 8 + k;
-        e[u][k] = (idx < nv && sl >= lo && sl < hi)
-                      ? ap.v_new[((size_t)(sg.row0 + sl - slot0) * hkv + h) * D + d]
-                      : 0u;
+    for (int k = 0; k < UK; ++k) {
+      const int idx = threadIdx.x + k * kThreads;  // (head, row, 16-byte chunk)
+      const int hl = idx / (16 * CPR), r = (idx / CPR) & 15, c = idx % CPR;
+      if (h0 + hl < hkv && r < n) {
+        const size_t off = ((size_t)(sg.row0 + r) * hkv + h0 + hl) * D + c * 8;
+        kr[k] = ld16(ap.k_new + off);
+        vr[k] = ld16(ap.v_new + off);
       }
     }
+    // All rows have landed before the first store: the compiler's own waits
+    // (the loads sit in masked branches) would otherwise also wait for the
+    // write-through stores issued in between, one round trip per unit.
+    vm_wait<0>();
 #pragma unroll
-    for (int u = 0; u < kUnits; ++u) {
-      const int idx = i0 + u * kThreads;
-      if (idx >= nv) continue;
-      const int h = h0 + idx / (2 * D), d = (idx >> 1) % D, half = idx & 1;
-      const int lo = max(half * 8, slot0), hi = min(half * 8 + 8, slot0 + sg.n);
-      if (lo >= hi) continue;
-      uint16_t* dst = ap.vc + pb + (size_t)h * 16 * D + (size_t)d * 16;
+    for (int k = 0; k < UK; ++k) {
+      const int idx = threadIdx.x + k * kThreads;
+      const int hl = idx / (16 * CPR), r = (idx / CPR) & 15, c = idx % CPR;
+      if (h0 + hl < hkv && r < n) {
+        st16_dev(ap.kc + pb + (size_t)(h0 + hl) * 16 * D + (size_t)(slot0 + r) * D + c * 8, kr[k]);
+        st16(vt + ((size_t)hl * 16 + r) * D + c * 8, vr[k]);
+      }
+    }
+    __syncthreads();
+    // value pages: units (head, dim, half page row of 8 slots)
+    for (int idx = threadIdx.x; idx < HG * 2 * D; idx += kThreads) {
+      const int hl = idx / (2 * D), d = (idx >> 1) % D, half = idx & 1;
+      const int lo = max(half * 8, slot0), hi = min(half * 8 + 8, slot0 + n);
+      if (h0 + hl >= hkv || lo >= hi) continue;
+      const uint16_t* col = vt + (size_t)hl * 16 * D + d;  // row s - slot0 at col[(s - slot0) * D]
+      uint16_t* dst = ap.vc + pb + (size_t)(h0 + hl) * 16 * D + (size_t)d * 16;
       if (lo == half * 8 && hi == half * 8 + 8) {
-        put16(dst + lo, u32x4{e[u][0] | (e[u][1] << 16), e[u][2] | (e[u][3] << 16),
-                              e[u][4] | (e[u][5] << 16), e[u][6] | (e[u][7] << 16)});
-      } else {
-        for (int sl = lo; sl < hi; ++sl) {
-          const uint16_t x = (uint16_t)e[u][sl - half * 8];
-          if (DEVICE_SCOPE)
-            __hip_atomic_store(dst + sl, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          else
-            dst[sl] = x;
+        uint32_t w[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int s0 = half * 8 + 2 * i - slot0;
+          w[i] = (uint32_t)col[s0 * D] | ((uint32_t)col[(s0 + 1) * D] << 16);
         }
+        st16_dev(dst + half * 8, u32x4{w[0], w[1], w[2], w[3]});
+      } else {
+        for (int sl = lo; sl < hi; ++sl)
+          __hip_atomic_store(dst + sl, col[(sl - slot0) * D], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
       }
     }
+    __syncthreads();  // the next pass reuses the staging area
   }
 }
 
@@ -1183,7 +1212,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint8_t* plan
   const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(plan);
   const AppendSeg sg = reinterpret_cast<const AppendSeg*>(plan + ap.off_segments)[blockIdx.x];
   if (hdr->magic != kPlanMagic || hdr->hash != hash) return;
-  append_rows<D, false>(ap, sg, bt, blockIdx.y, 1, hkv, maxp);
+  append_rows<D>(ap, sg, bt, blockIdx.y, hkv, maxp);
 }
 
 // kv_append and mixed attention in one launch.  Workgroups 0 .. append_wgs-1
@@ -1202,7 +1231,7 @@ __global__ __launch_bounds__(kThreads, 2) void append_attention_kernel(AttnArgs 
   if ((int)blockIdx.x < a.append_wgs) {
     const AppendSeg sg = reinterpret_cast<const AppendSeg*>(a.plan + ap.off_segments)[blockIdx.x];
     if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
-    append_rows<D, true>(ap, sg, a.bt, 0, a.hkv, a.hkv, a.maxp);
+    append_segment_staged<D>(ap, sg, a.bt, a.hkv, a.maxp, lds);
     vm_wait<0>();  // this thread's device-scope stores have completed
     __syncthreads();
     if (threadIdx.x == 0)
