@@ -23,6 +23,10 @@ Other modes (all single GPU):
   --traffic-json OUT --traffic-json-inputs F W CF CW
                      HBM traffic summary from rocprofv3 FETCH_SIZE / WRITE_SIZE CSVs
   --sweep-md JSONL   markdown tables of a --sweep file
+  --predictor OUT    batch latency predictor (Sec. 3.2, Eq. 5): time the fused
+                     launch on random batches of the three scenes, fit the
+                     library's predictor on 70% of them, report MAE / RMSE / R^2
+                     on the other 30% (as the paper's Tab. 5)
 """
 from __future__ import annotations
 
@@ -33,6 +37,8 @@ import os
 import statistics
 import sys
 import time
+
+import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -393,6 +399,116 @@ def main_traffic_json(args):
     print(json.dumps(out))
 
 
+# The paper evaluates its predictor on Qwen2.5-7B (Tab. 5): its attention shape
+# at one GPU is 28 q / 4 kv heads, D = 128.
+PRED_SHAPE = (28, 4, 128)
+
+
+def predictor_batch(rng, scene):
+    """(q_len, ctx_len) of a random batch of one scene (1 pure decode, 2 pure
+    prefill, 3 mixed): 1..256 decodes with u ~ round(LogN(7.2, 1.0)) in
+    [16, 16384], 1..4 chunks with c ~ U[16, 2048], u ~ U[0, 8192]."""
+    nd = 0 if scene == 2 else int(rng.integers(1, 256, endpoint=True))
+    npf = 0 if scene == 1 else int(rng.integers(1, 4, endpoint=True))
+    c = [int(rng.integers(16, 2048, endpoint=True)) for _ in range(npf)] + [1] * nd
+    u = [int(rng.integers(0, 8192, endpoint=True)) for _ in range(npf)] + [
+        int(np.clip(np.rint(rng.lognormal(7.2, 1.0)), 16, 16384)) for _ in range(nd)]
+    return c, u
+
+
+def pred_metrics(y, yhat):
+    y, yhat = np.asarray(y, dtype=np.float64), np.asarray(yhat, dtype=np.float64)
+    r = y - yhat
+    ss_tot = float(np.sum((y - y.mean()) ** 2))
+    return {"n": int(len(y)), "mae_us": round(float(np.mean(np.abs(r))), 3),
+            "rmse_us": round(float(np.sqrt(np.mean(r * r))), 3),
+            "r2": round(1.0 - float(np.sum(r * r)) / ss_tot, 5) if ss_tot > 0 else None}
+
+
+def main_predictor(args):
+    import torch
+    from paper_2606_05933_amd import ssa
+    torch.cuda.set_device(0)
+    hq, hkv, d = PRED_SHAPE
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([args.seed, 11])))
+    batches = [(1 + k % 3,) + predictor_batch(rng, 1 + k % 3)
+               for k in range(args.predictor_samples)]
+    need = [[(u + c + 15) // 16 for c, u in zip(cs, us)] for _, cs, us in batches]
+    num_pages = max(sum(nd) for nd in need) + 64
+    maxp = max(max(nd) for nd in need)
+    max_t = max(sum(cs) for _, cs, _ in batches)
+    max_n = max(len(cs) for _, cs, _ in batches)
+    shape = ssa.make_shape(hq, hkv, d, num_pages, maxp, d ** -0.5)
+    plan_bytes = ws_bytes = 0
+    for _, cs, us in batches:
+        pb, wb = ssa.ssa_plan_size(shape, cs, us)
+        plan_bytes, ws_bytes = max(plan_bytes, pb), max(ws_bytes, wb)
+    dev, bf = "cuda", torch.bfloat16
+    log(f"[predictor] {len(batches)} batches, pools of {num_pages} pages")
+    kc = torch.empty(num_pages * hkv * 16 * d, dtype=bf, device=dev).normal_()
+    vc = torch.empty_like(kc).normal_()
+    q = torch.empty(max_t * hq * d, dtype=bf, device=dev).normal_()
+    kn = torch.empty(max_t * hkv * d, dtype=bf, device=dev).normal_()
+    vn = torch.empty_like(kn).normal_()
+    out = torch.empty_like(q)
+    bt = torch.zeros(max_n * maxp, dtype=torch.int32, device=dev)
+    ws = torch.zeros(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    plan = torch.zeros(max(plan_bytes, 128), dtype=torch.uint8).pin_memory()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(5)]
+    for a, b in evs:
+        a.record()
+        b.record()
+    rows = []
+    for k, (scene, cs, us) in enumerate(batches):
+        table = np.zeros((max_n, maxp), dtype=np.int32)
+        pages = rng.permutation(num_pages)
+        off = 0
+        for i, npg in enumerate(need[k]):
+            table[i, :npg] = pages[off: off + npg]
+            off += npg
+        torch.cuda.synchronize()
+        bt.copy_(torch.from_numpy(table.reshape(-1)))
+        _, info = ssa.ssa_plan(shape, cs, us, out=plan)
+        call = ssa.bind_append_attention(shape, plan, plan, q, kn, vn, kc, vc, bt, out, ws)
+        call()
+        call()
+        for a, b in evs:
+            call(a, b)
+        torch.cuda.synchronize()
+        t_us = statistics.median(a.elapsed_time(b) for a, b in evs) * 1e3
+        rows.append({"scene": int(info.scene), "x": [float(v) for v in info.x],
+                     "us": round(t_us, 3), "reqs": len(cs), "tokens": int(sum(cs))})
+        if k % 100 == 99:
+            log(f"[predictor] {k + 1} batches timed")
+    order = np.random.Generator(np.random.PCG64(args.seed)).permutation(len(rows))
+    n_train = int(round(0.7 * len(rows)))
+    train, test = order[:n_train], order[n_train:]
+    res = {"shape": {"hq": hq, "hkv": hkv, "d": d}, "latency": "ssa_append_attention kernel, us",
+           "samples": len(rows), "train": int(len(train)), "test": int(len(test)),
+           "min_scene_samples": args.predictor_min_scene, "models": {}}
+    for label, min_scene in (("scene experts + global", args.predictor_min_scene),
+                             ("global only", 1 << 30)):
+        p = ssa.Predictor(min_scene_samples=min(min_scene, 1 << 30))
+        for i in train:
+            p.add(rows[i]["x"], rows[i]["scene"], rows[i]["us"])
+        p.fit()
+        entry = {}
+        for split, idx in (("train", train), ("test", test)):
+            for sc, name in ((0, "all"), (1, "pure decode"), (2, "pure prefill"), (3, "mixed")):
+                sel = [i for i in idx if sc == 0 or rows[i]["scene"] == sc]
+                y = [rows[i]["us"] for i in sel]
+                yh = [p.predict(rows[i]["x"], rows[i]["scene"]) for i in sel]
+                entry[f"{split}/{name}"] = pred_metrics(y, yh)
+        entry["coef"] = {m: (None if p.coefficients(m) is None else
+                             [float(v) for v in p.coefficients(m)]) for m in range(4)}
+        res["models"][label] = entry
+    if args.predictor:
+        with open(args.predictor, "w") as f:
+            json.dump({"summary": res, "rows": rows}, f)
+    print(json.dumps(res), flush=True)
+
+
 def main_sweep_md(args):
     """Markdown tables of a --sweep JSON-lines file, one per workload."""
     rows = [json.loads(l) for l in open(args.sweep_md) if l.strip()]
@@ -458,6 +574,10 @@ def main():
                                                                "COPY_WRITE"))
     ap.add_argument("--sweep-md", metavar="JSONL", default=None,
                     help="print the latency-vs-chunk tables of a --sweep file")
+    ap.add_argument("--predictor", metavar="OUT", default=None,
+                    help="fit and evaluate the batch latency predictor on measured batches")
+    ap.add_argument("--predictor-samples", type=int, default=600)
+    ap.add_argument("--predictor-min-scene", type=int, default=32)
     args = ap.parse_args()
     if args.traffic_json:
         return main_traffic_json(args)
@@ -475,6 +595,8 @@ def main():
         main_copy_probe(args)
     elif args.only_attention:
         main_only_attention(args)
+    elif args.predictor:
+        main_predictor(args)
     else:
         main_bench(args)
 

@@ -71,7 +71,8 @@ enum {
   SSA_ERR_PLAN_MISMATCH = -9, /* plan_host is not a plan of this shape (magic/hash) */
   SSA_ERR_HIP = -10,          /* a HIP launch failed */
   SSA_ERR_SCALE = -11,        /* softmax_scale negative or not finite */
-  SSA_ERR_TUNING = -12        /* a tuning field out of range */
+  SSA_ERR_TUNING = -12,       /* a tuning field out of range */
+  SSA_ERR_ARG = -13           /* another argument out of range (ssa_predictor.h) */
 };
 
 /* Scene of a batch (Sec. 3.2, Eq. 3).  A batch with no new token is EMPTY. */

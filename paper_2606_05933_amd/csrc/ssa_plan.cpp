@@ -524,6 +524,7 @@ const char* ssa_status_string(int code) {
     case SSA_ERR_HIP: return "HIP launch failed";
     case SSA_ERR_SCALE: return "softmax_scale is negative or not finite";
     case SSA_ERR_TUNING: return "tuning field out of range";
+    case SSA_ERR_ARG: return "an argument out of range";
     default: return "unknown";
   }
 }

@@ -43,6 +43,18 @@ class SsaTuning(ctypes.Structure):
                 ("num_xcds", ctypes.c_int32), ("mix_order", ctypes.c_int32)]
 
 
+PRED_FEATURES, PRED_MODELS, PRED_MOMENTS = 7, 4, 45
+
+
+class SsaPredictor(ctypes.Structure):
+    """ssa_predictor (include/ssa_predictor.h): caller-owned plain data."""
+    _fields_ = [("samples", ctypes.c_int64 * PRED_MODELS),
+                ("moments", (ctypes.c_double * PRED_MOMENTS) * PRED_MODELS),
+                ("coef", (ctypes.c_double * (1 + PRED_FEATURES)) * PRED_MODELS),
+                ("fitted", ctypes.c_int32 * PRED_MODELS),
+                ("min_scene_samples", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 class SsaPlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "num_reqs", "num_tokens", "num_decode_reqs", "num_chunk_reqs", "num_items",
@@ -110,6 +122,14 @@ def _load():
     lib.ssa_append_attention.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                          vp, vp, vp]
     lib.ssa_append_attention.restype = ctypes.c_int
+    dp = P(ctypes.c_double)
+    lib.ssa_predictor_init.argtypes = [P(SsaPredictor), ctypes.c_int32]
+    lib.ssa_predictor_add.argtypes = [P(SsaPredictor), dp, ctypes.c_int32, ctypes.c_double]
+    lib.ssa_predictor_fit.argtypes = [P(SsaPredictor)]
+    lib.ssa_predictor_predict.argtypes = [P(SsaPredictor), dp, ctypes.c_int32, dp]
+    for f in ("ssa_predictor_init", "ssa_predictor_add", "ssa_predictor_fit",
+              "ssa_predictor_predict"):
+        getattr(lib, f).restype = ctypes.c_int
     return lib
 
 
@@ -117,7 +137,56 @@ LIB = _load()
 
 EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
             "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed",
-            "ssa_append_attention")
+            "ssa_append_attention", "ssa_predictor_init", "ssa_predictor_add",
+            "ssa_predictor_fit", "ssa_predictor_predict")
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise SsaError(rc, what)
+
+
+class Predictor:
+    """Batch latency predictor (Sec. 3.2, Eq. 5): argument marshalling around
+    ssa_predictor_*; every step runs in the library."""
+
+    def __init__(self, min_scene_samples: int = 16):
+        self.p = SsaPredictor()
+        _check(LIB.ssa_predictor_init(ctypes.byref(self.p), int(min_scene_samples)),
+               "ssa_predictor_init")
+
+    @staticmethod
+    def _x(x):
+        a = (ctypes.c_double * PRED_FEATURES)(*[float(v) for v in x])
+        if len(x) != PRED_FEATURES:
+            raise ValueError(f"{PRED_FEATURES} features expected")
+        return a
+
+    def add(self, x, scene: int, latency: float):
+        _check(LIB.ssa_predictor_add(ctypes.byref(self.p), self._x(x), int(scene),
+                                     float(latency)), "ssa_predictor_add")
+
+    def fit(self):
+        _check(LIB.ssa_predictor_fit(ctypes.byref(self.p)), "ssa_predictor_fit")
+        return self
+
+    def predict(self, x, scene: int) -> float:
+        out = ctypes.c_double()
+        _check(LIB.ssa_predictor_predict(ctypes.byref(self.p), self._x(x), int(scene),
+                                         ctypes.byref(out)), "ssa_predictor_predict")
+        return out.value
+
+    def coefficients(self, model: int):
+        """(b, w1..w7) of model 0 (global) or a scene, or None if not fitted."""
+        if not self.p.fitted[model]:
+            return None
+        return np.array(list(self.p.coef[model]), dtype=np.float64)
+
+    def copy(self) -> "Predictor":
+        q = Predictor.__new__(Predictor)
+        q.p = SsaPredictor()
+        ctypes.memmove(ctypes.byref(q.p), ctypes.byref(self.p), ctypes.sizeof(SsaPredictor))
+        return q
 
 
 def ssa_status_string(code: int) -> str:

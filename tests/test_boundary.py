@@ -48,8 +48,11 @@ def shape_of(hq, hkv, d, q_len, ctx_len, extra_pages=0, num_pages=None, scale=No
 
 
 def test_library_exports_every_declared_symbol():
-    text = open(os.path.join(ROOT, "include", "ssa.h")).read()
-    declared = set(re.findall(r"\b(ssa_[a-z_]+)\s*\(", text))
+    declared = set()
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if h.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", h)).read()
+            declared |= set(re.findall(r"\b(ssa_[a-z_]+)\s*\(", text))
     assert declared == set(ssa.EXPORTED)
     lib = ctypes.CDLL(ssa.LIB_PATH)
     for name in declared:
