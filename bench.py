@@ -27,6 +27,10 @@ Other modes (all single GPU):
                      launch on random batches of the three scenes, fit the
                      library's predictor on 70% of them, report MAE / RMSE / R^2
                      on the other 30% (as the paper's Tab. 5)
+  --chunker OUT      SlidingChunker (Sec. 3.4, Alg. 1) on that predictor: each
+                     decision's batch runs on the GPU; reports the measured
+                     latency against the prediction and T_cur, and the window
+                     cost against the best budget
 """
 from __future__ import annotations
 
@@ -425,62 +429,106 @@ def pred_metrics(y, yhat):
             "r2": round(1.0 - float(np.sum(r * r)) / ss_tot, 5) if ss_tot > 0 else None}
 
 
+class BatchTimer:
+    """Times the fused launch (ssa_append_attention) of arbitrary batches
+    {(c_i, u_i)} of one shape: pools, new rows and queries sized once for the
+    largest batch, filled with N(0, 1) bf16; each batch gets a random block
+    table, a host plan and 2 + 5 launches (the median of the 5, from events the
+    kernel stamps itself)."""
+
+    def __init__(self, shape3, max_pages, max_pages_per_req, max_tokens, max_reqs, plan_bytes,
+                 ws_bytes, seed):
+        import torch
+        from paper_2606_05933_amd import ssa
+        self.torch, self.ssa = torch, ssa
+        hq, hkv, d = shape3
+        dev, bf = "cuda", torch.bfloat16
+        self.num_pages, self.maxp, self.max_reqs = max_pages, max_pages_per_req, max_reqs
+        self.shape = ssa.make_shape(hq, hkv, d, max_pages, max_pages_per_req, d ** -0.5)
+        self.kc = torch.empty(max_pages * hkv * 16 * d, dtype=bf, device=dev).normal_()
+        self.vc = torch.empty_like(self.kc).normal_()
+        self.q = torch.empty(max_tokens * hq * d, dtype=bf, device=dev).normal_()
+        self.kn = torch.empty(max_tokens * hkv * d, dtype=bf, device=dev).normal_()
+        self.vn = torch.empty_like(self.kn).normal_()
+        self.out = torch.empty_like(self.q)
+        self.bt = torch.zeros(max_reqs * max_pages_per_req, dtype=torch.int32, device=dev)
+        self.ws = torch.zeros(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+        self.plan = torch.zeros(max(plan_bytes, 128), dtype=torch.uint8).pin_memory()
+        self.evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    for _ in range(5)]
+        for a, b in self.evs:
+            a.record()
+            b.record()
+        self.rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 12])))
+
+    def time(self, cs, us):
+        """(kernel us, plan info) of the batch."""
+        torch, ssa = self.torch, self.ssa
+        table = np.zeros((self.max_reqs, self.maxp), dtype=np.int32)
+        pages = self.rng.permutation(self.num_pages)
+        off = 0
+        for i, (c, u) in enumerate(zip(cs, us)):
+            npg = (u + c + 15) // 16
+            table[i, :npg] = pages[off: off + npg]
+            off += npg
+        torch.cuda.synchronize()
+        self.bt.copy_(torch.from_numpy(table.reshape(-1)))
+        _, info = ssa.ssa_plan(self.shape, cs, us, out=self.plan)
+        call = ssa.bind_append_attention(self.shape, self.plan, self.plan, self.q, self.kn,
+                                         self.vn, self.kc, self.vc, self.bt, self.out, self.ws)
+        call()
+        call()
+        for a, b in self.evs:
+            call(a, b)
+        torch.cuda.synchronize()
+        return statistics.median(a.elapsed_time(b) for a, b in self.evs) * 1e3, info
+
+
+def timer_for(batches, seed):
+    """A BatchTimer sized for every (c list, u list) in ``batches``."""
+    from paper_2606_05933_amd import ssa
+    hq, hkv, d = PRED_SHAPE
+    need = [[(u + c + 15) // 16 for c, u in zip(cs, us)] for cs, us in batches]
+    num_pages = max(sum(nd) for nd in need) + 64
+    maxp = max(max(nd) for nd in need)
+    shape = ssa.make_shape(hq, hkv, d, num_pages, maxp, d ** -0.5)
+    plan_bytes = ws_bytes = 0
+    for cs, us in batches:
+        pb, wb = ssa.ssa_plan_size(shape, cs, us)
+        plan_bytes, ws_bytes = max(plan_bytes, pb), max(ws_bytes, wb)
+    return BatchTimer(PRED_SHAPE, num_pages, maxp, max(sum(cs) for cs, _ in batches),
+                      max(len(cs) for cs, _ in batches), plan_bytes, ws_bytes, seed)
+
+
+def fit_predictor(rows, idx, min_scene):
+    from paper_2606_05933_amd import ssa
+    p = ssa.Predictor(min_scene_samples=min_scene)
+    for i in idx:
+        p.add(rows[i]["x"], rows[i]["scene"], rows[i]["us"])
+    return p.fit()
+
+
+def time_batches(timer, batches, tag):
+    rows = []
+    for k, (scene, cs, us) in enumerate(batches):
+        t_us, info = timer.time(cs, us)
+        rows.append({"scene": int(info.scene), "x": [float(v) for v in info.x],
+                     "us": round(t_us, 3), "reqs": len(cs), "tokens": int(sum(cs))})
+        if k % 100 == 99:
+            log(f"[{tag}] {k + 1} batches timed")
+    return rows
+
+
 def main_predictor(args):
     import torch
-    from paper_2606_05933_amd import ssa
     torch.cuda.set_device(0)
     hq, hkv, d = PRED_SHAPE
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([args.seed, 11])))
     batches = [(1 + k % 3,) + predictor_batch(rng, 1 + k % 3)
                for k in range(args.predictor_samples)]
-    need = [[(u + c + 15) // 16 for c, u in zip(cs, us)] for _, cs, us in batches]
-    num_pages = max(sum(nd) for nd in need) + 64
-    maxp = max(max(nd) for nd in need)
-    max_t = max(sum(cs) for _, cs, _ in batches)
-    max_n = max(len(cs) for _, cs, _ in batches)
-    shape = ssa.make_shape(hq, hkv, d, num_pages, maxp, d ** -0.5)
-    plan_bytes = ws_bytes = 0
-    for _, cs, us in batches:
-        pb, wb = ssa.ssa_plan_size(shape, cs, us)
-        plan_bytes, ws_bytes = max(plan_bytes, pb), max(ws_bytes, wb)
-    dev, bf = "cuda", torch.bfloat16
-    log(f"[predictor] {len(batches)} batches, pools of {num_pages} pages")
-    kc = torch.empty(num_pages * hkv * 16 * d, dtype=bf, device=dev).normal_()
-    vc = torch.empty_like(kc).normal_()
-    q = torch.empty(max_t * hq * d, dtype=bf, device=dev).normal_()
-    kn = torch.empty(max_t * hkv * d, dtype=bf, device=dev).normal_()
-    vn = torch.empty_like(kn).normal_()
-    out = torch.empty_like(q)
-    bt = torch.zeros(max_n * maxp, dtype=torch.int32, device=dev)
-    ws = torch.zeros(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
-    plan = torch.zeros(max(plan_bytes, 128), dtype=torch.uint8).pin_memory()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(5)]
-    for a, b in evs:
-        a.record()
-        b.record()
-    rows = []
-    for k, (scene, cs, us) in enumerate(batches):
-        table = np.zeros((max_n, maxp), dtype=np.int32)
-        pages = rng.permutation(num_pages)
-        off = 0
-        for i, npg in enumerate(need[k]):
-            table[i, :npg] = pages[off: off + npg]
-            off += npg
-        torch.cuda.synchronize()
-        bt.copy_(torch.from_numpy(table.reshape(-1)))
-        _, info = ssa.ssa_plan(shape, cs, us, out=plan)
-        call = ssa.bind_append_attention(shape, plan, plan, q, kn, vn, kc, vc, bt, out, ws)
-        call()
-        call()
-        for a, b in evs:
-            call(a, b)
-        torch.cuda.synchronize()
-        t_us = statistics.median(a.elapsed_time(b) for a, b in evs) * 1e3
-        rows.append({"scene": int(info.scene), "x": [float(v) for v in info.x],
-                     "us": round(t_us, 3), "reqs": len(cs), "tokens": int(sum(cs))})
-        if k % 100 == 99:
-            log(f"[predictor] {k + 1} batches timed")
+    timer = timer_for([(cs, us) for _, cs, us in batches], args.seed)
+    log(f"[predictor] {len(batches)} batches, pools of {timer.num_pages} pages")
+    rows = time_batches(timer, batches, "predictor")
     order = np.random.Generator(np.random.PCG64(args.seed)).permutation(len(rows))
     n_train = int(round(0.7 * len(rows)))
     train, test = order[:n_train], order[n_train:]
@@ -489,10 +537,7 @@ def main_predictor(args):
            "min_scene_samples": args.predictor_min_scene, "models": {}}
     for label, min_scene in (("scene experts + global", args.predictor_min_scene),
                              ("global only", 1 << 30)):
-        p = ssa.Predictor(min_scene_samples=min(min_scene, 1 << 30))
-        for i in train:
-            p.add(rows[i]["x"], rows[i]["scene"], rows[i]["us"])
-        p.fit()
+        p = fit_predictor(rows, train, min_scene)
         entry = {}
         for split, idx in (("train", train), ("test", test)):
             for sc, name in ((0, "all"), (1, "pure decode"), (2, "pure prefill"), (3, "mixed")):
@@ -506,6 +551,83 @@ def main_predictor(args):
     if args.predictor:
         with open(args.predictor, "w") as f:
             json.dump({"summary": res, "rows": rows}, f)
+    print(json.dumps(res), flush=True)
+
+
+def chunker_state(rng):
+    """A scheduler state: 0..256 decodes (u ~ round(LogN(7.2, 1.0)) in
+    [16, 16384]), 1..6 waiting prefills in priority order (cached ~ U[0, 8192],
+    remaining ~ U[64, 4096]), the server budget B = |D| + 4096 and the window's
+    two latency bounds T_cur, T_next ~ U[60, 400] us."""
+    nd = int(rng.integers(0, 256, endpoint=True))
+    dctx = [int(np.clip(np.rint(rng.lognormal(7.2, 1.0)), 16, 16384)) for _ in range(nd)]
+    pf = [(int(rng.integers(0, 8192, endpoint=True)), int(rng.integers(64, 4096, endpoint=True)))
+          for _ in range(int(rng.integers(1, 6, endpoint=True)))]
+    return dctx, pf, nd + 4096, float(rng.uniform(60, 400)), float(rng.uniform(60, 400))
+
+
+def main_chunker(args):
+    """SlidingChunker (Alg. 1) with a predictor fitted on measured launches:
+    each decision's batch is run on the GPU and its measured latency compared
+    with the prediction and with T_cur; the chosen window cost is compared with
+    the best over every budget (exhaustive, on the host)."""
+    import torch
+    from paper_2606_05933_amd import ssa
+    torch.cuda.set_device(0)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([args.seed, 13])))
+    train = [(1 + k % 3,) + predictor_batch(rng, 1 + k % 3) for k in range(args.predictor_samples)]
+    states = [chunker_state(rng) for _ in range(args.chunker_states)]
+
+    def formed(dctx, pf, b, B):
+        chunks, _, _ = ssa.form_batch(dctx, pf, b, B)
+        cs = [1] * len(dctx) + [c for c in chunks if c > 0]
+        us = list(dctx) + [p[0] for p, c in zip(pf, chunks) if c > 0]
+        return cs, us
+
+    # the largest batch any decision can form: every decode and every prefill in full
+    bound = [formed(d, pf, B, B) for d, pf, B, _, _ in states]
+    timer = timer_for([(cs, us) for _, cs, us in train] + [b for b in bound if b[0]], args.seed)
+    rows = time_batches(timer, train, "chunker: predictor samples")
+    pred = fit_predictor(rows, range(len(rows)), args.predictor_min_scene)
+    out, t_host = [], []
+    for k, (dctx, pf, B, t_cur, t_next) in enumerate(states):
+        t0 = time.perf_counter()
+        b, chunks, t_pred = ssa.sliding_chunker(pred, dctx, pf, B, t_cur, t_next)
+        t_host.append(time.perf_counter() - t0)
+        b_cur = ssa.time_to_budget(pred, dctx, pf, B, t_cur)
+        b_sum = b_cur + ssa.time_to_budget(pred, dctx, pf, B, t_next)
+
+        def pb(x):
+            _, feats, sc = ssa.form_batch(dctx, pf, x, B)
+            return 0.0 if sc == 0 else pred.predict(feats, sc)
+        costs = [pb(x) + pb(b_sum - x) for x in range(len(dctx), min(B, b_cur) + 1)]
+        best = min(costs)
+        cs, us = formed(dctx, pf, b, B)
+        t_meas = timer.time(cs, us)[0] if cs else 0.0
+        out.append({"decodes": len(dctx), "prefills": len(pf), "B": B, "t_cur": round(t_cur, 2),
+                    "t_next": round(t_next, 2), "b_cur": b_cur, "b_sum": b_sum, "budget": b,
+                    "chunks": chunks, "t_pred": round(t_pred, 3), "t_measured": round(t_meas, 3),
+                    "window_cost": round(pb(b) + pb(b_sum - b), 3), "window_best": round(best, 3)})
+        if k % 50 == 49:
+            log(f"[chunker] {k + 1} decisions")
+    meas = np.array([o["t_measured"] for o in out])
+    prd = np.array([o["t_pred"] for o in out])
+    tc = np.array([o["t_cur"] for o in out])
+    gap = np.array([(o["window_cost"] - o["window_best"]) / max(o["window_best"], 1e-9)
+                    for o in out])
+    feasible = np.array([o["b_cur"] > o["decodes"] for o in out])
+    res = {"states": len(out), "predictor_samples": len(rows),
+           "host_us_per_decision": {"median": round(statistics.median(t_host) * 1e6, 1),
+                                    "max": round(max(t_host) * 1e6, 1)},
+           "window_cost_gap": {"optimal_fraction": round(float(np.mean(gap <= 1e-12)), 4),
+                               "mean": round(float(gap.mean()), 6), "max": round(float(gap.max()), 6)},
+           "prediction_error_us": pred_metrics(meas, prd),
+           "within_t_cur": {"predicted": round(float(np.mean(prd[feasible] <= tc[feasible])), 4),
+                            "measured": round(float(np.mean(meas[feasible] <= tc[feasible])), 4),
+                            "states": int(feasible.sum())}}
+    if args.chunker:
+        with open(args.chunker, "w") as f:
+            json.dump({"summary": res, "decisions": out}, f)
     print(json.dumps(res), flush=True)
 
 
@@ -578,6 +700,9 @@ def main():
                     help="fit and evaluate the batch latency predictor on measured batches")
     ap.add_argument("--predictor-samples", type=int, default=600)
     ap.add_argument("--predictor-min-scene", type=int, default=32)
+    ap.add_argument("--chunker", metavar="OUT", default=None,
+                    help="SlidingChunker decisions on a measured predictor, run on the GPU")
+    ap.add_argument("--chunker-states", type=int, default=200)
     args = ap.parse_args()
     if args.traffic_json:
         return main_traffic_json(args)
@@ -597,6 +722,8 @@ def main():
         main_only_attention(args)
     elif args.predictor:
         main_predictor(args)
+    elif args.chunker:
+        main_chunker(args)
     else:
         main_bench(args)
 

@@ -55,6 +55,11 @@ class SsaPredictor(ctypes.Structure):
                 ("min_scene_samples", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class SsaPrefillRequest(ctypes.Structure):
+    """ssa_prefill_request (include/ssa_chunker.h)."""
+    _fields_ = [("cached", ctypes.c_int32), ("remaining", ctypes.c_int32)]
+
+
 class SsaPlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "num_reqs", "num_tokens", "num_decode_reqs", "num_chunk_reqs", "num_items",
@@ -127,8 +132,15 @@ def _load():
     lib.ssa_predictor_add.argtypes = [P(SsaPredictor), dp, ctypes.c_int32, ctypes.c_double]
     lib.ssa_predictor_fit.argtypes = [P(SsaPredictor)]
     lib.ssa_predictor_predict.argtypes = [P(SsaPredictor), dp, ctypes.c_int32, dp]
+    ip, i32 = P(ctypes.c_int32), ctypes.c_int32
+    lib.ssa_form_batch.argtypes = [ip, i32, P(SsaPrefillRequest), i32, i32, i32, ip, dp, ip]
+    lib.ssa_time_to_budget.argtypes = [P(SsaPredictor), ip, i32, P(SsaPrefillRequest), i32, i32,
+                                       ctypes.c_double, ip]
+    lib.ssa_sliding_chunker.argtypes = [P(SsaPredictor), ip, i32, P(SsaPrefillRequest), i32, i32,
+                                        ctypes.c_double, ctypes.c_double, ip, ip, dp]
     for f in ("ssa_predictor_init", "ssa_predictor_add", "ssa_predictor_fit",
-              "ssa_predictor_predict"):
+              "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
+              "ssa_sliding_chunker"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -138,7 +150,8 @@ LIB = _load()
 EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
             "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed",
             "ssa_append_attention", "ssa_predictor_init", "ssa_predictor_add",
-            "ssa_predictor_fit", "ssa_predictor_predict")
+            "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
+            "ssa_sliding_chunker")
 
 
 def _check(rc: int, what: str):
@@ -187,6 +200,47 @@ class Predictor:
         q.p = SsaPredictor()
         ctypes.memmove(ctypes.byref(q.p), ctypes.byref(self.p), ctypes.sizeof(SsaPredictor))
         return q
+
+
+def _queue(decode_ctx, prefill):
+    """(decode context lengths, [(cached, remaining), ...]) as C arrays."""
+    dctx = (ctypes.c_int32 * max(1, len(decode_ctx)))(*[int(v) for v in decode_ctx])
+    pf = (SsaPrefillRequest * max(1, len(prefill)))(
+        *[SsaPrefillRequest(int(c), int(r)) for c, r in prefill])
+    return dctx, len(decode_ctx), pf, len(prefill)
+
+
+def form_batch(decode_ctx, prefill, budget: int, max_budget: int):
+    """The batch a budget forms (Alg. 1's BatchForwarder): per-prefill chunks,
+    Tab. 1 features, Eq. 3 scene."""
+    dctx, nd, pf, npf = _queue(decode_ctx, prefill)
+    chunk = (ctypes.c_int32 * max(1, npf))()
+    x = (ctypes.c_double * PRED_FEATURES)()
+    scene = ctypes.c_int32()
+    _check(LIB.ssa_form_batch(dctx, nd, pf, npf, int(budget), int(max_budget), chunk, x,
+                              ctypes.byref(scene)), "ssa_form_batch")
+    return list(chunk)[:npf], list(x), scene.value
+
+
+def time_to_budget(pred: Predictor, decode_ctx, prefill, max_budget: int, t_limit: float) -> int:
+    dctx, nd, pf, npf = _queue(decode_ctx, prefill)
+    out = ctypes.c_int32()
+    _check(LIB.ssa_time_to_budget(ctypes.byref(pred.p), dctx, nd, pf, npf, int(max_budget),
+                                  float(t_limit), ctypes.byref(out)), "ssa_time_to_budget")
+    return out.value
+
+
+def sliding_chunker(pred: Predictor, decode_ctx, prefill, max_budget: int, t_cur: float,
+                    t_next: float):
+    """Alg. 1: (budget, per-prefill chunks, predicted latency of this iteration)."""
+    dctx, nd, pf, npf = _queue(decode_ctx, prefill)
+    budget = ctypes.c_int32()
+    chunk = (ctypes.c_int32 * max(1, npf))()
+    t = ctypes.c_double()
+    _check(LIB.ssa_sliding_chunker(ctypes.byref(pred.p), dctx, nd, pf, npf, int(max_budget),
+                                   float(t_cur), float(t_next), ctypes.byref(budget), chunk,
+                                   ctypes.byref(t)), "ssa_sliding_chunker")
+    return budget.value, list(chunk)[:npf], t.value
 
 
 def ssa_status_string(code: int) -> str:
