@@ -31,6 +31,10 @@ Other modes (all single GPU):
                      decision's batch runs on the GPU; reports the measured
                      latency against the prediction and T_cur, and the window
                      cost against the best budget
+  --constructor OUT  priority sorter + BatchConstructor (Sec. 3.3, 3.5, Alg. 2):
+                     where it reconstructs the batch, the full-budget batch and
+                     the constructed one both run on the GPU; reports how many
+                     requests meet their TTFT slack in each
 """
 from __future__ import annotations
 
@@ -631,6 +635,85 @@ def main_chunker(args):
     print(json.dumps(res), flush=True)
 
 
+def constructor_state(rng):
+    """A scheduler state with TTFT pressure: 0..128 decodes (u ~ round(LogN(7.2,
+    1.0)) in [16, 16384]), 2..10 prefilling or waiting requests (cached ~
+    U[0, 4096], remaining ~ U[32, 1024], TTFT slack ~ U[30, 300] us of this
+    path's time, 1 in 10 safeguarded), B = |D| + 4096."""
+    nd = int(rng.integers(0, 128, endpoint=True))
+    dctx = [int(np.clip(np.rint(rng.lognormal(7.2, 1.0)), 16, 16384)) for _ in range(nd)]
+    cands = [(int(rng.integers(0, 4096, endpoint=True)), int(rng.integers(32, 1024, endpoint=True)),
+              float(rng.uniform(30, 300)), int(rng.random() < 0.1))
+             for _ in range(int(rng.integers(2, 10, endpoint=True)))]
+    return dctx, cands, nd + 4096
+
+
+def main_constructor(args):
+    """Multi-Level Priority Sorter + BatchConstructor (Alg. 2) with a predictor
+    fitted on measured launches.  Where Alg. 2 reconstructs the batch, both the
+    full-budget batch and the constructed one run on the GPU; a candidate meets
+    its TTFT if its whole remaining prefill is in the batch and the batch's
+    measured time is within its slack."""
+    import torch
+    from paper_2606_05933_amd import ssa
+    torch.cuda.set_device(0)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([args.seed, 14])))
+    train = [(1 + k % 3,) + predictor_batch(rng, 1 + k % 3) for k in range(args.predictor_samples)]
+    states = [constructor_state(rng) for _ in range(args.constructor_states)]
+    rho, alpha, eps = 20.0, 1.0, 1e-3  # tokens per us of recent throughput; urgency threshold
+
+    def batch_of(dctx, cands, take):
+        cs = [1] * len(dctx) + [t for t in take if t > 0]
+        us = list(dctx) + [c[0] for c, t in zip(cands, take) if t > 0]
+        return cs, us
+
+    bound = [batch_of(d, c, [x[1] for x in c]) for d, c, _ in states]
+    timer = timer_for([(cs, us) for _, cs, us in train] + bound, args.seed)
+    rows = time_batches(timer, train, "constructor: predictor samples")
+    pred = fit_predictor(rows, range(len(rows)), args.predictor_min_scene)
+    outcomes = {0: 0, 1: 0, 2: 0}
+    met_full = met_built = risky_total = 0
+    t_host, pairs = [], []
+    for k, (dctx, cands, B) in enumerate(states):
+        t0 = time.perf_counter()
+        order = ssa.priority_sort(cands, rho, alpha, eps)
+        sc = [cands[i] for i in order]
+        outcome, budget, take, t_full = ssa.batch_constructor(pred, dctx, sc, B, eps)
+        t_host.append(time.perf_counter() - t0)
+        outcomes[outcome] += 1
+        if outcome != ssa.CONSTRUCT_BATCH:
+            continue
+        full_take, _, _ = ssa.form_batch(dctx, [(c[0], c[1]) for c in sc], B, B)
+        t_f = timer.time(*batch_of(dctx, sc, full_take))[0]
+        t_b = timer.time(*batch_of(dctx, sc, take))[0]
+        risky_total += sum(1 for c in sc if c[2] < t_full)
+        met_full += sum(1 for c, t in zip(sc, full_take) if t == c[1] and t_f <= c[2])
+        met_built += sum(1 for c, t in zip(sc, take) if t == c[1] and t_b <= c[2])
+        pairs.append({"t_full_pred": round(t_full, 2), "t_full": round(t_f, 2),
+                      "t_built": round(t_b, 2), "budget_full": B, "budget_built": budget,
+                      "met_full": sum(1 for c, t in zip(sc, full_take) if t == c[1] and t_f <= c[2]),
+                      "met_built": sum(1 for c, t in zip(sc, take) if t == c[1] and t_b <= c[2]),
+                      "candidates": len(sc)})
+        if k % 50 == 49:
+            log(f"[constructor] {k + 1} states")
+    res = {"states": len(states), "predictor_samples": len(rows),
+           "outcomes": {"no risk": outcomes[0], "no feasible anchor": outcomes[1],
+                        "reconstructed": outcomes[2]},
+           "host_us_per_decision": {"median": round(statistics.median(t_host) * 1e6, 1),
+                                    "max": round(max(t_host) * 1e6, 1)},
+           "reconstructed_states": {"candidates_meeting_ttft_full_batch": met_full,
+                                    "candidates_meeting_ttft_constructed": met_built,
+                                    "risky_candidates": risky_total,
+                                    "mean_latency_full_us": round(float(np.mean(
+                                        [p["t_full"] for p in pairs])), 2) if pairs else None,
+                                    "mean_latency_constructed_us": round(float(np.mean(
+                                        [p["t_built"] for p in pairs])), 2) if pairs else None}}
+    if args.constructor:
+        with open(args.constructor, "w") as f:
+            json.dump({"summary": res, "pairs": pairs}, f)
+    print(json.dumps(res), flush=True)
+
+
 def main_sweep_md(args):
     """Markdown tables of a --sweep JSON-lines file, one per workload."""
     rows = [json.loads(l) for l in open(args.sweep_md) if l.strip()]
@@ -703,6 +786,9 @@ def main():
     ap.add_argument("--chunker", metavar="OUT", default=None,
                     help="SlidingChunker decisions on a measured predictor, run on the GPU")
     ap.add_argument("--chunker-states", type=int, default=200)
+    ap.add_argument("--constructor", metavar="OUT", default=None,
+                    help="priority sorter + BatchConstructor on a measured predictor, on the GPU")
+    ap.add_argument("--constructor-states", type=int, default=300)
     args = ap.parse_args()
     if args.traffic_json:
         return main_traffic_json(args)
@@ -724,6 +810,8 @@ def main():
         main_predictor(args)
     elif args.chunker:
         main_chunker(args)
+    elif args.constructor:
+        main_constructor(args)
     else:
         main_bench(args)
 

@@ -60,6 +60,16 @@ class SsaPrefillRequest(ctypes.Structure):
     _fields_ = [("cached", ctypes.c_int32), ("remaining", ctypes.c_int32)]
 
 
+class SsaCandidate(ctypes.Structure):
+    """ssa_candidate (include/ssa_constructor.h)."""
+    _fields_ = [("cached", ctypes.c_int32), ("remaining", ctypes.c_int32),
+                ("slack", ctypes.c_double), ("safeguard", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+CONSTRUCT_NO_RISK, CONSTRUCT_NO_ANCHOR, CONSTRUCT_BATCH = 0, 1, 2
+
+
 class SsaPlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "num_reqs", "num_tokens", "num_decode_reqs", "num_chunk_reqs", "num_items",
@@ -138,9 +148,13 @@ def _load():
                                        ctypes.c_double, ip]
     lib.ssa_sliding_chunker.argtypes = [P(SsaPredictor), ip, i32, P(SsaPrefillRequest), i32, i32,
                                         ctypes.c_double, ctypes.c_double, ip, ip, dp]
+    lib.ssa_priority_sort.argtypes = [P(SsaCandidate), i32, ctypes.c_double, ctypes.c_double,
+                                      ctypes.c_double, ip]
+    lib.ssa_batch_constructor.argtypes = [P(SsaPredictor), ip, i32, P(SsaCandidate), i32, i32,
+                                          ctypes.c_double, ip, ip, ip, dp]
     for f in ("ssa_predictor_init", "ssa_predictor_add", "ssa_predictor_fit",
               "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
-              "ssa_sliding_chunker"):
+              "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -151,7 +165,7 @@ EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
             "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed",
             "ssa_append_attention", "ssa_predictor_init", "ssa_predictor_add",
             "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
-            "ssa_sliding_chunker")
+            "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor")
 
 
 def _check(rc: int, what: str):
@@ -228,6 +242,38 @@ def time_to_budget(pred: Predictor, decode_ctx, prefill, max_budget: int, t_limi
     _check(LIB.ssa_time_to_budget(ctypes.byref(pred.p), dctx, nd, pf, npf, int(max_budget),
                                   float(t_limit), ctypes.byref(out)), "ssa_time_to_budget")
     return out.value
+
+
+def _candidates(cands):
+    """[(cached, remaining, slack, safeguard), ...] as a C array."""
+    return (SsaCandidate * max(1, len(cands)))(
+        *[SsaCandidate(int(c), int(r), float(s), int(g), 0) for c, r, s, g in cands])
+
+
+def priority_sort(cands, throughput: float, alpha: float, eps: float):
+    """Eq. 12-13: candidate indices in priority order."""
+    arr = _candidates(cands)
+    order = (ctypes.c_int32 * max(1, len(cands)))()
+    _check(LIB.ssa_priority_sort(arr, len(cands), float(throughput), float(alpha), float(eps),
+                                 order), "ssa_priority_sort")
+    return list(order)[:len(cands)]
+
+
+def batch_constructor(pred: Predictor, decode_ctx, cands, max_budget: int, eps: float):
+    """Alg. 2 on candidates in priority order: (outcome, budget, per-candidate
+    tokens, predicted latency of the full batch); budget and tokens are None
+    unless the outcome is CONSTRUCT_BATCH."""
+    dctx = (ctypes.c_int32 * max(1, len(decode_ctx)))(*[int(v) for v in decode_ctx])
+    arr = _candidates(cands)
+    outcome, budget, tf = ctypes.c_int32(), ctypes.c_int32(-1), ctypes.c_double()
+    take = (ctypes.c_int32 * max(1, len(cands)))()
+    _check(LIB.ssa_batch_constructor(ctypes.byref(pred.p), dctx, len(decode_ctx), arr, len(cands),
+                                     int(max_budget), float(eps), ctypes.byref(outcome),
+                                     ctypes.byref(budget), take, ctypes.byref(tf)),
+           "ssa_batch_constructor")
+    if outcome.value != CONSTRUCT_BATCH:
+        return outcome.value, None, None, tf.value
+    return outcome.value, budget.value, list(take)[:len(cands)], tf.value
 
 
 def sliding_chunker(pred: Predictor, decode_ctx, prefill, max_budget: int, t_cur: float,
