@@ -1,0 +1,52 @@
+/*
+ * ssa_layer.h -- the GPU steps around attention in one transformer layer of a
+ * serving iteration (Llama-3-8B: RMSNorm, QKV projection, rotary position
+ * embedding, attention over the paged cache, O projection, RMSNorm, SwiGLU
+ * MLP).  They measure what the linear layers add to an iteration's latency,
+ * the cost the paper's features x6 and x7 stand for (Tab. 1).
+ *
+ * Same conventions as ssa.h: 0 or a negative SSA_ERR_* code, validation before
+ * any HIP call, nothing written on an error, no allocation; bf16 as uint16_t
+ * bit patterns; arithmetic in fp32 with round-to-nearest-even to bf16.
+ */
+#ifndef SSA_LAYER_H
+#define SSA_LAYER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "ssa.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * Rotary position embedding of the new tokens' queries and keys, and kv_append
+ * of the rotated keys and the values, in one launch (one workgroup per append
+ * segment of the plan).
+ *   qkv      [T, (Hq + 2 Hkv) D] bf16: the QKV projection of the T new tokens,
+ *            per row the Hq query heads, then the Hkv key heads, then the Hkv
+ *            value heads, D each (rows in plan order, as q in ssa.h)
+ *   cos_sin  [max_position, D] fp32: row p holds cos(p t_i) in columns i < D/2
+ *            and sin(p t_i) in columns D/2 + i, t_i = base^(-2i/D)
+ *   q_out    [T, Hq, D] bf16: the rotated queries (the q of ssa_mixed_attention)
+ *   k_cache, v_cache, block_table: as ssa_kv_append; the rotated key and the
+ *            value of the token at position u_i + j go to that position's slot
+ * Rotation (the "rotate half" pairing): for dims i < D/2 of a head,
+ *   out[i] = x[i] cos - x[i + D/2] sin,  out[i + D/2] = x[i + D/2] cos + x[i] sin,
+ * with (cos, sin) the row of the token's position.  Values are copied bit for
+ * bit.  Every pool byte outside the new slots is left as it is.
+ * Errors: those of ssa_kv_append; SSA_ERR_NULL (qkv, cos_sin, q_out);
+ * SSA_ERR_ARG (a new token's position u_i + j >= max_position).
+ */
+int ssa_rope_append(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                    const uint16_t* qkv, const float* cos_sin, int32_t max_position,
+                    uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
+                    const int32_t* block_table, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSA_LAYER_H */

@@ -1,0 +1,163 @@
+// HIP kernels for gfx950 of the layer steps around attention (include/ssa_layer.h).
+//
+// ssa_rope_append: one workgroup per append segment of the plan (consecutive
+// new tokens of one request inside one page, at most 16).  It rotates the
+// segment's query and key heads (rotate-half pairs (i, i + D/2), cos/sin from
+// the position's row of the table) and writes the queries to q_out and the
+// keys to their slots of the key page (slot-major rows); the value rows are
+// staged in LDS and written to the dim-major value page as 16-byte half rows
+// (8 slots of one dim), the layout ssa_mixed_attention reads.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/ssa_layer.h"
+#include "ssa_plan_format.h"
+
+namespace ssa {
+int check_plan(const ssa_shape* s, const void* plan_host, const PlanHeader** out);
+}
+
+namespace {
+using namespace ssa;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kLayerThreads = 256;
+
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+// two fp32 to packed bf16, round to nearest even
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+// Rotate 8 pairs: x1 = dims i..i+7, x2 = dims i+D/2..i+D/2+7 of one head.
+__device__ __forceinline__ void rotate8(u32x4 x1, u32x4 x2, const float* cs, int half, int i,
+                                        u32x4* o1, u32x4* o2) {
+  const f32x4 c0 = *reinterpret_cast<const f32x4*>(cs + i);
+  const f32x4 c1 = *reinterpret_cast<const f32x4*>(cs + i + 4);
+  const f32x4 s0 = *reinterpret_cast<const f32x4*>(cs + half + i);
+  const f32x4 s1 = *reinterpret_cast<const f32x4*>(cs + half + i + 4);
+  const float c[8] = {c0[0], c0[1], c0[2], c0[3], c1[0], c1[1], c1[2], c1[3]};
+  const float s[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float a0 = bf16_lo(x1[w]), a1 = bf16_hi(x1[w]);
+    const float b0 = bf16_lo(x2[w]), b1 = bf16_hi(x2[w]);
+    const int k = 2 * w;
+    (*o1)[w] = pack2(a0 * c[k] - b0 * s[k], a1 * c[k + 1] - b1 * s[k + 1]);
+    (*o2)[w] = pack2(b0 * c[k] + a0 * s[k], b1 * c[k + 1] + a1 * s[k + 1]);
+  }
+}
+
+struct RopeArgs {
+  const uint8_t* plan;
+  uint64_t hash;
+  int32_t off_segments;
+  const uint16_t* qkv;
+  const float* cos_sin;
+  uint16_t* q_out;
+  uint16_t* kc;
+  uint16_t* vc;
+  const int32_t* bt;
+  int hq, hkv, maxp;
+};
+
+template <int D>
+__global__ __launch_bounds__(kLayerThreads) void rope_append_kernel(RopeArgs a) {
+  constexpr int HALF = D / 2, UPH = HALF / 8;  // 8-pair units per head
+  constexpr int HG = 8;                        // value heads staged per pass
+  __shared__ __attribute__((aligned(16))) uint16_t vt[HG * 16 * D];  // [head][row][D]
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
+  const AppendSeg sg = reinterpret_cast<const AppendSeg*>(a.plan + a.off_segments)[blockIdx.x];
+  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
+  const int n = sg.n, slot0 = sg.pos0 % 16;
+  const size_t stride = (size_t)(a.hq + 2 * a.hkv) * D;
+  const size_t pb = (size_t)a.bt[(size_t)sg.req * a.maxp + sg.pos0 / 16] * a.hkv * 16 * D;
+  // query and key heads: units (row, head, 8 pairs)
+  const int nrot = n * (a.hq + a.hkv) * UPH;
+  for (int idx = threadIdx.x; idx < nrot; idx += kLayerThreads) {
+    const int r = idx / ((a.hq + a.hkv) * UPH);
+    const int rem = idx % ((a.hq + a.hkv) * UPH);
+    const int h = rem / UPH, i = (rem % UPH) * 8;
+    const uint16_t* src = a.qkv + (size_t)(sg.row0 + r) * stride + (size_t)h * D;
+    u32x4 o1, o2;
+    rotate8(ld16(src + i), ld16(src + HALF + i), a.cos_sin + (size_t)(sg.pos0 + r) * D, HALF, i,
+            &o1, &o2);
+    uint16_t* dst = h < a.hq ? a.q_out + ((size_t)(sg.row0 + r) * a.hq + h) * D
+                             : a.kc + pb + (size_t)(h - a.hq) * 16 * D + (size_t)(slot0 + r) * D;
+    st16(dst + i, o1);
+    st16(dst + HALF + i, o2);
+  }
+  // value heads, HG at a time: rows to LDS, then 8-slot half rows of one dim
+  for (int h0 = 0; h0 < a.hkv; h0 += HG) {
+    const int nh = min(HG, a.hkv - h0);
+    const int nv = n * nh * (D / 8);
+    for (int idx = threadIdx.x; idx < nv; idx += kLayerThreads) {
+      const int r = idx / (nh * (D / 8)), rem = idx % (nh * (D / 8));
+      const int hl = rem / (D / 8), c = rem % (D / 8);
+      const uint16_t* src =
+          a.qkv + (size_t)(sg.row0 + r) * stride + (size_t)(a.hq + a.hkv + h0 + hl) * D + c * 8;
+      st16(vt + ((size_t)hl * 16 + r) * D + c * 8, ld16(src));
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < nh * 2 * D; idx += kLayerThreads) {
+      const int hl = idx / (2 * D), d = (idx >> 1) % D, half = idx & 1;
+      const int lo = max(half * 8, slot0), hi = min(half * 8 + 8, slot0 + n);
+      if (lo >= hi) continue;
+      const uint16_t* col = vt + (size_t)hl * 16 * D + d;  // slot s at col[(s - slot0) * D]
+      uint16_t* dst = a.vc + pb + (size_t)(h0 + hl) * 16 * D + (size_t)d * 16;
+      if (lo == half * 8 && hi == half * 8 + 8) {
+        uint32_t w[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int s0 = half * 8 + 2 * k - slot0;
+          w[k] = (uint32_t)col[s0 * D] | ((uint32_t)col[(s0 + 1) * D] << 16);
+        }
+        st16(dst + half * 8, u32x4{w[0], w[1], w[2], w[3]});
+      } else {
+        for (int s = lo; s < hi; ++s) dst[s] = col[(s - slot0) * D];
+      }
+    }
+    __syncthreads();  // the next pass reuses the staging rows
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssa_rope_append(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                    const uint16_t* qkv, const float* cos_sin, int32_t max_position,
+                    uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
+                    const int32_t* block_table, void* stream) {
+  const PlanHeader* h = nullptr;
+  int rc = check_plan(shape, plan_host, &h);
+  if (rc) return rc;
+  if (!plan_dev) return SSA_ERR_NULL;
+  const ReqEntry* reqs = reinterpret_cast<const ReqEntry*>(
+      static_cast<const uint8_t*>(plan_host) + h->off_reqs);
+  for (int32_t i = 0; i < h->num_reqs; ++i)
+    if (reqs[i].q_len > 0 && (int64_t)reqs[i].ctx_len + reqs[i].q_len > max_position)
+      return SSA_ERR_ARG;
+  if (h->num_segments == 0) return SSA_OK;
+  if (!qkv || !cos_sin || !q_out || !k_cache || !v_cache || !block_table) return SSA_ERR_NULL;
+  (void)hipGetLastError();
+  RopeArgs a{static_cast<const uint8_t*>(plan_dev), h->hash, h->off_segments, qkv, cos_sin,
+             q_out, k_cache, v_cache, block_table, h->hq, h->hkv, h->max_pages_per_req};
+  if (h->head_dim == 128)
+    hipLaunchKernelGGL(rope_append_kernel<128>, dim3(h->num_segments), dim3(kLayerThreads), 0,
+                       static_cast<hipStream_t>(stream), a);
+  else
+    hipLaunchKernelGGL(rope_append_kernel<64>, dim3(h->num_segments), dim3(kLayerThreads), 0,
+                       static_cast<hipStream_t>(stream), a);
+  return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+}
+
+}  // extern "C"

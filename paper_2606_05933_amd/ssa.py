@@ -148,6 +148,8 @@ def _load():
                                        ctypes.c_double, ip]
     lib.ssa_sliding_chunker.argtypes = [P(SsaPredictor), ip, i32, P(SsaPrefillRequest), i32, i32,
                                         ctypes.c_double, ctypes.c_double, ip, ip, dp]
+    lib.ssa_rope_append.argtypes = [P(SsaShape), vp, vp, vp, vp, i32, vp, vp, vp, vp, vp]
+    lib.ssa_rope_append.restype = ctypes.c_int
     lib.ssa_priority_sort.argtypes = [P(SsaCandidate), i32, ctypes.c_double, ctypes.c_double,
                                       ctypes.c_double, ip]
     lib.ssa_batch_constructor.argtypes = [P(SsaPredictor), ip, i32, P(SsaCandidate), i32, i32,
@@ -165,7 +167,8 @@ EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
             "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed",
             "ssa_append_attention", "ssa_predictor_init", "ssa_predictor_add",
             "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
-            "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor")
+            "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor",
+            "ssa_rope_append")
 
 
 def _check(rc: int, what: str):
@@ -486,6 +489,39 @@ def bind_mixed_attention(shape: SsaShape, plan_host, plan_dev, q, k_cache, v_cac
             vp(_ptr(k_cache)), vp(_ptr(v_cache)), vp(_ptr(block_table)), vp(_ptr(out)),
             vp(_ptr(workspace)), ctypes.c_size_t(ws_bytes), vp(_stream(stream)))
     return BoundCall(LIB.ssa_mixed_attention_timed, "ssa_mixed_attention", args, timed=True)
+
+
+def rope_cos_sin(max_position: int, d: int, base: float = 500000.0) -> np.ndarray:
+    """[max_position, d] fp32 table of ssa_rope_append: cos(p t_i) in columns
+    i < d/2, sin(p t_i) in columns d/2 + i, t_i = base^(-2i/d) (angles in fp64)."""
+    i = np.arange(d // 2, dtype=np.float64)
+    inv = base ** (-2.0 * i / d)
+    ang = np.arange(max_position, dtype=np.float64)[:, None] * inv[None, :]
+    return np.concatenate([np.cos(ang), np.sin(ang)], axis=1).astype(np.float32)
+
+
+def rope_append(shape: SsaShape, plan_host, plan_dev, qkv, cos_sin, q_out, k_cache, v_cache,
+                block_table, stream=None):
+    """ssa_rope_append: RoPE of the new queries and keys, and kv_append of the
+    rotated keys and the values, in one launch."""
+    h = _plan_header(plan_host)
+    T, n = h["num_tokens"], h["num_reqs"]
+    d, hq, hkv = shape.head_dim, shape.num_q_heads, shape.num_kv_heads
+    pool = shape.num_pages * hkv * shape.page_size * d
+    _check_dev("qkv", qkv, T * (hq + 2 * hkv) * d, 2)
+    _check_dev("q_out", q_out, T * hq * d, 2)
+    _check_dev("cos_sin", cos_sin, d, 4)
+    _check_dev("k_cache", k_cache, pool, 2)
+    _check_dev("v_cache", v_cache, pool, 2)
+    _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+    max_pos = cos_sin.numel() // d
+    vp = ctypes.c_void_p
+    rc = LIB.ssa_rope_append(ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)),
+                             vp(_ptr(qkv)), vp(_ptr(cos_sin)), int(max_pos), vp(_ptr(q_out)),
+                             vp(_ptr(k_cache)), vp(_ptr(v_cache)), vp(_ptr(block_table)),
+                             vp(_stream(stream)))
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_rope_append")
 
 
 def bind_append_attention(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,

@@ -1,0 +1,69 @@
+"""Pins of the layer oracle (``oracle/layer.py``) against closed forms, and of the
+library's rotary table against the oracle's angles.  No GPU.
+
+RoPE: position 0 is the identity; every (i, i + D/2) pair keeps its norm;
+rotations compose (rope(rope(x, a), b) = rope(x, a + b)); q . k of rotated heads
+depends on the positions only through their difference; a D = 4 case by hand.
+RMSNorm and SwiGLU: closed forms.
+"""
+import numpy as np
+import pytest
+
+from oracle import layer as orc
+from paper_2606_05933_amd import ssa
+
+
+def test_positions_by_hand():
+    assert list(orc.positions([3, 1, 0, 2], [5, 9, 4, 0])) == [5, 6, 7, 9, 0, 1]
+
+
+def test_rope_position_zero_is_the_identity():
+    x = np.random.default_rng(0).normal(size=(3, 4, 128))
+    assert np.array_equal(orc.rope(x, [0, 0, 0]), x)
+
+
+def test_rope_keeps_pair_norms_and_composes():
+    rng = np.random.default_rng(1)
+    x = rng.normal(size=(5, 2, 64))
+    a, b = rng.integers(0, 40000, size=5), rng.integers(0, 40000, size=5)
+    y = orc.rope(x, a)
+    pair = lambda z: z[..., :32] ** 2 + z[..., 32:] ** 2
+    assert np.allclose(pair(y), pair(x), rtol=1e-12)
+    assert np.allclose(orc.rope(y, b), orc.rope(x, a + b), atol=1e-9)
+
+
+def test_rope_scores_depend_on_the_position_difference():
+    rng = np.random.default_rng(2)
+    q, k = rng.normal(size=(1, 1, 128)), rng.normal(size=(1, 1, 128))
+    for m, n in ((10, 3), (5000, 4993), (123, 116)):
+        s = np.sum(orc.rope(q, [m]) * orc.rope(k, [n]))
+        assert s == pytest.approx(np.sum(orc.rope(q, [m - n]) * k), rel=1e-9)
+
+
+def test_rope_worked_by_hand():
+    # D = 4: pairs (0, 2) at angle p and (1, 3) at angle p * base^(-1/2)
+    base, p = 10000.0, 3
+    x = np.array([[[1.0, 2.0, 3.0, 4.0]]])
+    a0, a1 = p * 1.0, p * base ** -0.5
+    want = [1 * np.cos(a0) - 3 * np.sin(a0), 2 * np.cos(a1) - 4 * np.sin(a1),
+            3 * np.cos(a0) + 1 * np.sin(a0), 4 * np.cos(a1) + 2 * np.sin(a1)]
+    assert np.allclose(orc.rope(x, [p], base)[0, 0], want, rtol=1e-15)
+
+
+def test_library_rope_table_matches_the_oracle_angles():
+    tab = ssa.rope_cos_sin(40000, 128)
+    x = np.zeros((1, 1, 128))
+    x[0, 0, :64] = 1.0  # (1, 0) pairs: the rotation's (cos, sin)
+    for p in (0, 1, 777, 39999):
+        r = orc.rope(x, [p])[0, 0]
+        assert np.allclose(tab[p, :64], r[:64], atol=6e-8, rtol=0)
+        assert np.allclose(tab[p, 64:], r[64:], atol=6e-8, rtol=0)
+
+
+def test_rms_norm_and_silu_closed_forms():
+    w = np.linspace(0.5, 2.0, 8)
+    assert np.allclose(orc.rms_norm(np.full(8, 3.0), w, eps=0.0), w, rtol=1e-15)
+    assert np.allclose(orc.rms_norm(np.full(8, -2.0), w, eps=0.0), -w, rtol=1e-15)
+    assert orc.silu_mul(0.0, 5.0) == 0.0
+    assert orc.silu_mul(1.0, 2.0) == pytest.approx(2.0 / (1.0 + np.exp(-1.0)), rel=1e-15)
+    assert orc.silu_mul(-50.0, 1.0) == pytest.approx(-50.0 * np.exp(-50.0), rel=1e-9)
