@@ -45,6 +45,46 @@ int ssa_rope_append(const ssa_shape* shape, const void* plan_host, const void* p
                     uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
                     const int32_t* block_table, void* stream);
 
+/* Epilogues of ssa_linear. */
+enum {
+  SSA_EPILOGUE_NONE = 0,     /* out = x W^T                                   [M, N] */
+  SSA_EPILOGUE_RESIDUAL = 1, /* out = x W^T + residual                        [M, N] */
+  SSA_EPILOGUE_SWIGLU = 2    /* out = silu(x Wg^T) * (x Wu^T)                 [M, N/2] */
+};
+
+/*
+ * A linear layer on the matrix cores: out = x W^T with fp32 accumulation and
+ * one bf16 rounding of the result (after the epilogue's fp32 arithmetic).
+ *   x    [M, K] bf16, row-major;  W [N, K] bf16, row-major (torch Linear layout)
+ *   out  [M, N] bf16 ([M, N/2] for SWIGLU); residual [M, N] bf16 (RESIDUAL only;
+ *        it may be the same buffer as out)
+ *   SWIGLU: W holds the gate and up projections interleaved in blocks of 16 rows
+ *        (rows 32b .. 32b+15 = gate rows 16b .. 16b+15, rows 32b+16 .. 32b+31 =
+ *        up rows 16b .. 16b+15); silu(z) = z / (1 + e^-z).
+ *   workspace: ssa_linear_workspace_size bytes (0 when one pass over K fills the
+ *        chip).  Its first words are split tickets: zero before the first call
+ *        (a zeroed allocation), and zero again after every call.  Calls that
+ *        share a workspace must be ordered on one stream.
+ * Requires N % 128 == 0 and K % 64 == 0; M >= 0 (M == 0 does nothing).
+ * Results do not depend on the launch order of workgroups: split partials are
+ * added in split order.
+ * Errors: SSA_ERR_ARG (sizes, epilogue), SSA_ERR_NULL, SSA_ERR_WORKSPACE,
+ * SSA_ERR_HIP.
+ */
+int ssa_linear_workspace_size(int32_t m, int32_t n, int32_t k, size_t* ws_bytes);
+int ssa_linear(int32_t m, int32_t n, int32_t k, int32_t epilogue, const uint16_t* x,
+               const uint16_t* w, const uint16_t* residual, uint16_t* out, void* workspace,
+               size_t ws_bytes, void* stream);
+
+/*
+ * RMSNorm of each row: out = x / sqrt(mean(x^2) + eps) * weight, in fp32, one
+ * bf16 rounding.  x, out [M, N] bf16 (distinct buffers); weight [N] bf16.
+ * Requires N % 8 == 0, N <= 8192, eps >= 0.
+ * Errors: SSA_ERR_ARG, SSA_ERR_NULL, SSA_ERR_HIP.
+ */
+int ssa_rms_norm(int32_t m, int32_t n, const uint16_t* x, const uint16_t* weight, float eps,
+                 uint16_t* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

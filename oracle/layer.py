@@ -9,6 +9,7 @@ numpy in float64; it imports nothing from the library package.
   i < D/2 of a head, with angle a = p * base^(-2i/D),
       out[i] = x[i] cos a - x[i + D/2] sin a,  out[i + D/2] = x[i + D/2] cos a + x[i] sin a.
   Angles and products in float64.
+* A linear layer: x W^T for W stored [out features, in features].
 * RMSNorm: x / sqrt(mean(x^2) + eps) * weight.
 * SwiGLU: silu(gate) * up with silu(z) = z / (1 + exp(-z)).
 """
@@ -34,6 +35,11 @@ def rope(x, pos, base: float = 500000.0) -> np.ndarray:
     s = np.sin(ang)[:, None, :]
     x1, x2 = x[..., :half], x[..., half:]
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def linear(x, w) -> np.ndarray:
+    """x [M, K], w [N, K]: x w^T in float64."""
+    return np.asarray(x, dtype=np.float64) @ np.asarray(w, dtype=np.float64).T
 
 
 def rms_norm(x, weight, eps: float = 1e-5) -> np.ndarray:

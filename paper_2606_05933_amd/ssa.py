@@ -21,6 +21,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libssa.so")
 
 SSA_OK = 0
+SSA_ERR_NULL, SSA_ERR_WORKSPACE, SSA_ERR_HIP, SSA_ERR_ARG = -1, -8, -10, -13
 SCENES = {0: "empty", 1: "pure decode", 2: "pure prefill", 3: "mixed"}
 
 
@@ -150,6 +151,9 @@ def _load():
                                         ctypes.c_double, ctypes.c_double, ip, ip, dp]
     lib.ssa_rope_append.argtypes = [P(SsaShape), vp, vp, vp, vp, i32, vp, vp, vp, vp, vp]
     lib.ssa_rope_append.restype = ctypes.c_int
+    lib.ssa_linear_workspace_size.argtypes = [i32, i32, i32, P(sz)]
+    lib.ssa_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
+    lib.ssa_rms_norm.argtypes = [i32, i32, vp, vp, ctypes.c_float, vp, vp]
     lib.ssa_priority_sort.argtypes = [P(SsaCandidate), i32, ctypes.c_double, ctypes.c_double,
                                       ctypes.c_double, ip]
     lib.ssa_batch_constructor.argtypes = [P(SsaPredictor), ip, i32, P(SsaCandidate), i32, i32,
@@ -168,7 +172,9 @@ EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
             "ssa_append_attention", "ssa_predictor_init", "ssa_predictor_add",
             "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
             "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor",
-            "ssa_rope_append")
+            "ssa_rope_append", "ssa_linear_workspace_size", "ssa_linear", "ssa_rms_norm")
+
+EPILOGUE_NONE, EPILOGUE_RESIDUAL, EPILOGUE_SWIGLU = 0, 1, 2
 
 
 def _check(rc: int, what: str):
@@ -522,6 +528,63 @@ def rope_append(shape: SsaShape, plan_host, plan_dev, qkv, cos_sin, q_out, k_cac
                              vp(_stream(stream)))
     if rc != SSA_OK:
         raise SsaError(rc, "ssa_rope_append")
+
+
+def linear_workspace_size(m: int, n: int, k: int) -> int:
+    """Bytes of the workspace ssa_linear needs for an [m, k] x [n, k]^T product."""
+    ws = ctypes.c_size_t(0)
+    _check(LIB.ssa_linear_workspace_size(int(m), int(n), int(k), ctypes.byref(ws)),
+           "ssa_linear_workspace_size")
+    return int(ws.value)
+
+
+def linear(x, w, out, epilogue: int = EPILOGUE_NONE, residual=None, workspace=None, stream=None):
+    """ssa_linear: out = x w^T (+ residual, or the SwiGLU of interleaved gate/up
+    rows), x [m, k], w [n, k], bf16 device tensors."""
+    m, k = x.shape[0], x.shape[-1]
+    n = w.shape[0]
+    _check_dev("x", x, m * k, 2)
+    _check_dev("w", w, n * k, 2)
+    _check_dev("out", out, m * (n // 2 if epilogue == EPILOGUE_SWIGLU else n), 2)
+    if epilogue == EPILOGUE_RESIDUAL:
+        _check_dev("residual", residual, m * n, 2)
+    if w.numel() != n * k or x.numel() != m * k:
+        raise ValueError("x and w must be [m, k] and [n, k]")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    vp = ctypes.c_void_p
+    rc = LIB.ssa_linear(int(m), int(n), int(k), int(epilogue), vp(_ptr(x)), vp(_ptr(w)),
+                        vp(_ptr(residual)), vp(_ptr(out)), vp(_ptr(workspace)),
+                        ctypes.c_size_t(ws_bytes), vp(_stream(stream)))
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_linear")
+
+
+def rms_norm(x, weight, out, eps: float = 1e-5, stream=None):
+    """ssa_rms_norm of each row of x [m, n] (bf16 device tensors)."""
+    m, n = x.shape[0], x.shape[-1]
+    _check_dev("x", x, m * n, 2)
+    _check_dev("weight", weight, n, 2)
+    _check_dev("out", out, m * n, 2)
+    vp = ctypes.c_void_p
+    rc = LIB.ssa_rms_norm(int(m), int(n), vp(_ptr(x)), vp(_ptr(weight)), ctypes.c_float(eps),
+                          vp(_ptr(out)), vp(_stream(stream)))
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_rms_norm")
+
+
+def interleave_gate_up(w_gate, w_up):
+    """The [2I, K] weight of ssa_linear's SwiGLU epilogue from the gate and up
+    weights [I, K] (I % 64 == 0): blocks of 16 gate rows and 16 up rows
+    alternate.  A one-time layout change of the weights (numpy or torch)."""
+    i, k = w_gate.shape
+    if w_up.shape != (i, k) or i % 16:
+        raise ValueError("gate and up weights must both be [I, K] with I % 16 == 0")
+    if isinstance(w_gate, np.ndarray):
+        return np.stack([w_gate.reshape(i // 16, 16, k), w_up.reshape(i // 16, 16, k)],
+                        axis=1).reshape(2 * i, k)
+    import torch
+    return torch.stack([w_gate.reshape(i // 16, 16, k), w_up.reshape(i // 16, 16, k)],
+                       dim=1).reshape(2 * i, k).contiguous()
 
 
 def bind_append_attention(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,

@@ -116,9 +116,9 @@ class Batch:
 _SLAB = 1 << 22
 
 
-def _normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
-    """bf16 bits of fp32 N(0,1) draws.  Slab k of 2^22 values comes from its own
-    PCG64 stream (spawned from ``rng``), so the result does not depend on how
+def _normal_bf16(rng: np.random.Generator, shape, std: float = 1.0) -> np.ndarray:
+    """bf16 bits of fp32 N(0, std^2) draws.  Slab k of 2^22 values comes from its
+    own PCG64 stream (spawned from ``rng``), so the result does not depend on how
     many threads fill the slabs."""
     n = int(np.prod(shape))
     out = np.empty(n, dtype=np.uint16)
@@ -128,7 +128,10 @@ def _normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
     def fill(k):
         s, e = k * _SLAB, min(n, (k + 1) * _SLAB)
         g = np.random.Generator(np.random.PCG64(seeds[k]))
-        out[s:e] = f32_to_bf16_bits(g.standard_normal(e - s, dtype=np.float32))
+        z = g.standard_normal(e - s, dtype=np.float32)
+        if std != 1.0:
+            z *= np.float32(std)
+        out[s:e] = f32_to_bf16_bits(z)
 
     if nslab > 1:
         workers = max(1, min(16, len(os.sched_getaffinity(0))))
@@ -137,6 +140,12 @@ def _normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
     elif nslab == 1:
         fill(0)
     return out.reshape(shape)
+
+
+def normal_bf16(shape, seed: int, std: float = 1.0) -> np.ndarray:
+    """bf16 bits of seeded N(0, std^2) draws (activations, weights of the layer
+    around attention)."""
+    return _normal_bf16(np.random.default_rng(seed), tuple(shape), std)
 
 
 def make_batch(shape: Shape, q_len, ctx_len, seed: int = 0, spare_pages: int = 64,

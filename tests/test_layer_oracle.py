@@ -4,7 +4,7 @@ library's rotary table against the oracle's angles.  No GPU.
 RoPE: position 0 is the identity; every (i, i + D/2) pair keeps its norm;
 rotations compose (rope(rope(x, a), b) = rope(x, a + b)); q . k of rotated heads
 depends on the positions only through their difference; a D = 4 case by hand.
-RMSNorm and SwiGLU: closed forms.
+RMSNorm and SwiGLU: closed forms.  The linear layer: sums written out by loops.
 """
 import numpy as np
 import pytest
@@ -67,3 +67,22 @@ def test_rms_norm_and_silu_closed_forms():
     assert orc.silu_mul(0.0, 5.0) == 0.0
     assert orc.silu_mul(1.0, 2.0) == pytest.approx(2.0 / (1.0 + np.exp(-1.0)), rel=1e-15)
     assert orc.silu_mul(-50.0, 1.0) == pytest.approx(-50.0 * np.exp(-50.0), rel=1e-9)
+
+
+def test_linear_by_loops():
+    rng = np.random.default_rng(3)
+    x, w = rng.normal(size=(3, 5)), rng.normal(size=(4, 5))
+    want = np.array([[sum(x[i, k] * w[j, k] for k in range(5)) for j in range(4)]
+                     for i in range(3)])
+    assert np.allclose(orc.linear(x, w), want, rtol=1e-13, atol=1e-13)
+    assert orc.linear(x, w).shape == (3, 4)  # not the transposed product
+
+
+def test_library_gate_up_interleave_is_a_row_permutation():
+    i, k = 64, 3
+    g = np.arange(i * k).reshape(i, k)
+    u = -np.arange(i * k).reshape(i, k) - 1
+    wgu = ssa.interleave_gate_up(g, u)
+    for b in range(i // 16):
+        assert np.array_equal(wgu[32 * b:32 * b + 16], g[16 * b:16 * b + 16])
+        assert np.array_equal(wgu[32 * b + 16:32 * b + 32], u[16 * b:16 * b + 16])
