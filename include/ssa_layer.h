@@ -85,6 +85,60 @@ int ssa_linear(int32_t m, int32_t n, int32_t k, int32_t epilogue, const uint16_t
 int ssa_rms_norm(int32_t m, int32_t n, const uint16_t* x, const uint16_t* weight, float eps,
                  uint16_t* out, void* stream);
 
+/*
+ * The weights of one Llama-style decoder layer (device pointers, bf16 unless
+ * noted; the library keeps none of them).
+ *   attn_norm, mlp_norm [hidden]          RMSNorm weights
+ *   w_qkv     [(Hq + 2 Hkv) D, hidden]    query, key and value projections stacked
+ *   w_o       [hidden, Hq D]              output projection
+ *   w_gate_up [2 inter, hidden]           gate and up projections, interleaved in
+ *                                         blocks of 16 rows (ssa_linear SWIGLU)
+ *   w_down    [hidden, inter]             down projection
+ *   cos_sin   [max_position, D] fp32      the rotary table of ssa_rope_append
+ *   eps                                   the RMSNorm epsilon
+ */
+typedef struct ssa_layer_weights {
+  const uint16_t* attn_norm;
+  const uint16_t* w_qkv;
+  const uint16_t* w_o;
+  const uint16_t* mlp_norm;
+  const uint16_t* w_gate_up;
+  const uint16_t* w_down;
+  const float* cos_sin;
+  int32_t hidden, inter, max_position;
+  float eps;
+} ssa_layer_weights;
+
+/*
+ * Workspace bytes of ssa_layer_forward for this plan: the activations of the
+ * plan's T tokens, the attention workspace of the plan, the linear layers'
+ * split workspace.  The workspace must be zero before its first use (a zeroed
+ * allocation); the counters in it are zero again after every call.
+ */
+int ssa_layer_workspace_size(const ssa_shape* shape, const void* plan_host,
+                             const ssa_layer_weights* w, size_t* ws_bytes);
+
+/*
+ * One decoder layer over the T new tokens of a serving iteration (the batch
+ * B = {(c_i, u_i)} of Sec. 3.2, Llama-3-8B's block, eight launches on `stream`):
+ *   xn  = RMSNorm(x, attn_norm)
+ *   qkv = xn w_qkv^T;  RoPE + kv_append (ssa_rope_append) -> q, the caches
+ *   a   = ssa_mixed_attention(q, caches)
+ *   h   = x + a w_o^T
+ *   out = h + (silu(hn w_gate^T) * (hn w_up^T)) w_down^T,  hn = RMSNorm(h, mlp_norm)
+ *   x, out [T, hidden] bf16, rows in plan order; out may be the same buffer as x.
+ *   k_cache, v_cache, block_table: as ssa_kv_append (the new tokens' rotated
+ *   keys and values are appended).
+ * Requires hidden % 128 == 0, hidden <= 8192, inter % 64 == 0,
+ * (Hq + 2 Hkv) D % 128 == 0.  Everything is validated before the first launch.
+ * Errors: those of the steps (SSA_ERR_ARG for sizes and positions past the
+ * rotary table), SSA_ERR_WORKSPACE, SSA_ERR_NULL, SSA_ERR_HIP.
+ */
+int ssa_layer_forward(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                      const ssa_layer_weights* w, const uint16_t* x, uint16_t* out,
+                      uint16_t* k_cache, uint16_t* v_cache, const int32_t* block_table,
+                      void* workspace, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

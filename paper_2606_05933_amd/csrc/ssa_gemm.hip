@@ -37,11 +37,8 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kThreads = 256;
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int kStageBytes = (BM + BN) * BK * 2;       // 32 KB: x rows, then W rows
-constexpr int kLoads = kStageBytes / 1024 / 4;        // 1 KB copies per wave per stage
-constexpr int kTileFloats = BM * BN;
+constexpr int kNormThreads = 256;
+constexpr int BK = 64;  // K block: one 128-byte LDS row per operand row
 constexpr int kXcds = 8;
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -72,7 +69,8 @@ __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // Split partials cross workgroups and XCDs (whose L2s are not coherent with
-// each other): device-scope 8-byte stores and loads, a device-scope ticket.
+// each other): device-scope 8-byte stores, device-coherent loads (below), a
+// device-scope ticket.
 __device__ __forceinline__ void st16_dev(float* p, f32x4 v) {
   uint64_t* q = reinterpret_cast<uint64_t*>(p);
   const uint64_t lo = (uint64_t)__float_as_uint(v[0]) | ((uint64_t)__float_as_uint(v[1]) << 32);
@@ -80,13 +78,23 @@ __device__ __forceinline__ void st16_dev(float* p, f32x4 v) {
   __hip_atomic_store(q, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __hip_atomic_store(q + 1, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ f32x4 ld16_dev(const float* p) {
-  uint64_t* q = reinterpret_cast<uint64_t*>(const_cast<float*>(p));
-  const uint64_t lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const uint64_t hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return f32x4{__uint_as_float((uint32_t)lo), __uint_as_float((uint32_t)(lo >> 32)),
-               __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
-}
+// Reads of the partials: 16-byte buffer loads with the device-coherent cache
+// policy (sc1), the instruction of a device-scope load, so they do not hit a
+// stale line of this XCD's L2.  Being plain loads to the compiler, they are
+// issued back to back and waited for where a value is used (device-scope
+// atomic loads would be serialised).  Offsets are bytes from the tile's first
+// partial; a read past num_records would return zeros, never fault.
+constexpr int kCachePolicySc1 = 16;
+struct PartReader {
+  __amdgpu_buffer_rsrc_t rsrc;
+  __device__ explicit PartReader(const float* base)
+      : rsrc(__builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), (short)0, 0x7fffffff,
+                                               0x00020000)) {}
+  __device__ f32x4 operator()(int byte_off) const {
+    return __builtin_bit_cast(
+        f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, byte_off, 0, kCachePolicySc1));
+  }
+};
 
 // silu(z) = z / (1 + e^-z), with e^-z as 2^(-z log2 e)
 __device__ __forceinline__ float silu(float z) {
@@ -104,20 +112,39 @@ struct GemmArgs {
   int tiles_m, tiles_n, splits, kbps, kblocks;
 };
 
-// Wait until at most `left` K blocks (kLoads copies each) of this wave are in flight.
-template <int STAGES>
+// A tile configuration: NWM x NWN waves, each owning TM x TN MFMA tiles of
+// 16 x 16 (TM along tokens, TN along output features); STAGES K blocks in the
+// LDS ring; OCC workgroups per CU the launch bounds ask for.
+template <int NWM_, int NWN_, int TM_, int TN_, int STAGES_, int OCC_>
+struct TileCfg {
+  static constexpr int NWM = NWM_, NWN = NWN_, TM = TM_, TN = TN_, STAGES = STAGES_, OCC = OCC_;
+  static constexpr int kWaves = NWM * NWN, kThreads = kWaves * 64;
+  static constexpr int BM = NWM * TM * 16, BN = NWN * TN * 16;
+  static constexpr int kStage = (BM + BN) * BK * 2;  // x rows, then W rows
+  static constexpr int kPieces = (BM + BN) / 8;      // 1 KB copies (8 rows) per stage
+  static constexpr int kLoads = kPieces / kWaves;    // copies per wave per stage
+  static constexpr int kTileFloats = BM * BN;
+  static_assert(kPieces % kWaves == 0, "copies must split evenly over the waves");
+  static_assert(TN % 2 == 0, "the SwiGLU epilogue pairs n tiles");
+  static_assert((STAGES - 2) * kLoads < 64, "vmcnt range");
+};
+
+// Wait until at most `left` K blocks (LOADS copies each) of this wave are in flight.
+template <int STAGES, int LOADS>
 __device__ __forceinline__ void wait_blocks(int left) {
-  if (STAGES >= 4 && left >= 2) vm_wait<2 * kLoads>();
-  else if (STAGES >= 3 && left >= 1) vm_wait<kLoads>();
+  if (STAGES >= 4 && left >= 2) vm_wait<2 * LOADS>();
+  else if (STAGES >= 3 && left >= 1) vm_wait<LOADS>();
   else vm_wait<0>();
 }
 
-template <int STAGES, int EPI>
-__global__ __launch_bounds__(kThreads, STAGES <= 2 ? 2 : 1) void linear_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) char lds[STAGES * kStageBytes];
+template <class C, int EPI>
+__global__ __launch_bounds__(C::kThreads, C::OCC) void linear_kernel(GemmArgs a) {
+  constexpr int TM = C::TM, TN = C::TN, STAGES = C::STAGES, LOADS = C::kLoads;
+  constexpr int BM = C::BM, BN = C::BN;
+  __shared__ __attribute__((aligned(16))) char lds[STAGES * C::kStage];
   __shared__ int s_last;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w / C::NWN, wn = w % C::NWN;
   const int r16 = lane & 15, g = lane >> 4;
 
   // work id: consecutive ids on one XCD (dispatch goes round-robin over XCDs)
@@ -131,71 +158,74 @@ __global__ __launch_bounds__(kThreads, STAGES <= 2 ? 2 : 1) void linear_kernel(G
   const int kb0 = split * a.kbps;
   const int nkb = min(a.kbps, a.kblocks - kb0);
 
-  // Copy r of this wave fills 1 KB piece p = 4 r + w of a stage: pieces 0..15
-  // hold x rows 8p..8p+7, pieces 16..31 W rows; lane i fetches the chunk that
-  // belongs at its LDS slot (row 8p + i / 8, slot i % 8).
-  const uint16_t* src[kLoads];
+  // Copy r of this wave fills 1 KB piece p = kWaves r + w of a stage: pieces
+  // below BM / 8 hold x rows 8p..8p+7, the rest W rows; lane i fetches the
+  // chunk that belongs at its LDS slot (row 8p + i / 8, slot i % 8).
+  const uint16_t* src[LOADS];
 #pragma unroll
-  for (int r = 0; r < kLoads; ++r) {
-    const int p = r * 4 + w;
-    const int row = (p & 15) * 8 + (lane >> 3);
+  for (int r = 0; r < LOADS; ++r) {
+    const int p = r * C::kWaves + w;
     const int chunk = (lane & 7) ^ (lane >> 3);
-    if (p < 16)
+    if (p < BM / 8) {
+      const int row = p * 8 + (lane >> 3);
       src[r] = a.x + (size_t)min(m0 + row, a.m - 1) * a.k + (size_t)kb0 * BK + chunk * 8;
-    else
+    } else {
+      const int row = (p - BM / 8) * 8 + (lane >> 3);
       src[r] = a.w + (size_t)(n0 + row) * a.k + (size_t)kb0 * BK + chunk * 8;
+    }
   }
   auto issue = [&](int i) {
-    const char* st = lds + (i % STAGES) * kStageBytes;
+    const char* st = lds + (i % STAGES) * C::kStage;
 #pragma unroll
-    for (int r = 0; r < kLoads; ++r) dma16(src[r] + (size_t)i * BK, st + (r * 4 + w) * 1024);
+    for (int r = 0; r < LOADS; ++r)
+      dma16(src[r] + (size_t)i * BK, st + (r * C::kWaves + w) * 1024);
   };
 
   // fragment reads: row r16 of a 16-row tile, logical chunk 4 ks + g
-  const int xoff = (wm * 64 + r16) * 128;
-  const int woff = BM * 128 + (wn * 64 + r16) * 128;
+  const int xoff = (wm * TM * 16 + r16) * 128;
+  const int woff = BM * 128 + (wn * TN * 16 + r16) * 128;
   const int c0 = (g ^ (r16 & 7)) << 4, c1 = ((4 + g) ^ (r16 & 7)) << 4;
 
-  f32x4 acc[4][4];
+  f32x4 acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
   for (int i = 0; i < STAGES - 1; ++i)
     if (i < nkb) issue(i);
   for (int i = 0; i < nkb; ++i) {
-    wait_blocks<STAGES>(min(nkb - 1 - i, STAGES - 2));
+    wait_blocks<STAGES, LOADS>(min(nkb - 1 - i, STAGES - 2));
     __syncthreads();  // block i has landed for every wave; stage (i - 1) % STAGES is free
     if (i + STAGES - 1 < nkb) issue(i + STAGES - 1);
-    const char* st = lds + (i % STAGES) * kStageBytes;
+    const char* st = lds + (i % STAGES) * C::kStage;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       const int c = ks ? c1 : c0;
-      bf16x8 xf[4], wf[4];
+      bf16x8 xf[TM], wf[TN];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        xf[t] = as_bf16x8(ld16(st + xoff + t * 2048 + c));
-        wf[t] = as_bf16x8(ld16(st + woff + t * 2048 + c));
-      }
+      for (int t = 0; t < TM; ++t) xf[t] = as_bf16x8(ld16(st + xoff + t * 2048 + c));
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
+      for (int t = 0; t < TN; ++t) wf[t] = as_bf16x8(ld16(st + woff + t * 2048 + c));
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma(wf[nt], xf[mt], acc[mt][nt]);
+      for (int mt = 0; mt < TM; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < TN; ++nt) acc[mt][nt] = mfma(wf[nt], xf[mt], acc[mt][nt]);
     }
   }
 
   // 16-token tiles of this wave that hold rows < M (wave-uniform)
-  const int nmt = max(0, min(4, (a.m - (m0 + wm * 64) + 15) / 16));
+  const int nmt = max(0, min(TM, (a.m - (m0 + wm * TM * 16) + 15) / 16));
   if (a.splits > 1) {
     const int tile = tn * a.tiles_m + tm;
-    float* mine = a.part + ((size_t)tile * a.splits + split) * kTileFloats + w * 4096 + lane * 4;
+    const size_t wbase = (size_t)w * (TM * TN * 256) + lane * 4;
+    float* mine = a.part + ((size_t)tile * a.splits + split) * C::kTileFloats + wbase;
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+    for (int mt = 0; mt < TM; ++mt)
       if (mt < nmt)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) st16_dev(mine + (mt * 4 + nt) * 256, acc[mt][nt]);
+        for (int nt = 0; nt < TN; ++nt) st16_dev(mine + (mt * TN + nt) * 256, acc[mt][nt]);
     vm_wait<0>();  // this thread's device-scope stores have completed
     __syncthreads();
     if (tid == 0) {
@@ -205,42 +235,61 @@ __global__ __launch_bounds__(kThreads, STAGES <= 2 ? 2 : 1) void linear_kernel(G
     }
     __syncthreads();
     if (!s_last) return;
-    const float* base = a.part + (size_t)tile * a.splits * kTileFloats + w * 4096 + lane * 4;
+    // sum in split order, own split from registers (the same bits it stored);
+    // the partials of four splits are in flight at once
+    const PartReader rd(a.part + (size_t)tile * a.splits * C::kTileFloats);
+    const int wb = (int)wbase * 4;
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
+    for (int mt = 0; mt < TM; ++mt) {
       if (mt >= nmt) continue;
+      f32x4 tot[TN];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int s = 0; s < a.splits; ++s)
-          sum += (s == split) ? acc[mt][nt] : ld16_dev(base + (size_t)s * kTileFloats + (mt * 4 + nt) * 256);
-        acc[mt][nt] = sum;
+      for (int nt = 0; nt < TN; ++nt) tot[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int s0 = 0; s0 < a.splits; s0 += 4) {
+        f32x4 v[4][TN];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int s = s0 + j;
+#pragma unroll
+          for (int nt = 0; nt < TN; ++nt)
+            v[j][nt] = (s < a.splits && s != split)
+                           ? rd((s * C::kTileFloats + (mt * TN + nt) * 256) * 4 + wb)
+                           : acc[mt][nt];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (s0 + j < a.splits)
+#pragma unroll
+            for (int nt = 0; nt < TN; ++nt) tot[nt] += v[j][nt];
       }
+#pragma unroll
+      for (int nt = 0; nt < TN; ++nt) acc[mt][nt] = tot[nt];
     }
     if (tid == 0) __hip_atomic_store(&a.tickets[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
-  // epilogue: lane holds n = nbase + 4 g .. + 3 of token m0 + wm 64 + 16 mt + r16
+  // epilogue: lane holds n = nbase + 4 g .. + 3 of token m0 + wm TM 16 + 16 mt + r16
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) {
+  for (int mt = 0; mt < TM; ++mt) {
     if (mt >= nmt) continue;
-    const int tok = m0 + wm * 64 + mt * 16 + r16;
+    const int tok = m0 + wm * TM * 16 + mt * 16 + r16;
     if (tok >= a.m) continue;
+    const int nbase = n0 + wn * TN * 16;
     if (EPI == SSA_EPILOGUE_SWIGLU) {
       // W rows in 16-row blocks, gate block then up block of the same 16 outputs
       const int nout = a.n / 2;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < TN / 2; ++j) {
         const f32x4 gt = acc[mt][2 * j], up = acc[mt][2 * j + 1];
-        const int col = (n0 + wn * 64) / 2 + j * 16 + g * 4;
+        const int col = nbase / 2 + j * 16 + g * 4;
         u32x2 v = {pack2(silu(gt[0]) * up[0], silu(gt[1]) * up[1]),
                    pack2(silu(gt[2]) * up[2], silu(gt[3]) * up[3])};
         *reinterpret_cast<u32x2*>(a.out + (size_t)tok * nout + col) = v;
       }
     } else {
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int col = n0 + wn * 64 + nt * 16 + g * 4;
+      for (int nt = 0; nt < TN; ++nt) {
+        const int col = nbase + nt * 16 + g * 4;
         f32x4 v = acc[mt][nt];
         if (EPI == SSA_EPILOGUE_RESIDUAL) {
           const u32x2 r = *reinterpret_cast<const u32x2*>(a.res + (size_t)tok * a.n + col);
@@ -258,16 +307,16 @@ __global__ __launch_bounds__(kThreads, STAGES <= 2 ? 2 : 1) void linear_kernel(G
 
 // RMSNorm: one workgroup per row, up to 4 16-byte chunks per thread.
 constexpr int kNormChunks = 4;
-__global__ __launch_bounds__(kThreads) void rms_norm_kernel(const uint16_t* x, const uint16_t* wt,
+__global__ __launch_bounds__(kNormThreads) void rms_norm_kernel(const uint16_t* x, const uint16_t* wt,
                                                             uint16_t* out, int n, float eps) {
-  __shared__ float s_part[kThreads / 64];
+  __shared__ float s_part[kNormThreads / 64];
   const int tid = threadIdx.x;
   const uint16_t* row = x + (size_t)blockIdx.x * n;
   u32x4 v[kNormChunks];
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < kNormChunks; ++c) {
-    const int e = (c * kThreads + tid) * 8;
+    const int e = (c * kNormThreads + tid) * 8;
     v[c] = e < n ? ld16(row + e) : u32x4{0, 0, 0, 0};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -283,7 +332,7 @@ __global__ __launch_bounds__(kThreads) void rms_norm_kernel(const uint16_t* x, c
   const float rs = __builtin_amdgcn_rsqf(tot / (float)n + eps);
 #pragma unroll
   for (int c = 0; c < kNormChunks; ++c) {
-    const int e = (c * kThreads + tid) * 8;
+    const int e = (c * kNormThreads + tid) * 8;
     if (e >= n) continue;
     const u32x4 wv = ld16(wt + e);
     u32x4 o;
@@ -294,32 +343,103 @@ __global__ __launch_bounds__(kThreads) void rms_norm_kernel(const uint16_t* x, c
   }
 }
 
-constexpr int kStages = 3;
-constexpr int kTargetWgs = 512;
+// The tile configurations the host chooses from.
+using CfgMid = TileCfg<2, 2, 4, 4, 3, 1>;    // 128 x 128, 4 waves of 64 x 64
+using CfgMid2 = TileCfg<2, 2, 4, 4, 2, 2>;   // 128 x 128, two workgroups per CU
+using CfgBig = TileCfg<2, 4, 8, 4, 2, 1>;    // 256 x 256, 8 waves of 128 x 64
+using CfgWide = TileCfg<4, 2, 4, 4, 3, 1>;   // 256 x 128, 8 waves of 64 x 64
+using CfgWide4 = TileCfg<2, 2, 8, 4, 3, 1>;  // 256 x 128, 4 waves of 128 x 64
+using CfgSmall = TileCfg<1, 4, 4, 4, 3, 1>;  // 64 x 256: few tokens, weight streaming
+using CfgTiny = TileCfg<1, 4, 2, 4, 4, 1>;   // 32 x 256
+enum { kCfgMid, kCfgMid2, kCfgBig, kCfgWide, kCfgWide4, kCfgSmall, kCfgTiny, kNumCfgs };
 
-struct GemmCfg {
-  int tiles_m, tiles_n, splits, kbps, kblocks;
-  size_t ws;
+struct CfgShape {
+  int bm, bn, occ;
+};
+template <class C>
+constexpr CfgShape shape_of() {
+  return CfgShape{C::BM, C::BN, C::OCC};
+}
+constexpr CfgShape kCfgShapes[kNumCfgs] = {shape_of<CfgMid>(),   shape_of<CfgMid2>(),
+                                           shape_of<CfgBig>(),   shape_of<CfgWide>(),
+                                           shape_of<CfgWide4>(), shape_of<CfgSmall>(),
+                                           shape_of<CfgTiny>()};
+
+struct GemmPlan {
+  int cfg, tiles_m, tiles_n, splits, kbps, kblocks;
+  size_t tickets, ws;
 };
 
-GemmCfg gemm_cfg(int m, int n, int k) {
-  GemmCfg c;
-  c.tiles_m = (m + BM - 1) / BM;
-  c.tiles_n = n / BN;
+// Split K when the tiles alone leave the chip under target_wgs workgroups
+// (at least 4 K blocks per split).
+GemmPlan gemm_plan(int cfg, int m, int n, int k, int target_wgs) {
+  const CfgShape& cs = kCfgShapes[cfg];
+  GemmPlan c;
+  c.cfg = cfg;
+  c.tiles_m = (m + cs.bm - 1) / cs.bm;
+  c.tiles_n = n / cs.bn;
   c.kblocks = k / BK;
   const int tiles = c.tiles_m * c.tiles_n;
   int s = 1;
-  if (tiles < kTargetWgs / 2) s = (kTargetWgs + tiles - 1) / tiles;
-  s = std::max(1, std::min(s, c.kblocks / 4));  // at least 4 K blocks per split
+  if (tiles < target_wgs / 2) s = (target_wgs + tiles - 1) / tiles;
+  s = std::max(1, std::min(s, c.kblocks / 4));
   c.kbps = (c.kblocks + s - 1) / s;
   c.splits = (c.kblocks + c.kbps - 1) / c.kbps;
-  const size_t tickets = ((size_t)tiles * 4 + 255) / 256 * 256;
-  c.ws = c.splits > 1 ? tickets + (size_t)tiles * c.splits * kTileFloats * 4 : 0;
+  c.tickets = ((size_t)tiles * 4 + 255) / 256 * 256;
+  c.ws = c.splits > 1 ? c.tickets + (size_t)tiles * c.splits * cs.bm * cs.bn * 4 : 0;
   return c;
 }
 
+// Measured on MI355X against the Llama-3-8B projections (N x K = 6144 x 4096,
+// 4096 x 4096, 28672 x 4096, 4096 x 14336) for M = 28 .. 4096:
+//  * M <= 64: weight streaming; 32 x 256 tiles, K split to about 128 (long K
+//    and M > 32: 256) workgroups;
+//  * M >= 1024: 256 x 256 tiles when they alone fill the chip;
+//  * otherwise 128 x 128 tiles at two workgroups per CU, K split to about 256
+//    (K > 8192: 512) workgroups.
+GemmPlan choose_plan(int m, int n, int k) {
+  if (n % 256 == 0) {
+    if (m <= 64) return gemm_plan(kCfgTiny, m, n, k, (m > 32 && k > 8192) ? 256 : 128);
+    if (m >= 1024 && (int64_t)((m + 255) / 256) * (n / 256) >= 256)
+      return gemm_plan(kCfgBig, m, n, k, 256);
+  }
+  return gemm_plan(kCfgMid2, m, n, k, k > 8192 ? 512 : 256);
+}
+
+template <class C>
+void launch_cfg(const GemmPlan& c, int epilogue, const GemmArgs& a, hipStream_t s) {
+  const dim3 grid(c.tiles_m * c.tiles_n * c.splits), block(C::kThreads);
+  if (epilogue == SSA_EPILOGUE_NONE)
+    hipLaunchKernelGGL((linear_kernel<C, SSA_EPILOGUE_NONE>), grid, block, 0, s, a);
+  else if (epilogue == SSA_EPILOGUE_RESIDUAL)
+    hipLaunchKernelGGL((linear_kernel<C, SSA_EPILOGUE_RESIDUAL>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((linear_kernel<C, SSA_EPILOGUE_SWIGLU>), grid, block, 0, s, a);
+}
+
+// Launch a planned product; the workspace has been checked against c.ws.
+int launch_linear(const GemmPlan& c, int m, int n, int k, int epilogue, const uint16_t* x,
+                  const uint16_t* w, const uint16_t* residual, uint16_t* out, void* workspace,
+                  hipStream_t s) {
+  GemmArgs a{x, w, residual, out,
+             static_cast<int*>(workspace),
+             c.ws > 0 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + c.tickets) : nullptr,
+             m, n, k, c.tiles_m, c.tiles_n, c.splits, c.kbps, c.kblocks};
+  (void)hipGetLastError();
+  switch (c.cfg) {
+    case kCfgMid: launch_cfg<CfgMid>(c, epilogue, a, s); break;
+    case kCfgMid2: launch_cfg<CfgMid2>(c, epilogue, a, s); break;
+    case kCfgBig: launch_cfg<CfgBig>(c, epilogue, a, s); break;
+    case kCfgWide: launch_cfg<CfgWide>(c, epilogue, a, s); break;
+    case kCfgWide4: launch_cfg<CfgWide4>(c, epilogue, a, s); break;
+    case kCfgSmall: launch_cfg<CfgSmall>(c, epilogue, a, s); break;
+    default: launch_cfg<CfgTiny>(c, epilogue, a, s); break;
+  }
+  return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+}
+
 int check_linear(int32_t m, int32_t n, int32_t k, int32_t epilogue) {
-  if (m < 0 || n <= 0 || k <= 0 || n % BN || k % BK) return SSA_ERR_ARG;
+  if (m < 0 || n <= 0 || k <= 0 || n % 128 || k % BK) return SSA_ERR_ARG;
   if (epilogue < SSA_EPILOGUE_NONE || epilogue > SSA_EPILOGUE_SWIGLU) return SSA_ERR_ARG;
   if ((int64_t)m * k > INT64_C(1) << 40 || (int64_t)n * k > INT64_C(1) << 40) return SSA_ERR_ARG;
   return SSA_OK;
@@ -333,7 +453,7 @@ int ssa_linear_workspace_size(int32_t m, int32_t n, int32_t k, size_t* ws_bytes)
   if (!ws_bytes) return SSA_ERR_NULL;
   const int rc = check_linear(m, n, k, SSA_EPILOGUE_NONE);
   if (rc) return rc;
-  *ws_bytes = m == 0 ? 0 : gemm_cfg(m, n, k).ws;
+  *ws_bytes = m == 0 ? 0 : choose_plan(m, n, k).ws;
   return SSA_OK;
 }
 
@@ -344,33 +464,20 @@ int ssa_linear(int32_t m, int32_t n, int32_t k, int32_t epilogue, const uint16_t
   if (rc) return rc;
   if (m == 0) return SSA_OK;
   if (!x || !w || !out || (epilogue == SSA_EPILOGUE_RESIDUAL && !residual)) return SSA_ERR_NULL;
-  const GemmCfg c = gemm_cfg(m, n, k);
+  const GemmPlan c = choose_plan(m, n, k);
   if (c.ws > 0 && (!workspace || ws_bytes < c.ws)) return SSA_ERR_WORKSPACE;
-  const size_t tickets = ((size_t)c.tiles_m * c.tiles_n * 4 + 255) / 256 * 256;
-  GemmArgs a{x, w, residual, out,
-             static_cast<int*>(workspace),
-             c.ws > 0 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + tickets) : nullptr,
-             m, n, k, c.tiles_m, c.tiles_n, c.splits, c.kbps, c.kblocks};
-  (void)hipGetLastError();
-  const dim3 grid(c.tiles_m * c.tiles_n * c.splits);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (epilogue == SSA_EPILOGUE_NONE)
-    hipLaunchKernelGGL((linear_kernel<kStages, SSA_EPILOGUE_NONE>), grid, dim3(kThreads), 0, s, a);
-  else if (epilogue == SSA_EPILOGUE_RESIDUAL)
-    hipLaunchKernelGGL((linear_kernel<kStages, SSA_EPILOGUE_RESIDUAL>), grid, dim3(kThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL((linear_kernel<kStages, SSA_EPILOGUE_SWIGLU>), grid, dim3(kThreads), 0, s, a);
-  return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+  return launch_linear(c, m, n, k, epilogue, x, w, residual, out, workspace,
+                       static_cast<hipStream_t>(stream));
 }
 
 int ssa_rms_norm(int32_t m, int32_t n, const uint16_t* x, const uint16_t* weight, float eps,
                  uint16_t* out, void* stream) {
-  if (m < 0 || n <= 0 || n % 8 || n > kThreads * 8 * kNormChunks || !(eps >= 0.f))
+  if (m < 0 || n <= 0 || n % 8 || n > kNormThreads * 8 * kNormChunks || !(eps >= 0.f))
     return SSA_ERR_ARG;
   if (m == 0) return SSA_OK;
   if (!x || !weight || !out) return SSA_ERR_NULL;
   (void)hipGetLastError();
-  hipLaunchKernelGGL(rms_norm_kernel, dim3(m), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
+  hipLaunchKernelGGL(rms_norm_kernel, dim3(m), dim3(kNormThreads), 0, static_cast<hipStream_t>(stream),
                      x, weight, out, n, eps);
   return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
 }

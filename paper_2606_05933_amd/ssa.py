@@ -71,6 +71,15 @@ class SsaCandidate(ctypes.Structure):
 CONSTRUCT_NO_RISK, CONSTRUCT_NO_ANCHOR, CONSTRUCT_BATCH = 0, 1, 2
 
 
+class SsaLayerWeights(ctypes.Structure):
+    _fields_ = [("attn_norm", ctypes.c_void_p), ("w_qkv", ctypes.c_void_p),
+                ("w_o", ctypes.c_void_p), ("mlp_norm", ctypes.c_void_p),
+                ("w_gate_up", ctypes.c_void_p), ("w_down", ctypes.c_void_p),
+                ("cos_sin", ctypes.c_void_p), ("hidden", ctypes.c_int32),
+                ("inter", ctypes.c_int32), ("max_position", ctypes.c_int32),
+                ("eps", ctypes.c_float)]
+
+
 class SsaPlanInfo(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "num_reqs", "num_tokens", "num_decode_reqs", "num_chunk_reqs", "num_items",
@@ -154,6 +163,9 @@ def _load():
     lib.ssa_linear_workspace_size.argtypes = [i32, i32, i32, P(sz)]
     lib.ssa_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     lib.ssa_rms_norm.argtypes = [i32, i32, vp, vp, ctypes.c_float, vp, vp]
+    lib.ssa_layer_workspace_size.argtypes = [P(SsaShape), vp, P(SsaLayerWeights), P(sz)]
+    lib.ssa_layer_forward.argtypes = [P(SsaShape), vp, vp, P(SsaLayerWeights), vp, vp, vp, vp, vp,
+                                      vp, sz, vp]
     lib.ssa_priority_sort.argtypes = [P(SsaCandidate), i32, ctypes.c_double, ctypes.c_double,
                                       ctypes.c_double, ip]
     lib.ssa_batch_constructor.argtypes = [P(SsaPredictor), ip, i32, P(SsaCandidate), i32, i32,
@@ -172,7 +184,8 @@ EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
             "ssa_append_attention", "ssa_predictor_init", "ssa_predictor_add",
             "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
             "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor",
-            "ssa_rope_append", "ssa_linear_workspace_size", "ssa_linear", "ssa_rms_norm")
+            "ssa_rope_append", "ssa_linear_workspace_size", "ssa_linear", "ssa_rms_norm",
+            "ssa_layer_workspace_size", "ssa_layer_forward")
 
 EPILOGUE_NONE, EPILOGUE_RESIDUAL, EPILOGUE_SWIGLU = 0, 1, 2
 
@@ -585,6 +598,66 @@ def interleave_gate_up(w_gate, w_up):
     import torch
     return torch.stack([w_gate.reshape(i // 16, 16, k), w_up.reshape(i // 16, 16, k)],
                        dim=1).reshape(2 * i, k).contiguous()
+
+
+class LayerWeights:
+    """Device copies of one decoder layer's weights in the layout of
+    ssa_layer_forward (q/k/v rows stacked, gate/up rows interleaved), and the
+    rotary table.  `host` holds bf16 bit arrays [out, in] (numpy uint16)."""
+
+    def __init__(self, host: dict, hq: int, hkv: int, d: int, max_position: int,
+                 eps: float = 1e-5, base: float = 500000.0):
+        import torch
+
+        def dev(bits):
+            return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(
+                torch.bfloat16)
+
+        self.hidden = int(host["w_q"].shape[1])
+        self.inter = int(host["w_gate"].shape[0])
+        self.hq, self.hkv, self.d = hq, hkv, d
+        self.attn_norm = dev(host["attn_norm"])
+        self.mlp_norm = dev(host["mlp_norm"])
+        self.w_qkv = dev(np.concatenate([host["w_q"], host["w_k"], host["w_v"]], axis=0))
+        self.w_o = dev(host["w_o"])
+        self.w_gate_up = dev(interleave_gate_up(host["w_gate"], host["w_up"]))
+        self.w_down = dev(host["w_down"])
+        self.cos_sin = torch.from_numpy(rope_cos_sin(max_position, d, base)).cuda()
+        self.c = SsaLayerWeights(self.attn_norm.data_ptr(), self.w_qkv.data_ptr(),
+                                 self.w_o.data_ptr(), self.mlp_norm.data_ptr(),
+                                 self.w_gate_up.data_ptr(), self.w_down.data_ptr(),
+                                 self.cos_sin.data_ptr(), self.hidden, self.inter,
+                                 int(max_position), float(eps))
+
+
+def layer_workspace_size(shape: SsaShape, plan_host, weights: LayerWeights) -> int:
+    ws = ctypes.c_size_t(0)
+    _check(LIB.ssa_layer_workspace_size(ctypes.byref(shape), ctypes.c_void_p(_ptr(plan_host)),
+                                        ctypes.byref(weights.c), ctypes.byref(ws)),
+           "ssa_layer_workspace_size")
+    return int(ws.value)
+
+
+def layer_forward(shape: SsaShape, plan_host, plan_dev, weights: LayerWeights, x, out, k_cache,
+                  v_cache, block_table, workspace, stream=None):
+    """ssa_layer_forward: one decoder layer over the plan's new tokens (x, out
+    [T, hidden] bf16; out may be x)."""
+    h = _plan_header(plan_host)
+    T, n = h["num_tokens"], h["num_reqs"]
+    pool = shape.num_pages * shape.num_kv_heads * shape.page_size * shape.head_dim
+    _check_dev("x", x, T * weights.hidden, 2)
+    _check_dev("out", out, T * weights.hidden, 2)
+    _check_dev("k_cache", k_cache, pool, 2)
+    _check_dev("v_cache", v_cache, pool, 2)
+    _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    vp = ctypes.c_void_p
+    rc = LIB.ssa_layer_forward(ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)),
+                               ctypes.byref(weights.c), vp(_ptr(x)), vp(_ptr(out)),
+                               vp(_ptr(k_cache)), vp(_ptr(v_cache)), vp(_ptr(block_table)),
+                               vp(_ptr(workspace)), ctypes.c_size_t(ws_bytes), vp(_stream(stream)))
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_layer_forward")
 
 
 def bind_append_attention(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,

@@ -148,6 +148,22 @@ def normal_bf16(shape, seed: int, std: float = 1.0) -> np.ndarray:
     return _normal_bf16(np.random.default_rng(seed), tuple(shape), std)
 
 
+def layer_weights(seed: int, hidden: int, inter: int, hq: int, hkv: int, d: int) -> dict:
+    """Random weights of one Llama-style decoder layer, as bf16 bits in the
+    torch Linear layout [out, in]: projections N(0, 1/fan_in), RMSNorm weights
+    N(1, 0.1^2)."""
+    shapes = {"w_q": (hq * d, hidden), "w_k": (hkv * d, hidden), "w_v": (hkv * d, hidden),
+              "w_o": (hidden, hq * d), "w_gate": (inter, hidden), "w_up": (inter, hidden),
+              "w_down": (hidden, inter)}
+    out = {}
+    for i, (name, shp) in enumerate(shapes.items()):
+        out[name] = normal_bf16(shp, seed * 16 + i, shp[1] ** -0.5)
+    for j, name in enumerate(("attn_norm", "mlp_norm")):
+        z = np.random.default_rng(seed * 16 + 8 + j).standard_normal(hidden, dtype=np.float32)
+        out[name] = f32_to_bf16_bits(np.float32(1.0) + np.float32(0.1) * z)
+    return out
+
+
 def make_batch(shape: Shape, q_len, ctx_len, seed: int = 0, spare_pages: int = 64,
                poison: bool = True, extra_pages_per_req: int = 0, name: str = "") -> Batch:
     """Draw a batch for the given per-request (c_i, u_i) lists."""

@@ -1,4 +1,5 @@
-"""GPU parity of ssa_rope_append (include/ssa_layer.h) with the CPU oracles.
+"""GPU parity of ssa_rope_append and ssa_layer_forward (include/ssa_layer.h)
+with the CPU oracles.
 
 Bars:
 * rotated queries and keys within bf16 rounding of the float64 rotation
@@ -7,7 +8,10 @@ Bars:
   untouched;
 * RoPE + append, then ssa_mixed_attention, within the attention bar
   (max 2e-2, mean 2e-3) of the attention oracle run on the oracle's own rotated
-  inputs.
+  inputs;
+* ssa_layer_forward (a Llama-style decoder layer) against the composed float64
+  oracle with bf16 tensors at the same places: |err| <= 2^-5 (|ref| + 1),
+  mean <= 3e-3; appended keys and values within two bf16 steps.
 """
 import sys
 
@@ -127,3 +131,62 @@ def test_rope_append_rejects_positions_past_the_table(torch_dev):
                         db.v_cache, db.block_table)
     torch.cuda.synchronize()
     assert torch.equal(before.view(torch.int16), db.k_cache.view(torch.int16))  # NaN-poisoned
+
+
+# ---- ssa_layer_forward: one decoder layer against the composed oracle
+
+LAYER_CASES = [
+    # hidden, inter, hq, hkv, d, [(c, u), ...]
+    (256, 256, 4, 2, 64, [(20, 30), (1, 100), (1, 5), (37, 0)]),
+    (4096, 14336, 32, 8, 128, [(64, 192), (1, 1000), (1, 4000), (1, 17), (70, 0)]),  # Llama-3-8B
+]
+
+
+@pytest.mark.parametrize("case", range(len(LAYER_CASES)))
+def test_layer_forward_matches_the_oracle(torch_dev, case):
+    from dense_ref import to_f32
+    from oracle import layer as olay
+    from paper_2606_05933_amd import ssa, workload
+    from paper_2606_05933_amd.device import DeviceBatch, bits_of
+    torch = torch_dev
+    hidden, inter, hq, hkv, d, cu = LAYER_CASES[case]
+    seed = 40 + case
+    w = workload.layer_weights(seed, hidden, inter, hq, hkv, d)
+    b = workload.make_batch(workload.Shape(hq, hkv, d), [c for c, _ in cu], [u for _, u in cu],
+                            seed=seed, spare_pages=5, name="layer")
+    T = b.num_tokens
+    say(f"[gpu layer] hidden={hidden} inter={inter} hq/hkv/d={hq}/{hkv}/{d} T={T} seed={seed}")
+    x = workload.normal_bf16((T, hidden), seed + 99)
+    db = DeviceBatch(b)
+    lw = ssa.LayerWeights(w, hq, hkv, d, max_position=int(max(c + u for c, u in cu)) + 1)
+    ws = torch.zeros(ssa.layer_workspace_size(db.shape, db.plan_host, lw), dtype=torch.uint8,
+                     device="cuda")
+    xd = torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)
+    out = torch.full((T, hidden), float("nan"), dtype=torch.bfloat16, device="cuda")
+    ssa.layer_forward(db.shape, db.plan_host, db.plan_dev, lw, xd, out, db.k_cache, db.v_cache,
+                      db.block_table, ws)
+    torch.cuda.synchronize()
+    ref, kc_ref, vc_ref = olay.decoder_layer(x, w, hq, hkv, d, b.q_len, b.ctx_len,
+                                             b.block_table, b.k_cache, b.v_cache, eps=1e-5)
+    got = to_f32(bits_of(out).reshape(T, hidden)).astype(np.float64)
+    err = np.abs(got - ref)
+    rel = err / (np.abs(ref) + 1.0)
+    say(f"    out: max_abs={err.max():.3e} mean_abs={err.mean():.3e} max_rel1={rel.max():.3e} "
+        f"rms_ref={np.sqrt(np.mean(ref ** 2)):.3f}")
+    # the new pool slots: within a few bf16 rounding steps of the oracle's
+    kc = to_f32(bits_of(db.k_cache).reshape(b.k_cache.shape)).astype(np.float64)
+    vc = to_f32(bits_of(db.v_cache).reshape(b.v_cache.shape)).astype(np.float64)
+    kr, vr = to_f32(kc_ref).astype(np.float64), to_f32(vc_ref).astype(np.float64)
+    fin = np.isfinite(kr)
+    vfin = np.isfinite(vr)
+    kerr, verr = np.abs(kc[fin] - kr[fin]), np.abs(vc[vfin] - vr[vfin])
+    say(f"    pools: k max_abs={kerr.max():.3e} v max_abs={verr.max():.3e}")
+    assert np.array_equal(np.isfinite(kc), fin)  # no slot outside the new ones written
+    assert np.isfinite(got).all()
+    # Seven bf16 tensors lie between x and out; each may round one step apart
+    # from the oracle's (fp32 vs fp64 sums), and the residual stream carries
+    # such steps with gain about one: a few bf16 steps at unit scale.
+    assert np.all(err <= 2.0 ** -5 * (np.abs(ref) + 1.0)) and err.mean() <= 3e-3
+    # the appended keys and values: at most two rounding steps apart
+    assert np.all(kerr <= 2.0 ** -6 * np.abs(kr[fin]) + 2.0 ** -10)
+    assert np.all(verr <= 2.0 ** -6 * np.abs(vr[vfin]) + 2.0 ** -10)

@@ -86,3 +86,73 @@ def test_library_gate_up_interleave_is_a_row_permutation():
     for b in range(i // 16):
         assert np.array_equal(wgu[32 * b:32 * b + 16], g[16 * b:16 * b + 16])
         assert np.array_equal(wgu[32 * b + 16:32 * b + 32], u[16 * b:16 * b + 16])
+
+
+# ---- the composed decoder layer (oracle.layer.decoder_layer)
+
+def test_bf16_round_ties_and_a_bit_level_rounding():
+    assert orc.bf16_round(1.0) == 1.0
+    assert orc.bf16_round(1 + 2.0 ** -8) == 1.0                   # tie -> even mantissa
+    assert orc.bf16_round(1 + 3 * 2.0 ** -8) == 1 + 2.0 ** -6      # tie -> even mantissa
+    assert orc.bf16_round(1 + 0.6 * 2.0 ** -7) == 1 + 2.0 ** -7
+    assert orc.bf16_round(-(1 + 3 * 2.0 ** -8)) == -(1 + 2.0 ** -6)
+    # float32 inputs are exact in float64, so one rounding: the integer trick on
+    # the float32 bits must agree everywhere
+    from dense_ref import to_bf16, to_f32
+    x = np.random.default_rng(4).standard_normal(200000).astype(np.float32) * 37.0
+    want = to_f32(to_bf16(x)).astype(np.float64)
+    assert np.array_equal(orc.bf16_round(x.astype(np.float64)), want)
+    assert np.array_equal(orc.bf16_bits(want), to_bf16(want.astype(np.float32)))
+
+
+SMALL = dict(hidden=256, inter=256, hq=4, hkv=2, d=64)
+
+
+def small_layer(seed, q_len, ctx_len, zero=()):
+    from paper_2606_05933_amd import workload
+    s = SMALL
+    w = workload.layer_weights(seed, s["hidden"], s["inter"], s["hq"], s["hkv"], s["d"])
+    for name in zero:
+        w[name] = np.zeros_like(w[name])
+    b = workload.make_batch(workload.Shape(s["hq"], s["hkv"], s["d"]), q_len, ctx_len,
+                            seed=seed, spare_pages=3)
+    x = workload.normal_bf16((b.num_tokens, s["hidden"]), seed + 99)
+    return w, b, x
+
+
+def run_layer(w, b, x, q_len=None, ctx_len=None, k_cache=None, v_cache=None):
+    s = SMALL
+    return orc.decoder_layer(x, w, s["hq"], s["hkv"], s["d"],
+                             b.q_len if q_len is None else q_len,
+                             b.ctx_len if ctx_len is None else ctx_len, b.block_table,
+                             b.k_cache if k_cache is None else k_cache,
+                             b.v_cache if v_cache is None else v_cache, eps=1e-5)
+
+
+def test_layer_with_zero_output_projections_is_the_identity():
+    w, b, x = small_layer(1, [5, 1, 1], [0, 7, 40], zero=("w_o", "w_down"))
+    out, _, _ = run_layer(w, b, x)
+    assert np.array_equal(out, orc.from_bits(x))
+
+
+def test_layer_is_causal_and_requests_are_independent():
+    w, b, x = small_layer(2, [6, 1, 4], [3, 20, 0])
+    out, _, _ = run_layer(w, b, x)
+    x2 = x.copy()
+    x2[5] ^= np.uint16(0x0040)  # the last token of request 0
+    out2, _, _ = run_layer(w, b, x2)
+    assert np.array_equal(out2[:5], out[:5]) and np.array_equal(out2[6:], out[6:])
+    assert not np.array_equal(out2[5], out[5])
+    x3 = x.copy()
+    x3[7:] = x3[7:][::-1]  # request 2's rows
+    out3, _, _ = run_layer(w, b, x3)
+    assert np.array_equal(out3[:7], out[:7])
+
+
+def test_layer_chunked_prefill_equals_one_pass():
+    w, b, x = small_layer(3, [24], [10])
+    out, kc, vc = run_layer(w, b, x)
+    o1, kc1, vc1 = run_layer(w, b, x[:16], q_len=[16], ctx_len=[10])
+    o2, kc2, vc2 = run_layer(w, b, x[16:], q_len=[8], ctx_len=[26], k_cache=kc1, v_cache=vc1)
+    assert np.array_equal(np.concatenate([o1, o2]), out)
+    assert np.array_equal(kc2, kc) and np.array_equal(vc2, vc)
