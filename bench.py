@@ -31,6 +31,11 @@ Other modes (all single GPU):
                      decision's batch runs on the GPU; reports the measured
                      latency against the prediction and T_cur, and the window
                      cost against the best budget
+  --layer OUT        a Llama-3-8B decoder layer on the library's kernels (RMSNorm,
+                     projections on the matrix cores, RoPE + kv_append, mixed
+                     attention, SwiGLU MLP) vs chunk size, each step timed, the
+                     projections also through hipBLASLt for comparison (what the
+                     linear layers, Tab. 1's x6 / x7 terms, add to an iteration)
   --constructor OUT  priority sorter + BatchConstructor (Sec. 3.3, 3.5, Alg. 2):
                      where it reconstructs the batch, the full-budget batch and
                      the constructed one both run on the GPU; reports how many
@@ -714,6 +719,112 @@ def main_constructor(args):
     print(json.dumps(res), flush=True)
 
 
+LAYER_DIMS = dict(hidden=4096, inter=14336, hq=32, hkv=8, d=128)  # Llama-3-8B
+LAYER_CHUNKS = (0, 64, 128, 256, 512, 1024, 2048)
+
+
+def time_calls(fns, reps):
+    """Mean duration (us) of each callable over reps rounds, from event pairs
+    recorded around every call on the current stream."""
+    import torch
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in fns] for _ in range(reps)]
+    for f in fns:  # warm up
+        f()
+    torch.cuda.synchronize()
+    for r in range(reps):
+        for (a, b), f in zip(ev[r], fns):
+            a.record()
+            f()
+            b.record()
+    torch.cuda.synchronize()
+    return [statistics.mean(ev[r][i][0].elapsed_time(ev[r][i][1]) for r in range(reps)) * 1e3
+            for i in range(len(fns))]
+
+
+def main_layer(args):
+    """One Llama-3-8B decoder layer (ssa_layer_forward: RMSNorm, QKV projection,
+    RoPE + kv_append, mixed attention, O projection + residual, RMSNorm, SwiGLU
+    MLP + residual; random weights) on the chunk-sweep batches: 128 decodes
+    (u ~ round(LogN(7.0, 0.8)) in [64, 8192]) plus one chunk of c tokens of an
+    8192-token prompt at prefix 2048.  Reports the layer's latency, each step's
+    time, and the same four projections through torch.matmul (hipBLASLt)."""
+    import torch
+    from paper_2606_05933_amd import ssa, workload
+    from paper_2606_05933_amd.device import DeviceBatch
+    torch.cuda.set_device(0)
+    L = LAYER_DIMS
+    host = workload.layer_weights(args.seed, L["hidden"], L["inter"], L["hq"], L["hkv"], L["d"])
+    lw = ssa.LayerWeights(host, L["hq"], L["hkv"], L["d"], max_position=8192 + 2048 + 1)
+    hid, inter, qd = L["hidden"], L["inter"], L["hq"] * L["d"]
+    nqkv = (L["hq"] + 2 * L["hkv"]) * L["d"]
+    rows = []
+    for c in LAYER_CHUNKS:
+        b = workload.make_workload("l8b_sweep", seed=args.seed, chunk=c, prefix=2048)
+        db = DeviceBatch(b)
+        T = b.num_tokens
+        x = torch.from_numpy(workload.normal_bf16((T, hid), args.seed + 7).view(np.int16)).cuda().view(
+            torch.bfloat16)
+        out = torch.empty_like(x)
+        ws = torch.zeros(ssa.layer_workspace_size(db.shape, db.plan_host, lw), dtype=torch.uint8,
+                         device="cuda")
+        (t_layer,) = time_calls([lambda: ssa.layer_forward(
+            db.shape, db.plan_host, db.plan_dev, lw, x, out, db.k_cache, db.v_cache,
+            db.block_table, ws)], args.steps)
+        # the steps one by one, on buffers of their own
+        bf = dict(dtype=torch.bfloat16, device="cuda")
+        xn, qkv, q, a, h = (torch.empty((T, n), **bf) for n in (hid, nqkv, qd, qd, hid))
+        act = torch.empty((T, inter), **bf)
+        gws = torch.zeros(max(4, max(ssa.linear_workspace_size(T, n, k) for n, k in
+                                     ((nqkv, hid), (hid, qd), (2 * inter, hid), (hid, inter)))),
+                          dtype=torch.uint8, device="cuda")
+        steps = {
+            "rms_norm": lambda: ssa.rms_norm(x, lw.attn_norm, xn),
+            "qkv": lambda: ssa.linear(xn, lw.w_qkv, qkv, workspace=gws),
+            "rope_append": lambda: ssa.rope_append(db.shape, db.plan_host, db.plan_dev, qkv,
+                                                   lw.cos_sin, q, db.k_cache, db.v_cache,
+                                                   db.block_table),
+            "attention": lambda: db.attention(),
+            "o_proj": lambda: ssa.linear(a, lw.w_o, h, ssa.EPILOGUE_RESIDUAL, residual=x,
+                                         workspace=gws),
+            "rms_norm_2": lambda: ssa.rms_norm(h, lw.mlp_norm, xn),
+            "gate_up": lambda: ssa.linear(xn, lw.w_gate_up, act, ssa.EPILOGUE_SWIGLU,
+                                          workspace=gws),
+            "down": lambda: ssa.linear(act, lw.w_down, out, ssa.EPILOGUE_RESIDUAL, residual=h,
+                                       workspace=gws),
+        }
+        t_steps = dict(zip(steps, time_calls(list(steps.values()), args.steps)))
+        blas = {"qkv": lambda: torch.matmul(xn, lw.w_qkv.t()),
+                "o_proj": lambda: torch.matmul(a, lw.w_o.t()),
+                "gate_up": lambda: torch.matmul(xn, lw.w_gate_up.t()),
+                "down": lambda: torch.matmul(act, lw.w_down.t())}
+        t_blas = dict(zip(blas, time_calls(list(blas.values()), args.steps)))
+        lin = sum(t_steps[k] for k in blas)
+        flops = 2 * T * (nqkv * hid + hid * qd + 2 * inter * hid + hid * inter)
+        row = {"chunk": c, "tokens": T, "decodes": int((b.q_len == 1).sum()),
+               "layer_us": round(t_layer, 1),
+               "steps_us": {k: round(v, 1) for k, v in t_steps.items()},
+               "linear_us": round(lin, 1), "linear_share": round(lin / sum(t_steps.values()), 3),
+               "linear_TFLOPs": round(flops / lin / 1e6, 1),
+               "hipblaslt_linear_us": {k: round(v, 1) for k, v in t_blas.items()},
+               "hipblaslt_linear_total_us": round(sum(t_blas.values()), 1)}
+        rows.append(row)
+        log(f"[layer] c={c} T={T} layer={t_layer:.1f}us linear={lin:.1f}us "
+            f"(hipBLASLt {sum(t_blas.values()):.1f}us) attention={t_steps['attention']:.1f}us")
+        del db, x, out, ws, xn, qkv, q, a, h, act, gws
+        torch.cuda.empty_cache()
+    tok = np.array([r["tokens"] for r in rows], dtype=np.float64)
+    lay = np.array([r["layer_us"] for r in rows])
+    slope, icpt = np.polyfit(tok, lay, 1)
+    res = {"model": "Llama-3-8B layer (hidden 4096, 32q/8kv/D128, MLP 14336), bf16, random weights",
+           "batches": DESCR["l8b_sweep"] + " at prefix 2048", "rows": rows,
+           "fit_layer_us": {"per_token": round(float(slope), 4), "intercept": round(float(icpt), 1)}}
+    if args.layer:
+        with open(args.layer, "w") as f:
+            json.dump(res, f)
+    print(json.dumps(res), flush=True)
+
+
 def main_sweep_md(args):
     """Markdown tables of a --sweep JSON-lines file, one per workload."""
     rows = [json.loads(l) for l in open(args.sweep_md) if l.strip()]
@@ -789,6 +900,8 @@ def main():
     ap.add_argument("--constructor", metavar="OUT", default=None,
                     help="priority sorter + BatchConstructor on a measured predictor, on the GPU")
     ap.add_argument("--constructor-states", type=int, default=300)
+    ap.add_argument("--layer", metavar="OUT", default=None,
+                    help="a Llama-3-8B decoder layer on the library's kernels vs chunk size")
     args = ap.parse_args()
     if args.traffic_json:
         return main_traffic_json(args)
@@ -812,6 +925,8 @@ def main():
         main_chunker(args)
     elif args.constructor:
         main_constructor(args)
+    elif args.layer:
+        main_layer(args)
     else:
         main_bench(args)
 

@@ -371,7 +371,9 @@ struct GemmPlan {
 };
 
 // Split K when the tiles alone leave the chip under target_wgs workgroups
-// (at least 4 K blocks per split).
+// (at least 4 K blocks per split).  Tiles that overfill the chip by a partial
+// round are not split: measured on MI355X, the extra partials cost about what
+// the evened rounds save (an even spread needs per-unit scheduling instead).
 GemmPlan gemm_plan(int cfg, int m, int n, int k, int target_wgs) {
   const CfgShape& cs = kCfgShapes[cfg];
   GemmPlan c;
@@ -396,14 +398,14 @@ GemmPlan gemm_plan(int cfg, int m, int n, int k, int target_wgs) {
 //    and M > 32: 256) workgroups;
 //  * M >= 1024: 256 x 256 tiles when they alone fill the chip;
 //  * otherwise 128 x 128 tiles at two workgroups per CU, K split to about 256
-//    (K > 8192: 512) workgroups.
+//    (K > 8192: 384) workgroups.
 GemmPlan choose_plan(int m, int n, int k) {
   if (n % 256 == 0) {
     if (m <= 64) return gemm_plan(kCfgTiny, m, n, k, (m > 32 && k > 8192) ? 256 : 128);
     if (m >= 1024 && (int64_t)((m + 255) / 256) * (n / 256) >= 256)
       return gemm_plan(kCfgBig, m, n, k, 256);
   }
-  return gemm_plan(kCfgMid2, m, n, k, k > 8192 ? 512 : 256);
+  return gemm_plan(kCfgMid2, m, n, k, k > 8192 ? 384 : 256);
 }
 
 template <class C>

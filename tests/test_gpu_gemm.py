@@ -39,7 +39,7 @@ CASES = [  # (M, N, K, epilogue)
     (300, 640, 1024, RES),
     (129, 256, 2048, SWIGLU),
     (28, 6144, 4096, NONE),        # a decode-only batch through the QKV projection
-    (520, 4096, 14336, RES),       # the down projection of a mixed batch, K split
+    (520, 4096, 14336, RES),       # the down projection of a mixed batch, K split 3
     (1000, 1024, 512, SWIGLU),
     (257, 28672, 4096, SWIGLU),    # gate/up projection
 ]
@@ -140,7 +140,8 @@ def test_linear_residual_in_place(torch_dev):
 
 
 @pytest.mark.parametrize("m,n,k,epi", [(4096, 6144, 4096, NONE), (2048, 28672, 4096, SWIGLU),
-                                       (3000, 4096, 14336, RES)])
+                                       (3000, 4096, 14336, RES),
+                                       (2176, 4096, 14336, NONE)])
 def test_linear_full_size_sampled_rows(torch_dev, m, n, k, epi):
     from dense_ref import to_f32
     say(f"[gpu linear full] M={m} N={n} K={k} epilogue={epi}")

@@ -187,6 +187,11 @@ def test_layer_forward_matches_the_oracle(torch_dev, case):
     # from the oracle's (fp32 vs fp64 sums), and the residual stream carries
     # such steps with gain about one: a few bf16 steps at unit scale.
     assert np.all(err <= 2.0 ** -5 * (np.abs(ref) + 1.0)) and err.mean() <= 3e-3
-    # the appended keys and values: at most two rounding steps apart
-    assert np.all(kerr <= 2.0 ** -6 * np.abs(kr[fin]) + 2.0 ** -10)
+    # the appended keys and values: at most two rounding steps apart; a key
+    # pair (i, i + D/2) is rotated together, which spreads a rounding step of
+    # one member over both and keeps the pair's norm
+    half = d // 2
+    pn = np.sqrt(kr[..., :half] ** 2 + kr[..., half:] ** 2)
+    pn = np.concatenate([pn, pn], axis=-1)
+    assert np.all(kerr <= 2.0 ** -6 * pn[fin] + 2.0 ** -10)
     assert np.all(verr <= 2.0 ** -6 * np.abs(vr[vfin]) + 2.0 ** -10)
