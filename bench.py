@@ -759,7 +759,9 @@ def main_layer(args):
     hid, inter, qd = L["hidden"], L["inter"], L["hq"] * L["d"]
     nqkv = (L["hq"] + 2 * L["hkv"]) * L["d"]
     rows = []
-    for c in LAYER_CHUNKS:
+    chunks = LAYER_CHUNKS if args.layer_chunks is None else [int(c) for c in
+                                                             args.layer_chunks.split(",")]
+    for c in chunks:
         b = workload.make_workload("l8b_sweep", seed=args.seed, chunk=c, prefix=2048)
         db = DeviceBatch(b)
         T = b.num_tokens
@@ -902,6 +904,8 @@ def main():
     ap.add_argument("--constructor-states", type=int, default=300)
     ap.add_argument("--layer", metavar="OUT", default=None,
                     help="a Llama-3-8B decoder layer on the library's kernels vs chunk size")
+    ap.add_argument("--layer-chunks", default=None,
+                    help="comma-separated chunk sizes for --layer (default 0,64,...,2048)")
     args = ap.parse_args()
     if args.traffic_json:
         return main_traffic_json(args)

@@ -42,6 +42,11 @@ CASES = [  # (M, N, K, epilogue)
     (520, 4096, 14336, RES),       # the down projection of a mixed batch, K split 3
     (1000, 1024, 512, SWIGLU),
     (257, 28672, 4096, SWIGLU),    # gate/up projection
+    # tiles that overfill the chip by part of a round
+    (700, 11264, 512, RES),        # 528 tiles of 128 x 128, ragged M
+    (1100, 8192, 256, NONE),       # 576 tiles, 4 K blocks each
+    (640, 28672, 4096, SWIGLU),    # 1120 tiles of 128 x 128
+    (1152, 28672, 4096, SWIGLU),   # 560 tiles of 256 x 256
 ]
 
 
