@@ -36,6 +36,8 @@ Other modes (all single GPU):
                      attention, SwiGLU MLP) vs chunk size, each step timed, the
                      projections also through hipBLASLt for comparison (what the
                      linear layers, Tab. 1's x6 / x7 terms, add to an iteration)
+  --peaks OUT        achievable peaks of this GPU (HBM read and copy, bf16 MFMA)
+                     from the library's probe kernels, next to the published ones
   --constructor OUT  priority sorter + BatchConstructor (Sec. 3.3, 3.5, Alg. 2):
                      where it reconstructs the batch, the full-budget batch and
                      the constructed one both run on the GPU; reports how many
@@ -224,11 +226,14 @@ def main_bench(args):
     alg_bytes = info.decode_bytes + info.chunk_bytes + info.append_bytes
     achieved = alg_bytes / fused_s / 1e9
     tb = traffic_bytes()
+    hbm_read = hbm_read_probe()
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": None if tb is None else round(tb),
                 "kernel": "append_attention", "algorithmic_bytes": round(alg_bytes),
-                "kernel_us": round(fused_s * 1e6, 2)}
+                "kernel_us": round(fused_s * 1e6, 2),
+                "achievable_peak": round(hbm_read, 1),
+                "frac_of_achievable": round(achieved / hbm_read, 4)}
 
     extra = {}
     if args.extras:
@@ -344,6 +349,70 @@ def main_sweep(args):
                 + ", ".join(f"{k} {v['us']} us" for k, v in segs.items()))
             del db
             torch.cuda.empty_cache()
+
+
+def hbm_read_probe(gib: int = 4, workgroups: int = 16384, reps: int = 8) -> float:
+    """Achievable HBM read rate (GB/s) on this GPU: ssa_probe_hbm_read streaming
+    `gib` GiB (far beyond the 256 MB MALL), best of `reps` launches, timed with
+    events around each."""
+    import torch
+    from paper_2606_05933_amd import ssa
+    src = torch.ones((gib << 30) // 4, dtype=torch.float32, device="cuda")
+    out = torch.empty(workgroups, dtype=torch.int32, device="cuda")
+    best = float("inf")
+    for _ in range(reps + 1):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        nbytes = ssa.probe_hbm_read(src, out, workgroups)
+        b.record()
+        torch.cuda.synchronize()
+        best = min(best, a.elapsed_time(b) / 1e3)
+    del src, out
+    torch.cuda.empty_cache()
+    return nbytes / best / 1e9
+
+
+def main_peaks(args):
+    """Achievable peaks of this GPU for the rooflines: HBM read (the library's
+    streaming probe over a 4 GiB buffer, several grid sizes), HBM copy (torch's
+    device copy of 1 GiB, read + write bytes), and bf16 MFMA (the library's
+    register-only v_mfma_f32_16x16x32_bf16 loop, several grid sizes)."""
+    import torch
+    from paper_2606_05933_amd import ssa
+    torch.cuda.set_device(0)
+    res = {"hbm_read_GBps": {}, "mfma_bf16_TFLOPs": {}}
+    for wg in (1024, 4096, 16384, 32768, 65536):
+        res["hbm_read_GBps"][wg] = round(hbm_read_probe(4, wg), 1)
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    t = []
+    for _ in range(9):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        torch.cuda.synchronize()
+        t.append(a.elapsed_time(b) / 1e3)
+    res["hbm_copy_GBps"] = round(2 * (1 << 30) / min(t[1:]) / 1e9, 1)
+    del src, dst
+    for wg in (256, 512, 1024, 2048, 4096):
+        out = torch.empty(wg, dtype=torch.float32, device="cuda")
+        best = float("inf")
+        for _ in range(6):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            flops = ssa.probe_mfma_bf16(4096, wg, out)
+            b.record()
+            torch.cuda.synchronize()
+            best = min(best, a.elapsed_time(b) / 1e3)
+        res["mfma_bf16_TFLOPs"][wg] = round(flops / best / 1e12, 1)
+    res["hbm_read_best_GBps"] = max(res["hbm_read_GBps"].values())
+    res["mfma_bf16_best_TFLOPs"] = max(res["mfma_bf16_TFLOPs"].values())
+    res["published"] = {"hbm_GBps": HBM_PEAK_GBS, "mfma_bf16_TFLOPs": MFMA_BF16_PEAK_TFLOPS}
+    if args.peaks:
+        with open(args.peaks, "w") as f:
+            json.dump(res, f)
+    print(json.dumps(res), flush=True)
 
 
 def main_copy_probe(args):
@@ -904,6 +973,8 @@ def main():
     ap.add_argument("--constructor-states", type=int, default=300)
     ap.add_argument("--layer", metavar="OUT", default=None,
                     help="a Llama-3-8B decoder layer on the library's kernels vs chunk size")
+    ap.add_argument("--peaks", metavar="OUT", default=None,
+                    help="measure the achievable HBM read / copy and bf16 MFMA rates")
     ap.add_argument("--layer-chunks", default=None,
                     help="comma-separated chunk sizes for --layer (default 0,64,...,2048)")
     args = ap.parse_args()
@@ -931,6 +1002,8 @@ def main():
         main_constructor(args)
     elif args.layer:
         main_layer(args)
+    elif args.peaks:
+        main_peaks(args)
     else:
         main_bench(args)
 

@@ -1,0 +1,46 @@
+/*
+ * ssa_probe.h -- measurement support: the achievable peaks of the GPU that
+ * the rooflines of the library's kernels are stated against, next to the
+ * published ones.  Not part of any serving path.
+ *
+ * Same conventions as ssa.h: 0 or a negative SSA_ERR_* code, validation before
+ * any HIP call, no allocation.
+ */
+#ifndef SSA_PROBE_H
+#define SSA_PROBE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "ssa.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * Streams `bytes` of device memory at `src` (16-byte aligned, bytes a multiple
+ * of 16 and > 0) through 16-byte vector loads, several in flight per thread,
+ * and writes one 32-bit XOR of the data per workgroup to out[workgroups]
+ * (`workgroups` in 1..65536) so that no load can be dropped.  Bytes read per
+ * launch: `bytes`.
+ * Errors: SSA_ERR_ARG, SSA_ERR_NULL, SSA_ERR_HIP.
+ */
+int ssa_probe_hbm_read(const void* src, size_t bytes, uint32_t* out, int32_t workgroups,
+                       void* stream);
+
+/*
+ * Runs `iters` rounds of 16 independent v_mfma_f32_16x16x32_bf16 chains in
+ * each wave of `workgroups` workgroups of 256 threads (iters in 1..2^20,
+ * workgroups in 1..65536) on register data, and writes one float per
+ * workgroup to out[workgroups].  Flops per launch:
+ * workgroups * 4 * iters * 16 * 16384.
+ * Errors: SSA_ERR_ARG, SSA_ERR_NULL, SSA_ERR_HIP.
+ */
+int ssa_probe_mfma_bf16(int32_t iters, int32_t workgroups, float* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSA_PROBE_H */

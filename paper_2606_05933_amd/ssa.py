@@ -163,6 +163,8 @@ def _load():
     lib.ssa_linear_workspace_size.argtypes = [i32, i32, i32, P(sz)]
     lib.ssa_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     lib.ssa_rms_norm.argtypes = [i32, i32, vp, vp, ctypes.c_float, vp, vp]
+    lib.ssa_probe_hbm_read.argtypes = [vp, sz, vp, i32, vp]
+    lib.ssa_probe_mfma_bf16.argtypes = [i32, i32, vp, vp]
     lib.ssa_layer_workspace_size.argtypes = [P(SsaShape), vp, P(SsaLayerWeights), P(sz)]
     lib.ssa_layer_forward.argtypes = [P(SsaShape), vp, vp, P(SsaLayerWeights), vp, vp, vp, vp, vp,
                                       vp, sz, vp]
@@ -185,7 +187,8 @@ EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
             "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
             "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor",
             "ssa_rope_append", "ssa_linear_workspace_size", "ssa_linear", "ssa_rms_norm",
-            "ssa_layer_workspace_size", "ssa_layer_forward")
+            "ssa_layer_workspace_size", "ssa_layer_forward", "ssa_probe_hbm_read",
+            "ssa_probe_mfma_bf16")
 
 EPILOGUE_NONE, EPILOGUE_RESIDUAL, EPILOGUE_SWIGLU = 0, 1, 2
 
@@ -628,6 +631,22 @@ class LayerWeights:
                                  self.w_gate_up.data_ptr(), self.w_down.data_ptr(),
                                  self.cos_sin.data_ptr(), self.hidden, self.inter,
                                  int(max_position), float(eps))
+
+
+def probe_hbm_read(src, out, workgroups: int, stream=None):
+    """ssa_probe_hbm_read over the whole of the device tensor src."""
+    nbytes = src.numel() * src.element_size()
+    _check(LIB.ssa_probe_hbm_read(ctypes.c_void_p(_ptr(src)), ctypes.c_size_t(nbytes),
+                                  ctypes.c_void_p(_ptr(out)), int(workgroups),
+                                  ctypes.c_void_p(_stream(stream))), "ssa_probe_hbm_read")
+    return nbytes
+
+
+def probe_mfma_bf16(iters: int, workgroups: int, out, stream=None):
+    """ssa_probe_mfma_bf16; returns the flops of the launch."""
+    _check(LIB.ssa_probe_mfma_bf16(int(iters), int(workgroups), ctypes.c_void_p(_ptr(out)),
+                                   ctypes.c_void_p(_stream(stream))), "ssa_probe_mfma_bf16")
+    return workgroups * 4 * iters * 16 * 16384
 
 
 def layer_workspace_size(shape: SsaShape, plan_host, weights: LayerWeights) -> int:

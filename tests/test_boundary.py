@@ -52,7 +52,7 @@ def test_library_exports_every_declared_symbol():
     for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
         if h.endswith(".h"):
             text = open(os.path.join(ROOT, "include", h)).read()
-            declared |= set(re.findall(r"\b(ssa_[a-z_]+)\s*\(", text))
+            declared |= set(re.findall(r"\b(ssa_[a-z0-9_]+)\s*\(", text))
     assert declared == set(ssa.EXPORTED)
     lib = ctypes.CDLL(ssa.LIB_PATH)
     for name in declared:
