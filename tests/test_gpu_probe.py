@@ -1,0 +1,54 @@
+"""The probe kernels of include/ssa_probe.h compute what they claim, so that the
+rates measured with them count real work: the read probe's per-workgroup XORs
+combine to the XOR of every word of the buffer (each byte was loaded), and the
+MFMA probe's sum equals the closed form of its MFMA chains."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    torch.cuda.set_device(0)
+    return torch
+
+
+@pytest.mark.parametrize("words,wgs", [(4, 1), (1 << 20, 37), ((1 << 22) + 12, 4096)])
+def test_hbm_read_probe_reads_every_word(torch_dev, words, wgs):
+    from paper_2606_05933_amd import ssa
+    torch = torch_dev
+    host = np.random.default_rng(words).integers(0, 2 ** 32, size=words, dtype=np.uint64).astype(
+        np.uint32)
+    src = torch.from_numpy(host.view(np.int32)).cuda()
+    out = torch.zeros(wgs, dtype=torch.int32, device="cuda")
+    assert ssa.probe_hbm_read(src, out, wgs) == words * 4
+    torch.cuda.synchronize()
+    got = np.bitwise_xor.reduce(out.cpu().numpy().view(np.uint32))
+    assert got == np.bitwise_xor.reduce(host)
+
+
+def test_mfma_probe_matches_the_closed_form(torch_dev):
+    from dense_ref import to_bf16, to_f32
+    from paper_2606_05933_amd import ssa
+    torch = torch_dev
+    iters, wgs = 8, 3
+    out = torch.zeros(wgs, dtype=torch.float32, device="cuda")
+    assert ssa.probe_mfma_bf16(iters, wgs, out) == wgs * 4 * iters * 16 * 16384
+    torch.cuda.synchronize()
+    # lane l supplies row / column l % 16 of k block l // 16: a[j] = s + 0.01 j with
+    # s = 0.125 (l % 8), b[j] = 0.5 - 0.01 j, both rounded to bf16
+    j = np.arange(8)
+    def bf(x):
+        return to_f32(to_bf16(np.asarray(x, np.float32))).astype(np.float64)
+    b = bf(0.5 - 0.01 * j)
+    d = np.zeros((16, 16))
+    for r in range(16):
+        for g in range(4):
+            a = bf(np.float32(0.125 * ((g * 16 + r) % 8)) + np.float32(0.01) * j.astype(np.float32))
+            d[r, :] += np.dot(a, b)  # every column of a k block sees the same b
+    want = 4 * 16 * iters * d.sum()  # waves x chains x iterations x all 256 outputs
+    got = out.cpu().numpy().astype(np.float64)
+    assert np.allclose(got, want, rtol=1e-5)
