@@ -326,40 +326,74 @@ __device__ __forceinline__ void col_target(const WorkItem& it, const ReqEntry& r
 
 // Partial records cross workgroups (and XCDs, whose L2s are not coherent with
 // each other).  They are written with device-scope stores, which write through
-// to the device coherence point, and read back with device-scope loads, which
-// do not hit a stale L2 copy; the ticket is a device-scope atomic.  This needs
-// no L2 write-back or invalidation.
+// to the device coherence point, and read back with device-coherent loads
+// (RecordReader below), which do not hit a stale L2 copy; the ticket is a
+// device-scope atomic.  This needs no L2 write-back or invalidation.
 __device__ __forceinline__ void st_dev(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float ld_dev(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 // s_waitcnt vmcnt(0): this wave's stores have completed at their scope.
 __device__ __forceinline__ void wait_vm_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Reads of the partial records by the merging workgroup: 4-byte buffer loads
+// with the device-coherent cache policy (sc1), the instruction of a
+// device-scope load, so they do not hit a stale L2 line.  Being plain loads to
+// the compiler, many are issued before the first wait (device-scope atomic
+// loads are issued one split at a time).  Offsets are bytes from the group's
+// first record.
+constexpr int kCachePolicySc1 = 16;
+struct RecordReader {
+  __amdgpu_buffer_rsrc_t rsrc;
+  __device__ explicit RecordReader(const float* base)
+      : rsrc(__builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), (short)0, 0x7fffffff,
+                                               0x00020000)) {}
+  __device__ float operator()(int64_t float_off) const {
+    return __builtin_bit_cast(
+        float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)(float_off * 4), 0, kCachePolicySc1));
+  }
+};
 
 // Last arriver of a merge group: combine the split records in split order.
 template <int D>
 __device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
                             const MergeGroup& grp) {
-  const float* base = reinterpret_cast<const float*>(a.ws + a.ws_partials_off) + grp.ws_off;
-  const int C = grp.ncols;
+  const RecordReader rd(reinterpret_cast<const float*>(a.ws + a.ws_partials_off) + grp.ws_off);
+  const int C = grp.ncols, S = grp.nsplit;
   const int64_t rec = (int64_t)C * (D + 2);
   for (int idx = threadIdx.x; idx < C * (D / 4); idx += kThreads) {
     const int col = idx / (D / 4);
     const int d0 = (idx % (D / 4)) * 4;
+    // the splits' maxima, eight in flight
     float M = kNegInf;
-    for (int s = 0; s < grp.nsplit; ++s) M = fmaxf(M, ld_dev(base + s * rec + col));
+    for (int s0 = 0; s0 < S; s0 += 8) {
+      float ms[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) ms[j] = s0 + j < S ? rd((s0 + j) * rec + col) : kNegInf;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) M = fmaxf(M, ms[j]);
+    }
+    // weights and sums in split order, four splits' records in flight
     float L = 0.f;
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < grp.nsplit; ++s) {
-      const float* r = base + s * rec;
-      const float ms = ld_dev(r + col);
-      const float w = (ms == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(ms - M);
-      L += w * ld_dev(r + C + col);
-      const float* o = r + 2 * C + (int64_t)col * D + d0;
+    for (int s0 = 0; s0 < S; s0 += 4) {
+      float ms[4], ls[4], os[4][4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) acc[k] += w * ld_dev(o + k);
+      for (int j = 0; j < 4; ++j) {
+        const int64_t r = (int64_t)(s0 + j) * rec;
+        const bool in = s0 + j < S;
+        ms[j] = in ? rd(r + col) : kNegInf;
+        ls[j] = in ? rd(r + C + col) : 0.f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) os[j][k] = in ? rd(r + 2 * C + (int64_t)col * D + d0 + k) : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (s0 + j >= S) break;
+        const float w = (ms[j] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(ms[j] - M);
+        L += w * ls[j];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc[k] += w * os[j][k];
+      }
     }
     const float inv = 1.f / L;
     int row, head;
