@@ -344,14 +344,11 @@ __global__ __launch_bounds__(kNormThreads) void rms_norm_kernel(const uint16_t* 
 }
 
 // The tile configurations the host chooses from.
-using CfgMid = TileCfg<2, 2, 4, 4, 3, 1>;    // 128 x 128, 4 waves of 64 x 64
-using CfgMid2 = TileCfg<2, 2, 4, 4, 2, 2>;   // 128 x 128, two workgroups per CU
+using CfgMid2 = TileCfg<2, 2, 4, 4, 2, 2>;   // 128 x 128, 4 waves of 64 x 64, two per CU
 using CfgBig = TileCfg<2, 4, 8, 4, 2, 1>;    // 256 x 256, 8 waves of 128 x 64
-using CfgWide = TileCfg<4, 2, 4, 4, 3, 1>;   // 256 x 128, 8 waves of 64 x 64
-using CfgWide4 = TileCfg<2, 2, 8, 4, 3, 1>;  // 256 x 128, 4 waves of 128 x 64
-using CfgSmall = TileCfg<1, 4, 4, 4, 3, 1>;  // 64 x 256: few tokens, weight streaming
-using CfgTiny = TileCfg<1, 4, 2, 4, 4, 1>;   // 32 x 256
-enum { kCfgMid, kCfgMid2, kCfgBig, kCfgWide, kCfgWide4, kCfgSmall, kCfgTiny, kNumCfgs };
+using CfgM64 = TileCfg<2, 2, 2, 4, 3, 2>;    // 64 x 128, 4 waves of 32 x 64, two per CU
+using CfgTiny = TileCfg<1, 4, 2, 4, 4, 1>;   // 32 x 256: few tokens, weight streaming
+enum { kCfgMid2, kCfgBig, kCfgM64, kCfgTiny, kNumCfgs };
 
 struct CfgShape {
   int bm, bn, occ;
@@ -360,10 +357,8 @@ template <class C>
 constexpr CfgShape shape_of() {
   return CfgShape{C::BM, C::BN, C::OCC};
 }
-constexpr CfgShape kCfgShapes[kNumCfgs] = {shape_of<CfgMid>(),   shape_of<CfgMid2>(),
-                                           shape_of<CfgBig>(),   shape_of<CfgWide>(),
-                                           shape_of<CfgWide4>(), shape_of<CfgSmall>(),
-                                           shape_of<CfgTiny>()};
+constexpr CfgShape kCfgShapes[kNumCfgs] = {shape_of<CfgMid2>(), shape_of<CfgBig>(),
+                                           shape_of<CfgM64>(), shape_of<CfgTiny>()};
 
 struct GemmPlan {
   int cfg, tiles_m, tiles_n, splits, kbps, kblocks;
@@ -392,21 +387,47 @@ GemmPlan gemm_plan(int cfg, int m, int n, int k, int target_wgs) {
   return c;
 }
 
+// The same tiles in (up to) s K splits of at least 4 K blocks.
+GemmPlan split_plan(GemmPlan c, int s) {
+  const CfgShape& cs = kCfgShapes[c.cfg];
+  s = std::max(1, std::min(s, c.kblocks / 4));
+  c.kbps = (c.kblocks + s - 1) / s;
+  c.splits = (c.kblocks + c.kbps - 1) / c.kbps;
+  const size_t tiles = (size_t)c.tiles_m * c.tiles_n;
+  c.ws = c.splits > 1 ? c.tickets + tiles * c.splits * cs.bm * cs.bn * 4 : 0;
+  return c;
+}
+
 // Measured on MI355X against the Llama-3-8B projections (N x K = 6144 x 4096,
-// 4096 x 4096, 28672 x 4096, 4096 x 14336) for M = 28 .. 4096:
+// 4096 x 4096, 28672 x 4096, 4096 x 14336) for M = 28 .. 4096, with the
+// weights out of the caches as they are inside a layer (T128 = the number of
+// 128 x 128 tiles):
 //  * M <= 64: weight streaming; 32 x 256 tiles, K split to about 128 (long K
 //    and M > 32: 256) workgroups;
-//  * M >= 1536: 256 x 256 tiles when they alone fill the chip (at M = 1152
-//    the 128 x 128 tiles are faster: 259 against 305 us for gate/up);
-//  * otherwise 128 x 128 tiles at two workgroups per CU, K split to about 256
-//    (K > 8192: 384) workgroups.
+//  * M >= 1536 with at least 192 tiles of 256 x 256: those;
+//  * K > 8192: 64 x 128 tiles when T128 < 96, else 128 x 128 tiles in three
+//    K splits (the down projection: 94 against 198 us unsplit at M = 384, 338
+//    against 360 at M = 2176);
+//  * otherwise 64 x 128 tiles when T128 < 256, else 128 x 128 tiles (at
+//    M = 640: 40 against 60 us for the O projection);
+//  * 64 x 128 tiles are K-split to about 256 workgroups when there are at most
+//    128 of them, and at least in two for K > 8192 (at M = 256 the down
+//    projection's 128 tiles: 108 us unsplit).
 GemmPlan choose_plan(int m, int n, int k) {
+  const int64_t t128 = (int64_t)((m + 127) / 128) * (n / 128);
   if (n % 256 == 0) {
     if (m <= 64) return gemm_plan(kCfgTiny, m, n, k, (m > 32 && k > 8192) ? 256 : 128);
-    if (m >= 1536 && (int64_t)((m + 255) / 256) * (n / 256) >= 256)
+    if (m >= 1536 && (int64_t)((m + 255) / 256) * (n / 256) >= 192)
       return gemm_plan(kCfgBig, m, n, k, 256);
   }
-  return gemm_plan(kCfgMid2, m, n, k, k > 8192 ? 384 : 256);
+  auto m64 = [&](int min_splits) {
+    const GemmPlan c = gemm_plan(kCfgM64, m, n, k, 1);
+    const int tiles = c.tiles_m * c.tiles_n;
+    return split_plan(c, std::max(min_splits, tiles <= 128 ? (256 + tiles - 1) / tiles : 1));
+  };
+  if (k > 8192) return t128 < 96 ? m64(2) : split_plan(gemm_plan(kCfgMid2, m, n, k, 1), 3);
+  if (t128 < 256) return m64(1);
+  return gemm_plan(kCfgMid2, m, n, k, 1);
 }
 
 template <class C>
@@ -430,12 +451,9 @@ int launch_linear(const GemmPlan& c, int m, int n, int k, int epilogue, const ui
              m, n, k, c.tiles_m, c.tiles_n, c.splits, c.kbps, c.kblocks};
   (void)hipGetLastError();
   switch (c.cfg) {
-    case kCfgMid: launch_cfg<CfgMid>(c, epilogue, a, s); break;
     case kCfgMid2: launch_cfg<CfgMid2>(c, epilogue, a, s); break;
     case kCfgBig: launch_cfg<CfgBig>(c, epilogue, a, s); break;
-    case kCfgWide: launch_cfg<CfgWide>(c, epilogue, a, s); break;
-    case kCfgWide4: launch_cfg<CfgWide4>(c, epilogue, a, s); break;
-    case kCfgSmall: launch_cfg<CfgSmall>(c, epilogue, a, s); break;
+    case kCfgM64: launch_cfg<CfgM64>(c, epilogue, a, s); break;
     default: launch_cfg<CfgTiny>(c, epilogue, a, s); break;
   }
   return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
