@@ -65,7 +65,8 @@ enum {
  *        chip).  Its first words are split tickets: zero before the first call
  *        (a zeroed allocation), and zero again after every call.  Calls that
  *        share a workspace must be ordered on one stream.
- * Requires N % 128 == 0 and K % 64 == 0; M >= 0 (M == 0 does nothing).
+ * Requires N % 128 == 0 and K % 64 == 0; M >= 0 (M == 0 does nothing); M K and N K
+ * below 2^40 and (M / 32 + 1) (N / 128) at most 2^24.
  * Results do not depend on the launch order of workgroups: split partials are
  * added in split order.
  * Errors: SSA_ERR_ARG (sizes, epilogue), SSA_ERR_NULL, SSA_ERR_WORKSPACE,

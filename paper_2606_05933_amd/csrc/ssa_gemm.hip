@@ -459,10 +459,14 @@ int launch_linear(const GemmPlan& c, int m, int n, int k, int epilogue, const ui
   return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
 }
 
+// Sizes whose tile and workgroup counts fit the plan's 32-bit fields (at most
+// 2^24 tiles of the smallest tile, 32 x 128, each split at most kblocks / 4
+// ways) and whose operands stay below 2^40 elements.
 int check_linear(int32_t m, int32_t n, int32_t k, int32_t epilogue) {
   if (m < 0 || n <= 0 || k <= 0 || n % 128 || k % BK) return SSA_ERR_ARG;
   if (epilogue < SSA_EPILOGUE_NONE || epilogue > SSA_EPILOGUE_SWIGLU) return SSA_ERR_ARG;
   if ((int64_t)m * k > INT64_C(1) << 40 || (int64_t)n * k > INT64_C(1) << 40) return SSA_ERR_ARG;
+  if ((int64_t)(m / 32 + 1) * (n / 128) > INT64_C(1) << 24) return SSA_ERR_ARG;
   return SSA_OK;
 }
 

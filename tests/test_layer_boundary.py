@@ -18,7 +18,7 @@ def ws(m, n, k):
 
 
 @pytest.mark.parametrize("m,n,k", [(-1, 128, 64), (4, 100, 64), (4, 128, 65), (4, 0, 64),
-                                   (4, 128, 0)])
+                                   (4, 128, 0), (2 ** 31 - 1, 1 << 20, 64)])
 def test_linear_rejects_bad_sizes(m, n, k):
     assert ws(m, n, k)[0] == ssa.SSA_ERR_ARG
     assert LIB.ssa_linear(m, n, k, 0, NULL, NULL, NULL, NULL, NULL, 0, NULL) == ssa.SSA_ERR_ARG
