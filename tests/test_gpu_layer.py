@@ -136,9 +136,11 @@ def test_rope_append_rejects_positions_past_the_table(torch_dev):
 # ---- ssa_layer_forward: one decoder layer against the composed oracle
 
 LAYER_CASES = [
-    # hidden, inter, hq, hkv, d, [(c, u), ...]
-    (256, 256, 4, 2, 64, [(20, 30), (1, 100), (1, 5), (37, 0)]),
-    (4096, 14336, 32, 8, 128, [(64, 192), (1, 1000), (1, 4000), (1, 17), (70, 0)]),  # Llama-3-8B
+    # hidden, inter, hq, hkv, d, [(c, u), ...], out written over x
+    (256, 256, 4, 2, 64, [(20, 30), (1, 100), (1, 5), (37, 0)], False),
+    (4096, 14336, 32, 8, 128, [(64, 192), (1, 1000), (1, 4000), (1, 17), (70, 0)], False),
+    (4096, 14336, 32, 8, 128, [(1, u) for u in (3, 90, 700, 2500, 6000)], True),  # decodes only
+    (512, 1024, 8, 8, 64, [(150, 0), (33, 260)], True),                            # prefill only
 ]
 
 
@@ -149,20 +151,22 @@ def test_layer_forward_matches_the_oracle(torch_dev, case):
     from paper_2606_05933_amd import ssa, workload
     from paper_2606_05933_amd.device import DeviceBatch, bits_of
     torch = torch_dev
-    hidden, inter, hq, hkv, d, cu = LAYER_CASES[case]
+    hidden, inter, hq, hkv, d, cu, in_place = LAYER_CASES[case]
     seed = 40 + case
     w = workload.layer_weights(seed, hidden, inter, hq, hkv, d)
     b = workload.make_batch(workload.Shape(hq, hkv, d), [c for c, _ in cu], [u for _, u in cu],
                             seed=seed, spare_pages=5, name="layer")
     T = b.num_tokens
-    say(f"[gpu layer] hidden={hidden} inter={inter} hq/hkv/d={hq}/{hkv}/{d} T={T} seed={seed}")
+    say(f"[gpu layer] hidden={hidden} inter={inter} hq/hkv/d={hq}/{hkv}/{d} T={T} seed={seed} "
+        f"in_place={in_place}")
     x = workload.normal_bf16((T, hidden), seed + 99)
     db = DeviceBatch(b)
     lw = ssa.LayerWeights(w, hq, hkv, d, max_position=int(max(c + u for c, u in cu)) + 1)
     ws = torch.zeros(ssa.layer_workspace_size(db.shape, db.plan_host, lw), dtype=torch.uint8,
                      device="cuda")
     xd = torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16)
-    out = torch.full((T, hidden), float("nan"), dtype=torch.bfloat16, device="cuda")
+    out = xd if in_place else torch.full((T, hidden), float("nan"), dtype=torch.bfloat16,
+                                         device="cuda")
     ssa.layer_forward(db.shape, db.plan_host, db.plan_dev, lw, xd, out, db.k_cache, db.v_cache,
                       db.block_table, ws)
     torch.cuda.synchronize()
