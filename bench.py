@@ -75,6 +75,8 @@ DESCR = {
              "u~round(LogN(7.2,1.0)) in [64,16384]",
     "l70b": "Llama-3-70B-shaped layer: 64q/8kv/D128, 1 chunk (u=32768,c=1024) + 32 decodes "
             "u~U[8192,32768]",
+    "l70b_tp8": "one GPU's share of the Llama-3-70B-shaped layer under 8-way head parallelism: "
+                "8q/1kv/D128, 1 chunk (u=32768,c=1024) + 32 decodes u~U[8192,32768]",
 }
 
 
@@ -285,7 +287,7 @@ def sweep_rows(name):
         return [(0, 0)] + [(c, u) for u in (0, 2048, 6144) for c in (128, 256, 512, 1024, 2048)]
     if name == "multi":
         return [(0, None)] + [(c, None) for c in (128, 256, 512, 1024)]
-    if name == "l70b":
+    if name in ("l70b", "l70b_tp8"):
         return [(c, 32768) for c in (0, 128, 256, 512, 1024, 2048)]
     raise KeyError(name)
 

@@ -238,6 +238,8 @@ def workload_lengths(name: str, seed: int = 0, chunk: int | None = None,
       multi       28q/4kv/D128: 4 chunks c in {64,256,512,1024}, u ~ U[0,8192]
                   + 256 decodes, u ~ round(LogN(7.2,1.0)) clipped to [64,16384]
       l70b        64q/8kv/D128: 1 chunk (u=32768, c=1024) + 32 decodes, u ~ U[8192,32768]
+      l70b_tp8    one GPU's share of l70b under 8-way head parallelism: 8q/1kv/D128,
+                  the same lengths
     ``chunk`` / ``prefix`` override the chunk size / prefix of the first chunk
     request (the chunk-size sweep knob); ``chunk=0`` leaves a pure-decode batch.
     Uniform integers are inclusive at both ends; lognormal draws are rounded then
@@ -267,8 +269,8 @@ def workload_lengths(name: str, seed: int = 0, chunk: int | None = None,
             chunks = [max(0, int(round(x * chunk / 512))) for x in chunks]
         c = chunks + [1] * 256
         u = pre.tolist() + dec.tolist()
-    elif name == "l70b":
-        shape = Shape(64, 8, 128)
+    elif name in ("l70b", "l70b_tp8"):
+        shape = Shape(64, 8, 128) if name == "l70b" else Shape(8, 1, 128)
         dec = rng.integers(8192, 32768, size=32, endpoint=True)
         c = [1024 if chunk is None else chunk] + [1] * 32
         u = [32768 if prefix is None else prefix] + dec.tolist()
@@ -282,7 +284,7 @@ def workload_lengths(name: str, seed: int = 0, chunk: int | None = None,
     return shape, q_len, ctx_len
 
 
-WORKLOADS = ("tiny", "l8b", "l8b_sweep", "multi", "l70b")
+WORKLOADS = ("tiny", "l8b", "l8b_sweep", "multi", "l70b", "l70b_tp8")
 
 
 def make_workload(name: str, seed: int = 0, chunk: int | None = None,

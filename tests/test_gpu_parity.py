@@ -195,7 +195,7 @@ def sampled_parity(b, n_chunk_rows=24, heads_per_row=4, seed=0):
     ("multi", None, None), ("l70b", None, None),
     ("l8b_sweep", 2048, 6144), ("l8b_sweep", 128, 0), ("l8b_sweep", 1024, 2048),
     ("l8b_sweep", 2048, 0), ("l8b_sweep", 256, 6144), ("multi", 1024, None),
-    ("l70b", 2048, None), ("l8b", 2048, None),
+    ("l70b", 2048, None), ("l8b", 2048, None), ("l70b_tp8", None, None),
 ])
 def test_full_size_sampled_parity(torch_dev, name, chunk, prefix):
     from paper_2606_05933_amd import workload
