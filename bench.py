@@ -36,6 +36,10 @@ Other modes (all single GPU):
                      attention, SwiGLU MLP) vs chunk size, each step timed, the
                      projections also through hipBLASLt for comparison (what the
                      linear layers, Tab. 1's x6 / x7 terms, add to an iteration)
+  --layer-predictor OUT
+                     Eq. 5 fitted on measured whole-layer times (random batches of
+                     the three scenes), with all seven Tab. 1 features and without
+                     the linear layers' terms x6, x7
   --peaks OUT        achievable peaks of this GPU (HBM read and copy, bf16 MFMA)
                      from the library's probe kernels, next to the published ones
   --constructor OUT  priority sorter + BatchConstructor (Sec. 3.3, 3.5, Alg. 2):
@@ -634,6 +638,102 @@ def main_predictor(args):
     print(json.dumps(res), flush=True)
 
 
+class LayerTimer:
+    """Times ssa_layer_forward (one Llama-3-8B decoder layer, random weights) on
+    arbitrary batches {(c_i, u_i)}: buffers sized once for the largest batch,
+    each batch gets a random block table and a host plan; the median of 5
+    calls, from events recorded around each call."""
+
+    def __init__(self, batches, seed):
+        import torch
+        from paper_2606_05933_amd import ssa, workload
+        self.torch, self.ssa = torch, ssa
+        L = LAYER_DIMS
+        hq, hkv, d = L["hq"], L["hkv"], L["d"]
+        need = [[(u + c + 15) // 16 for c, u in zip(cs, us)] for cs, us in batches]
+        self.num_pages = max(sum(nd) for nd in need) + 64
+        self.maxp = max(max(nd) for nd in need)
+        self.max_reqs = max(len(cs) for cs, _ in batches)
+        max_tokens = max(sum(cs) for cs, _ in batches)
+        max_pos = max(u + c for cs, us in batches for c, u in zip(cs, us)) + 1
+        self.shape = ssa.make_shape(hq, hkv, d, self.num_pages, self.maxp, d ** -0.5)
+        host = workload.layer_weights(seed, L["hidden"], L["inter"], hq, hkv, d)
+        self.lw = ssa.LayerWeights(host, hq, hkv, d, max_position=max_pos)
+        plan_bytes, ws_bytes = 0, 0
+        for cs, us in batches:
+            pb, _ = ssa.ssa_plan_size(self.shape, cs, us)
+            plan_bytes = max(plan_bytes, pb)
+        self.plan = torch.zeros(max(plan_bytes, 128), dtype=torch.uint8).pin_memory()
+        for cs, us in batches:
+            ssa.ssa_plan(self.shape, cs, us, out=self.plan)
+            ws_bytes = max(ws_bytes, ssa.layer_workspace_size(self.shape, self.plan, self.lw))
+        dev, bf = "cuda", torch.bfloat16
+        self.kc = torch.empty(self.num_pages * hkv * 16 * d, dtype=bf, device=dev).normal_()
+        self.vc = torch.empty_like(self.kc).normal_()
+        self.x = torch.empty((max_tokens, L["hidden"]), dtype=bf, device=dev).normal_()
+        self.out = torch.empty_like(self.x)
+        self.bt = torch.zeros(self.max_reqs * self.maxp, dtype=torch.int32, device=dev)
+        self.ws = torch.zeros(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+        self.rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 14])))
+
+    def time(self, cs, us):
+        """(layer us, plan info) of the batch."""
+        torch, ssa = self.torch, self.ssa
+        table = np.zeros((self.max_reqs, self.maxp), dtype=np.int32)
+        pages = self.rng.permutation(self.num_pages)
+        off = 0
+        for i, (c, u) in enumerate(zip(cs, us)):
+            npg = (u + c + 15) // 16
+            table[i, :npg] = pages[off: off + npg]
+            off += npg
+        torch.cuda.synchronize()
+        self.bt.copy_(torch.from_numpy(table.reshape(-1)))
+        _, info = ssa.ssa_plan(self.shape, cs, us, out=self.plan)
+        t = sum(cs)
+
+        def call():
+            ssa.layer_forward(self.shape, self.plan, self.plan, self.lw, self.x[:t], self.out[:t],
+                              self.kc, self.vc, self.bt, self.ws)
+        (med,) = time_calls([call], 5)
+        return med, info
+
+
+def main_layer_predictor(args):
+    """Eq. 5 (per scene, Tab. 1 features) fitted on measured whole-layer times:
+    with all seven features, and with the linear layers' terms x6 = sum c and
+    x7 = max c removed."""
+    import torch
+    torch.cuda.set_device(0)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([args.seed, 15])))
+    batches = [(1 + k % 3,) + predictor_batch(rng, 1 + k % 3)
+               for k in range(args.predictor_samples)]
+    timer = LayerTimer([(cs, us) for _, cs, us in batches], args.seed)
+    log(f"[layer-predictor] {len(batches)} batches, pools of {timer.num_pages} pages")
+    rows = time_batches(timer, batches, "layer-predictor")
+    order = np.random.Generator(np.random.PCG64(args.seed)).permutation(len(rows))
+    n_train = int(round(0.7 * len(rows)))
+    train, test = order[:n_train], order[n_train:]
+    res = {"model": "Llama-3-8B decoder layer (ssa_layer_forward), bf16, random weights",
+           "latency": "one layer, us", "samples": len(rows), "train": int(len(train)),
+           "test": int(len(test)), "models": {}}
+    for label, drop in (("all seven features", ()), ("without x6, x7", (5, 6))):
+        rows_d = [dict(r, x=[0.0 if j in drop else v for j, v in enumerate(r["x"])])
+                  for r in rows]
+        p = fit_predictor(rows_d, train, args.predictor_min_scene)
+        entry = {}
+        for split, idx in (("train", train), ("test", test)):
+            for sc, name in ((0, "all"), (1, "pure decode"), (2, "pure prefill"), (3, "mixed")):
+                sel = [i for i in idx if sc == 0 or rows_d[i]["scene"] == sc]
+                y = [rows_d[i]["us"] for i in sel]
+                yh = [p.predict(rows_d[i]["x"], rows_d[i]["scene"]) for i in sel]
+                entry[f"{split}/{name}"] = pred_metrics(y, yh)
+        res["models"][label] = entry
+    if args.layer_predictor:
+        with open(args.layer_predictor, "w") as f:
+            json.dump({"summary": res, "rows": rows}, f)
+    print(json.dumps(res), flush=True)
+
+
 def chunker_state(rng):
     """A scheduler state: 0..256 decodes (u ~ round(LogN(7.2, 1.0)) in
     [16, 16384]), 1..6 waiting prefills in priority order (cached ~ U[0, 8192],
@@ -975,6 +1075,8 @@ def main():
     ap.add_argument("--constructor-states", type=int, default=300)
     ap.add_argument("--layer", metavar="OUT", default=None,
                     help="a Llama-3-8B decoder layer on the library's kernels vs chunk size")
+    ap.add_argument("--layer-predictor", metavar="OUT", default=None,
+                    help="fit Eq. 5 on measured whole-layer times, with and without x6, x7")
     ap.add_argument("--peaks", metavar="OUT", default=None,
                     help="measure the achievable HBM read / copy and bf16 MFMA rates")
     ap.add_argument("--layer-chunks", default=None,
@@ -1006,6 +1108,8 @@ def main():
         main_layer(args)
     elif args.peaks:
         main_peaks(args)
+    elif args.layer_predictor:
+        main_layer_predictor(args)
     else:
         main_bench(args)
 
