@@ -4,11 +4,14 @@
 //
 // ssa_linear: out = x W^T, x [M, K] and W [N, K] bf16, both K-contiguous (the
 // torch Linear layout), fp32 accumulation.
-//  * One workgroup (4 waves, 2 x 2) per 128 x 128 output tile and K range; each
-//    wave owns 64 x 64 = 4 x 4 v_mfma_f32_16x16x32_bf16 tiles, with W as the A
-//    operand (MFMA rows = output columns n) and x as the B operand (MFMA columns
-//    = tokens), so a lane ends with 4 consecutive n of one token: one 8-byte
-//    store per tile.
+//  * One workgroup per output tile and K range.  A tile configuration
+//    (TileCfg) sets the wave grid and each wave's share in
+//    v_mfma_f32_16x16x32_bf16 tiles: 128 x 128 on 2 x 2 waves of 64 x 64,
+//    256 x 256 on 2 x 4 waves of 128 x 64, 64 x 128 on 2 x 2 waves of 32 x 64,
+//    32 x 256 on 1 x 4 waves of 32 x 64.  The host picks one per shape.
+//  * W is the MFMA A operand (MFMA rows = output columns n) and x the B operand
+//    (MFMA columns = tokens), so a lane ends with 4 consecutive n of one token:
+//    one 8-byte store per 16 x 16 tile.
 //  * K blocks of 64 are copied global -> LDS without registers
 //    (global_load_lds_dwordx4) into a ring of STAGES stages, STAGES - 1 blocks
 //    ahead; one barrier per block.  LDS rows are 128 bytes; the 16-byte chunk c
