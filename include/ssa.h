@@ -72,7 +72,7 @@ enum {
   SSA_ERR_HIP = -10,          /* a HIP launch failed */
   SSA_ERR_SCALE = -11,        /* softmax_scale negative or not finite */
   SSA_ERR_TUNING = -12,       /* a tuning field out of range */
-  SSA_ERR_ARG = -13           /* another argument out of range (ssa_predictor.h) */
+  SSA_ERR_ARG = -13           /* another argument out of range (the other headers) */
 };
 
 /* Scene of a batch (Sec. 3.2, Eq. 3).  A batch with no new token is EMPTY. */
