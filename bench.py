@@ -734,16 +734,31 @@ def main_layer_predictor(args):
     print(json.dumps(res), flush=True)
 
 
-def chunker_state(rng):
+# A whole decoder layer takes about 3-5x the attention launch of the same batch
+# (profiles/layer_llama3_8b_vs_chunk.md): the latency bounds of the scheduler
+# states scale by this when each batch runs as a layer (--timer layer).
+LAYER_TIME_SCALE = 4.0
+
+
+def chunker_state(rng, scale=1.0):
     """A scheduler state: 0..256 decodes (u ~ round(LogN(7.2, 1.0)) in
     [16, 16384]), 1..6 waiting prefills in priority order (cached ~ U[0, 8192],
     remaining ~ U[64, 4096]), the server budget B = |D| + 4096 and the window's
-    two latency bounds T_cur, T_next ~ U[60, 400] us."""
+    two latency bounds T_cur, T_next ~ U[60, 400] us (times `scale`)."""
     nd = int(rng.integers(0, 256, endpoint=True))
     dctx = [int(np.clip(np.rint(rng.lognormal(7.2, 1.0)), 16, 16384)) for _ in range(nd)]
     pf = [(int(rng.integers(0, 8192, endpoint=True)), int(rng.integers(64, 4096, endpoint=True)))
           for _ in range(int(rng.integers(1, 6, endpoint=True)))]
-    return dctx, pf, nd + 4096, float(rng.uniform(60, 400)), float(rng.uniform(60, 400))
+    return (dctx, pf, nd + 4096, scale * float(rng.uniform(60, 400)),
+            scale * float(rng.uniform(60, 400)))
+
+
+def timer_of(args, batches):
+    """The GPU work each batch runs as: the fused attention launch (default) or a
+    whole Llama-3-8B decoder layer (--timer layer)."""
+    if args.timer == "layer":
+        return LayerTimer(batches, args.seed)
+    return timer_for(batches, args.seed)
 
 
 def main_chunker(args):
@@ -756,7 +771,8 @@ def main_chunker(args):
     torch.cuda.set_device(0)
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([args.seed, 13])))
     train = [(1 + k % 3,) + predictor_batch(rng, 1 + k % 3) for k in range(args.predictor_samples)]
-    states = [chunker_state(rng) for _ in range(args.chunker_states)]
+    scale = LAYER_TIME_SCALE if args.timer == "layer" else 1.0
+    states = [chunker_state(rng, scale) for _ in range(args.chunker_states)]
 
     def formed(dctx, pf, b, B):
         chunks, _, _ = ssa.form_batch(dctx, pf, b, B)
@@ -766,7 +782,7 @@ def main_chunker(args):
 
     # the largest batch any decision can form: every decode and every prefill in full
     bound = [formed(d, pf, B, B) for d, pf, B, _, _ in states]
-    timer = timer_for([(cs, us) for _, cs, us in train] + [b for b in bound if b[0]], args.seed)
+    timer = timer_of(args, [(cs, us) for _, cs, us in train] + [b for b in bound if b[0]])
     rows = time_batches(timer, train, "chunker: predictor samples")
     pred = fit_predictor(rows, range(len(rows)), args.predictor_min_scene)
     out, t_host = [], []
@@ -796,7 +812,7 @@ def main_chunker(args):
     gap = np.array([(o["window_cost"] - o["window_best"]) / max(o["window_best"], 1e-9)
                     for o in out])
     feasible = np.array([o["b_cur"] > o["decodes"] for o in out])
-    res = {"states": len(out), "predictor_samples": len(rows),
+    res = {"states": len(out), "predictor_samples": len(rows), "timer": args.timer,
            "host_us_per_decision": {"median": round(statistics.median(t_host) * 1e6, 1),
                                     "max": round(max(t_host) * 1e6, 1)},
            "window_cost_gap": {"optimal_fraction": round(float(np.mean(gap <= 1e-12)), 4),
@@ -811,15 +827,15 @@ def main_chunker(args):
     print(json.dumps(res), flush=True)
 
 
-def constructor_state(rng):
+def constructor_state(rng, scale=1.0):
     """A scheduler state with TTFT pressure: 0..128 decodes (u ~ round(LogN(7.2,
     1.0)) in [16, 16384]), 2..10 prefilling or waiting requests (cached ~
     U[0, 4096], remaining ~ U[32, 1024], TTFT slack ~ U[30, 300] us of this
-    path's time, 1 in 10 safeguarded), B = |D| + 4096."""
+    path's time (times `scale`), 1 in 10 safeguarded), B = |D| + 4096."""
     nd = int(rng.integers(0, 128, endpoint=True))
     dctx = [int(np.clip(np.rint(rng.lognormal(7.2, 1.0)), 16, 16384)) for _ in range(nd)]
     cands = [(int(rng.integers(0, 4096, endpoint=True)), int(rng.integers(32, 1024, endpoint=True)),
-              float(rng.uniform(30, 300)), int(rng.random() < 0.1))
+              scale * float(rng.uniform(30, 300)), int(rng.random() < 0.1))
              for _ in range(int(rng.integers(2, 10, endpoint=True)))]
     return dctx, cands, nd + 4096
 
@@ -835,7 +851,8 @@ def main_constructor(args):
     torch.cuda.set_device(0)
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([args.seed, 14])))
     train = [(1 + k % 3,) + predictor_batch(rng, 1 + k % 3) for k in range(args.predictor_samples)]
-    states = [constructor_state(rng) for _ in range(args.constructor_states)]
+    scale = LAYER_TIME_SCALE if args.timer == "layer" else 1.0
+    states = [constructor_state(rng, scale) for _ in range(args.constructor_states)]
     rho, alpha, eps = 20.0, 1.0, 1e-3  # tokens per us of recent throughput; urgency threshold
 
     def batch_of(dctx, cands, take):
@@ -844,7 +861,7 @@ def main_constructor(args):
         return cs, us
 
     bound = [batch_of(d, c, [x[1] for x in c]) for d, c, _ in states]
-    timer = timer_for([(cs, us) for _, cs, us in train] + bound, args.seed)
+    timer = timer_of(args, [(cs, us) for _, cs, us in train] + bound)
     rows = time_batches(timer, train, "constructor: predictor samples")
     pred = fit_predictor(rows, range(len(rows)), args.predictor_min_scene)
     outcomes = {0: 0, 1: 0, 2: 0}
@@ -872,7 +889,7 @@ def main_constructor(args):
                       "candidates": len(sc)})
         if k % 50 == 49:
             log(f"[constructor] {k + 1} states")
-    res = {"states": len(states), "predictor_samples": len(rows),
+    res = {"states": len(states), "predictor_samples": len(rows), "timer": args.timer,
            "outcomes": {"no risk": outcomes[0], "no feasible anchor": outcomes[1],
                         "reconstructed": outcomes[2]},
            "host_us_per_decision": {"median": round(statistics.median(t_host) * 1e6, 1),
@@ -1075,6 +1092,9 @@ def main():
     ap.add_argument("--constructor-states", type=int, default=300)
     ap.add_argument("--layer", metavar="OUT", default=None,
                     help="a Llama-3-8B decoder layer on the library's kernels vs chunk size")
+    ap.add_argument("--timer", choices=["attention", "layer"], default="attention",
+                    help="--chunker / --constructor: run each batch as the fused attention "
+                         "launch or as a whole Llama-3-8B decoder layer")
     ap.add_argument("--layer-predictor", metavar="OUT", default=None,
                     help="fit Eq. 5 on measured whole-layer times, with and without x6, x7")
     ap.add_argument("--peaks", metavar="OUT", default=None,
