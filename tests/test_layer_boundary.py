@@ -50,3 +50,61 @@ def test_rms_norm_rejects_bad_arguments():
     assert LIB.ssa_rms_norm(4, 64, NULL, NULL, f(float("nan")), NULL, NULL) == ssa.SSA_ERR_ARG
     assert LIB.ssa_rms_norm(4, 64, NULL, NULL, f(1e-5), NULL, NULL) == ssa.SSA_ERR_NULL
     assert LIB.ssa_rms_norm(0, 64, NULL, NULL, f(1e-5), NULL, NULL) == ssa.SSA_OK
+
+
+def layer_args(hidden=256, inter=256, max_position=64, q_len=(5, 1), ctx_len=(10, 40)):
+    """A host plan of a small batch and a weights struct of dummy device pointers
+    (validation never dereferences them)."""
+    import numpy as np
+    shape = ssa.make_shape(4, 2, 64, 64, 8, 0.125)
+    plan, _ = ssa.ssa_plan(shape, np.array(q_len, np.int32), np.array(ctx_len, np.int32))
+    fake = ctypes.c_void_p(1 << 40)
+    w = ssa.SsaLayerWeights(fake, fake, fake, fake, fake, fake, fake, hidden, inter,
+                            max_position, 1e-5)
+    return shape, plan, w, fake
+
+
+def forward(shape, plan, w, fake, ws_bytes):
+    return LIB.ssa_layer_forward(ctypes.byref(shape), ctypes.c_void_p(plan.ctypes.data), fake,
+                                 ctypes.byref(w), fake, fake, fake, fake, fake, fake, ws_bytes,
+                                 NULL)
+
+
+def layer_ws(shape, plan, w):
+    out = ctypes.c_size_t(0)
+    rc = LIB.ssa_layer_workspace_size(ctypes.byref(shape), ctypes.c_void_p(plan.ctypes.data),
+                                      ctypes.byref(w), ctypes.byref(out))
+    return rc, out.value
+
+
+def test_layer_workspace_holds_the_activations():
+    shape, plan, w, _ = layer_args()
+    rc, b = layer_ws(shape, plan, w)
+    # 6 tokens: xn, h (hidden), qkv ((4 + 2 * 2) * 64), q and attention out (4 * 64), act
+    assert rc == ssa.SSA_OK and b >= 6 * 2 * (256 * 2 + 512 + 256 * 2 + 256)
+
+
+@pytest.mark.parametrize("hidden,inter", [(200, 256), (8320, 256), (256, 100), (256, 0)])
+def test_layer_rejects_bad_sizes(hidden, inter):
+    shape, plan, w, fake = layer_args(hidden=hidden, inter=inter)
+    assert layer_ws(shape, plan, w)[0] == ssa.SSA_ERR_ARG
+    assert forward(shape, plan, w, fake, 1 << 30) == ssa.SSA_ERR_ARG
+
+
+def test_layer_rejects_positions_past_the_rotary_table_and_a_small_workspace():
+    shape, plan, w, fake = layer_args(max_position=40)  # position 40 needs 41 rows
+    assert forward(shape, plan, w, fake, 1 << 30) == ssa.SSA_ERR_ARG
+    shape, plan, w, fake = layer_args(max_position=41)
+    _, need = layer_ws(shape, plan, w)
+    assert forward(shape, plan, w, fake, need - 1) == ssa.SSA_ERR_WORKSPACE
+
+
+def test_layer_rejects_null_pointers_and_accepts_an_empty_batch():
+    shape, plan, w, fake = layer_args()
+    w.w_down = None
+    assert forward(shape, plan, w, fake, 1 << 30) == ssa.SSA_ERR_NULL
+    # no new tokens: nothing to launch, so no buffer is needed but the plan
+    shape, plan, w, fake = layer_args(q_len=(0, 0))
+    rc = LIB.ssa_layer_forward(ctypes.byref(shape), ctypes.c_void_p(plan.ctypes.data), fake,
+                               ctypes.byref(w), NULL, NULL, NULL, NULL, NULL, NULL, 0, NULL)
+    assert rc == ssa.SSA_OK
