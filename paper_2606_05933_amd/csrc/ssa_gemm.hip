@@ -145,7 +145,11 @@ __global__ __launch_bounds__(C::kThreads, C::OCC) void linear_kernel(GemmArgs a)
   constexpr int TM = C::TM, TN = C::TN, STAGES = C::STAGES, LOADS = C::kLoads;
   constexpr int BM = C::BM, BN = C::BN;
   __shared__ __attribute__((aligned(16))) char lds[STAGES * C::kStage];
-  __shared__ int s_last;
+  // The split reduction's "last arriver" flag shares the ring's first word: it
+  // is written after every wave has drained its copies (vmcnt(0)) and passed a
+  // barrier behind its last ring read.  (A separate word would take the
+  // 192-row tile's two workgroups 8 bytes past the CU's 160 KB.)
+  int& s_last = *reinterpret_cast<int*>(lds);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wm = w / C::NWN, wn = w % C::NWN;
   const int r16 = lane & 15, g = lane >> 4;
@@ -351,7 +355,9 @@ using CfgMid2 = TileCfg<2, 2, 4, 4, 2, 2>;   // 128 x 128, 4 waves of 64 x 64, t
 using CfgBig = TileCfg<2, 4, 8, 4, 2, 1>;    // 256 x 256, 8 waves of 128 x 64
 using CfgM64 = TileCfg<2, 2, 2, 4, 3, 2>;    // 64 x 128, 4 waves of 32 x 64, two per CU
 using CfgTiny = TileCfg<1, 4, 2, 4, 4, 1>;   // 32 x 256: few tokens, weight streaming
-enum { kCfgMid2, kCfgBig, kCfgM64, kCfgTiny, kNumCfgs };
+using CfgM160 = TileCfg<2, 2, 5, 4, 2, 2>;   // 160 x 128, 4 waves of 80 x 64, two per CU
+using CfgM192 = TileCfg<2, 2, 6, 4, 2, 2>;   // 192 x 128, 4 waves of 96 x 64, two per CU
+enum { kCfgMid2, kCfgBig, kCfgM64, kCfgTiny, kCfgM160, kCfgM192, kNumCfgs };
 
 struct CfgShape {
   int bm, bn, occ;
@@ -361,12 +367,15 @@ constexpr CfgShape shape_of() {
   return CfgShape{C::BM, C::BN, C::OCC};
 }
 constexpr CfgShape kCfgShapes[kNumCfgs] = {shape_of<CfgMid2>(), shape_of<CfgBig>(),
-                                           shape_of<CfgM64>(), shape_of<CfgTiny>()};
+                                           shape_of<CfgM64>(),  shape_of<CfgTiny>(),
+                                           shape_of<CfgM160>(), shape_of<CfgM192>()};
 
 struct GemmPlan {
   int cfg, tiles_m, tiles_n, splits, kbps, kblocks;
   size_t tickets, ws;
 };
+
+constexpr int kCus = 256;
 
 // Split K when the tiles alone leave the chip under target_wgs workgroups
 // (at least 4 K blocks per split).  Tiles that overfill the chip by a partial
@@ -401,6 +410,29 @@ GemmPlan split_plan(GemmPlan c, int s) {
   return c;
 }
 
+// Among the 128 x 128, 160 x 128 and 192 x 128 tiles (two workgroups per CU)
+// and 1 or s K splits: the one whose workgroups take the fewest rounds of the
+// chip's 512 slots, counted in rows of tile per split (a last partial round
+// costs about a whole one); splits pay their partials' write and read, about
+// 1.35x on this count (measured on the down projection).  Ties go to the
+// smaller tile.
+GemmPlan fewest_rounds(int m, int n, int k, int max_splits) {
+  GemmPlan best{};
+  double best_cost = 1e30;
+  for (int cfg : {kCfgMid2, kCfgM160, kCfgM192}) {
+    for (int s : {1, max_splits}) {
+      const GemmPlan c = split_plan(gemm_plan(cfg, m, n, k, 1), s);
+      const CfgShape& cs = kCfgShapes[cfg];
+      const int64_t wgs = (int64_t)c.tiles_m * c.tiles_n * c.splits;
+      const int64_t slots = (int64_t)kCus * cs.occ;
+      double cost = (double)((wgs + slots - 1) / slots) * cs.bm / c.splits;
+      if (c.splits > 1) cost *= 1.35;
+      if (cost < best_cost - 1e-9) best_cost = cost, best = c;
+    }
+  }
+  return best;
+}
+
 // Measured on MI355X against the Llama-3-8B projections (N x K = 6144 x 4096,
 // 4096 x 4096, 28672 x 4096, 4096 x 14336) for M = 28 .. 4096, with the
 // weights out of the caches as they are inside a layer (T128 = the number of
@@ -408,14 +440,13 @@ GemmPlan split_plan(GemmPlan c, int s) {
 //  * M <= 64: weight streaming; 32 x 256 tiles, K split to about 128 (long K
 //    and M > 32: 256) workgroups;
 //  * M >= 1536 with at least 192 tiles of 256 x 256: those;
-//  * K > 8192: 64 x 128 tiles when T128 < 96, else 128 x 128 tiles in three
-//    K splits (the down projection: 94 against 198 us unsplit at M = 384, 338
-//    against 360 at M = 2176);
-//  * otherwise 64 x 128 tiles when T128 < 256, else 128 x 128 tiles (at
-//    M = 640: 40 against 60 us for the O projection);
-//  * 64 x 128 tiles are K-split to about 256 workgroups when there are at most
-//    128 of them, and at least in two for K > 8192 (at M = 256 the down
-//    projection's 128 tiles: 108 us unsplit).
+//  * under-filled shapes, T128 < 256 (K > 8192: T128 < 96): 64 x 128 tiles, K-split
+//    to about 256 workgroups when there are at most 128 of them, and at least
+//    in two for K > 8192 (at M = 640: 40 against 60 us for the O projection);
+//  * otherwise fewest_rounds over 128-, 160- and 192-row tiles (1 or 3 K splits
+//    for K > 8192): gate/up at M = 384 102 against 133 us (192 rows), at
+//    M = 640 169 against 194 us (160 rows); the down projection at M = 2176
+//    252 against 342 us (160 rows unsplit).
 GemmPlan choose_plan(int m, int n, int k) {
   const int64_t t128 = (int64_t)((m + 127) / 128) * (n / 128);
   if (n % 256 == 0) {
@@ -428,9 +459,9 @@ GemmPlan choose_plan(int m, int n, int k) {
     const int tiles = c.tiles_m * c.tiles_n;
     return split_plan(c, std::max(min_splits, tiles <= 128 ? (256 + tiles - 1) / tiles : 1));
   };
-  if (k > 8192) return t128 < 96 ? m64(2) : split_plan(gemm_plan(kCfgMid2, m, n, k, 1), 3);
+  if (k > 8192) return t128 < 96 ? m64(2) : fewest_rounds(m, n, k, 3);
   if (t128 < 256) return m64(1);
-  return gemm_plan(kCfgMid2, m, n, k, 1);
+  return fewest_rounds(m, n, k, 1);
 }
 
 template <class C>
@@ -457,6 +488,8 @@ int launch_linear(const GemmPlan& c, int m, int n, int k, int epilogue, const ui
     case kCfgMid2: launch_cfg<CfgMid2>(c, epilogue, a, s); break;
     case kCfgBig: launch_cfg<CfgBig>(c, epilogue, a, s); break;
     case kCfgM64: launch_cfg<CfgM64>(c, epilogue, a, s); break;
+    case kCfgM160: launch_cfg<CfgM160>(c, epilogue, a, s); break;
+    case kCfgM192: launch_cfg<CfgM192>(c, epilogue, a, s); break;
     default: launch_cfg<CfgTiny>(c, epilogue, a, s); break;
   }
   return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;

@@ -47,6 +47,9 @@ CASES = [  # (M, N, K, epilogue)
     (1100, 8192, 256, NONE),       # 576 tiles, 4 K blocks each
     (640, 28672, 4096, SWIGLU),    # 1120 tiles of 128 x 128
     (1152, 28672, 4096, SWIGLU),   # 560 tiles of 256 x 256
+    # where 192-row tiles fit one round of the chip and 128- or 160-row ones do not
+    (370, 28672, 1024, SWIGLU),    # ragged M
+    (384, 28672, 4096, NONE),
 ]
 
 
