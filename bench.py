@@ -958,9 +958,22 @@ def main_layer(args):
         out = torch.empty_like(x)
         ws = torch.zeros(ssa.layer_workspace_size(db.shape, db.plan_host, lw), dtype=torch.uint8,
                          device="cuda")
-        (t_layer,) = time_calls([lambda: ssa.layer_forward(
-            db.shape, db.plan_host, db.plan_dev, lw, x, out, db.k_cache, db.v_cache,
-            db.block_table, ws)], args.steps)
+        def layer():
+            ssa.layer_forward(db.shape, db.plan_host, db.plan_dev, lw, x, out, db.k_cache,
+                              db.v_cache, db.block_table, ws)
+        (t_layer,) = time_calls([layer], args.steps)
+        # the same eight launches captured once in a HIP graph and replayed
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            layer()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            layer()
+        (t_graph,) = time_calls([graph.replay], args.steps)
+        del graph
         # the steps one by one, on buffers of their own
         bf = dict(dtype=torch.bfloat16, device="cuda")
         xn, qkv, q, a, h = (torch.empty((T, n), **bf) for n in (hid, nqkv, qd, qd, hid))
@@ -992,14 +1005,14 @@ def main_layer(args):
         lin = sum(t_steps[k] for k in blas)
         flops = 2 * T * (nqkv * hid + hid * qd + 2 * inter * hid + hid * inter)
         row = {"chunk": c, "tokens": T, "decodes": int((b.q_len == 1).sum()),
-               "layer_us": round(t_layer, 1),
+               "layer_us": round(t_layer, 1), "layer_graph_us": round(t_graph, 1),
                "steps_us": {k: round(v, 1) for k, v in t_steps.items()},
                "linear_us": round(lin, 1), "linear_share": round(lin / sum(t_steps.values()), 3),
                "linear_TFLOPs": round(flops / lin / 1e6, 1),
                "hipblaslt_linear_us": {k: round(v, 1) for k, v in t_blas.items()},
                "hipblaslt_linear_total_us": round(sum(t_blas.values()), 1)}
         rows.append(row)
-        log(f"[layer] c={c} T={T} layer={t_layer:.1f}us linear={lin:.1f}us "
+        log(f"[layer] c={c} T={T} layer={t_layer:.1f}us (graph {t_graph:.1f}us) linear={lin:.1f}us "
             f"(hipBLASLt {sum(t_blas.values()):.1f}us) attention={t_steps['attention']:.1f}us")
         del db, x, out, ws, xn, qkv, q, a, h, act, gws
         torch.cuda.empty_cache()

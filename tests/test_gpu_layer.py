@@ -199,3 +199,57 @@ def test_layer_forward_matches_the_oracle(torch_dev, case):
     pn = np.concatenate([pn, pn], axis=-1)
     assert np.all(kerr <= 2.0 ** -6 * pn[fin] + 2.0 ** -10)
     assert np.all(verr <= 2.0 ** -6 * np.abs(vr[vfin]) + 2.0 ** -10)
+
+
+def test_layer_forward_replays_from_a_hip_graph(torch_dev):
+    """ssa_layer_forward captured in a HIP graph (eight launches, no allocation,
+    no memset) replays to the eager result, bit for bit, with eager work and
+    synchronisations between the replays."""
+    from paper_2606_05933_amd import ssa, workload
+    from paper_2606_05933_amd.device import DeviceBatch
+    torch = torch_dev
+    hidden, inter, hq, hkv, d = 512, 1024, 8, 2, 64
+    cu = [(40, 100), (1, 300), (1, 7), (17, 0)]
+    w = workload.layer_weights(60, hidden, inter, hq, hkv, d)
+    b = workload.make_batch(workload.Shape(hq, hkv, d), [c for c, _ in cu], [u for _, u in cu],
+                            seed=60, spare_pages=5, name="graph")
+    T = b.num_tokens
+    say(f"[gpu layer graph] T={T}")
+    db = DeviceBatch(b)
+    lw = ssa.LayerWeights(w, hq, hkv, d, max_position=400)
+    ws = torch.zeros(ssa.layer_workspace_size(db.shape, db.plan_host, lw), dtype=torch.uint8,
+                     device="cuda")
+    x = torch.from_numpy(workload.normal_bf16((T, hidden), 61).view(np.int16)).cuda().view(
+        torch.bfloat16)
+    out = torch.empty_like(x)
+    kc0, vc0 = db.k_cache.clone(), db.v_cache.clone()
+
+    def layer():
+        ssa.layer_forward(db.shape, db.plan_host, db.plan_dev, lw, x, out, db.k_cache,
+                          db.v_cache, db.block_table, ws)
+
+    layer()
+    torch.cuda.synchronize()
+    eager = out.clone()
+    kc1, vc1 = db.k_cache.clone(), db.v_cache.clone()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        layer()  # warm the stream before capture
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        layer()
+    for k in range(4):
+        out.zero_()
+        db.k_cache.copy_(kc0)
+        db.v_cache.copy_(vc0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), k
+        assert torch.equal(db.k_cache.view(torch.int16), kc1.view(torch.int16)), k
+        assert torch.equal(db.v_cache.view(torch.int16), vc1.view(torch.int16)), k
+        layer()  # eager work between replays
+        torch.cuda.synchronize()
