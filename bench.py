@@ -1038,8 +1038,9 @@ def main_sweep_md(args):
         lines.append(f"### {name}: {DESCR.get(name, name)}\n")
         lines.append("| chunk c | prefix u | scene | tokens | attention us (cold) | attention us (warm) | "
                      "kv_append us | fused us | plan us | step us | tokens/s | decode-only us | "
-                     "chunk-only us | HBM GB/s (% of 8 TB/s) | MFMA TFLOP/s (% of 2.5 PF) |")
-        lines.append("|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|")
+                     "chunk-only us | HBM GB/s (% of 8 TB/s) | MFMA TFLOP/s (% of 2.5 PF) | "
+                     "floor us: overlap / sum | attention / floor (overlap, sum) |")
+        lines.append("|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|")
         for r in rows:
             if r["workload"] != name:
                 continue
@@ -1049,13 +1050,23 @@ def main_sweep_md(args):
             mark = " (config)" if own.get(name) == (r["chunk"], r["prefix"]) else ""
             hbm = r["hbm_GBps"]
             tf = r["mfma_TFLOPs"]
+            # the mixed launch against its floors at the published peaks: perfect
+            # overlap max(bytes / BW, flops / peak), and the sum of the two
+            t_mem = r["decode_bytes"] / (HBM_PEAK_GBS * 1e3)
+            t_mfma = r["chunk_flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e6)
+            f_max, f_sum = max(t_mem, t_mfma), t_mem + t_mfma
+            if f_max < 10.0:  # launch- and latency-bound: fractions mean nothing here
+                frac = "not meaningful"
+            else:
+                frac = f"{f_max / r['attention_us']:.0%}, {f_sum / r['attention_us']:.0%}"
             lines.append(
                 f"| {r['chunk']}{mark} | "
                 f"{r['prefix'] if r['prefix'] is not None else 'drawn'} | {r['scene']} | {r['tokens']} | "
                 f"{r['attention_us']} | {r['attention_warm_us']} | {r['kv_append_us']} | "
                 f"{r.get('fused_us', '')} | {r['plan_us']} | "
                 f"{r['step_us']} | {r['tokens_per_s']:.3g} | {dec} | {chk} | "
-                f"{hbm} ({hbm / HBM_PEAK_GBS:.0%}) | {tf} ({tf / MFMA_BF16_PEAK_TFLOPS:.0%}) |")
+                f"{hbm} ({hbm / HBM_PEAK_GBS:.0%}) | {tf} ({tf / MFMA_BF16_PEAK_TFLOPS:.0%}) | "
+                f"{f_max:.1f} / {f_sum:.1f} | {frac} |")
         lines.append("")
     print("\n".join(lines))
 
