@@ -132,8 +132,9 @@ struct AttnArgs {
   float scale_log2;
   int hq, hkv, G, maxp;
   // fused launch (append workgroups first in the grid): their number, and the
-  // attention items in the grid; 0 for a plain attention launch
-  int append_wgs, num_items;
+  // chunk items in the grid (the only ones that read rows appended in the
+  // launch); 0 for a plain attention launch
+  int append_wgs, num_chunk_items;
   // fused launch: this iteration's new key / value rows ([T, Hkv, D])
   const uint16_t* k_new;
   const uint16_t* v_new;
@@ -161,8 +162,8 @@ __device__ __forceinline__ void st16_dev(void* p, u32x4 v) {
 }
 
 // Workspace words of a fused launch (ahead of the merge tickets): appending
-// workgroups that have finished, attention workgroups that have finished.
-// Both are zero at rest; the last attention workgroup resets them.
+// workgroups that have finished, chunk items that have finished.  Both are
+// zero at rest; the last chunk item to finish resets them.
 constexpr int kCounterAppended = 0, kCounterAttended = 1;
 
 // Wait (a fused launch) until every appending workgroup has published its
@@ -1256,7 +1257,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(const uint8_t* plan
 // is read, at device scope, only after every appending workgroup has counted
 // (they never wait, and workgroups are dispatched in index order, so they all
 // run); a decode item appends its request's one new row itself.  The last
-// attention workgroup resets both counters for the next launch.
+// chunk item to finish resets both counters for the next launch.
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void append_attention_kernel(AttnArgs a, AppendArgs ap) {
   __shared__ __attribute__((aligned(16))) char lds[Cfg<D>::LDS];
@@ -1277,11 +1278,14 @@ __global__ __launch_bounds__(kThreads, 2) void append_attention_kernel(AttnArgs 
       reinterpret_cast<const WorkItem*>(a.plan + a.off_items)[(int)blockIdx.x - a.append_wgs];
   if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
   attention_wg<D, true>(a, it, lds);
+  // Decode items never read the appended rows: only chunk items count, so the
+  // many decode workgroups of a batch end without a device-scope atomic.
+  if (it.kind != kItemChunk) return;
   __syncthreads();
   if (threadIdx.x == 0) {
     const int prev = __hip_atomic_fetch_add(&counters[kCounterAttended], 1, __ATOMIC_RELAXED,
                                             __HIP_MEMORY_SCOPE_AGENT);
-    if (prev == a.num_items - 1) {
+    if (prev == a.num_chunk_items - 1) {
       wait_appended(a);  // no appending workgroup still to count
       __hip_atomic_store(&counters[kCounterAppended], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(&counters[kCounterAttended], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1360,7 +1364,7 @@ int attention_args(const ssa_shape* shape, const void* plan_host, const void* pl
   a->G = h->hq / h->hkv;
   a->maxp = h->max_pages_per_req;
   a->append_wgs = 0;
-  a->num_items = h->num_items;
+  a->num_chunk_items = h->num_chunk_items;
   a->k_new = nullptr;
   a->v_new = nullptr;
   return SSA_OK;
@@ -1410,6 +1414,8 @@ int ssa_append_attention(const ssa_shape* shape, const void* plan_host, const vo
                           workspace, workspace_bytes, &h, &a);
   if (rc || h->num_items == 0) return rc;
   if (h->num_segments > 0 && (!k_new || !v_new)) return SSA_ERR_NULL;
+  // the last chunk item resets the counters: appending workgroups need one
+  if (h->num_chunk_segments > 0 && h->num_chunk_items == 0) return SSA_ERR_PLAN_MISMATCH;
   a.append_wgs = h->num_chunk_segments;
   a.k_new = k_new;
   a.v_new = v_new;
