@@ -93,9 +93,9 @@ def sha256_file(p):
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def time_kernel_events(fn, n, flush=None):
-    """Average duration (s) of n launches of fn (a DeviceBatch launch method),
-    from events that the kernel stamps with its own start and end."""
+def kernel_event_samples(fn, n, flush=None):
+    """Durations (s) of n launches of fn (a DeviceBatch launch method), from
+    events that the kernel stamps with its own start and end."""
     import torch
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(n)]
@@ -107,7 +107,19 @@ def time_kernel_events(fn, n, flush=None):
             flush()
         fn(events=(a, b))
     torch.cuda.synchronize()
-    return statistics.mean(a.elapsed_time(b) for a, b in evs) / 1e3
+    return [a.elapsed_time(b) / 1e3 for a, b in evs]
+
+
+def time_kernel_events(fn, n, flush=None):
+    """Average duration (s) of n launches of fn (see kernel_event_samples)."""
+    return statistics.mean(kernel_event_samples(fn, n, flush))
+
+
+def percentiles_us(samples_s):
+    """Median, 10th and 90th percentile (us) of durations in seconds (nearest rank)."""
+    xs = sorted(x * 1e6 for x in samples_s)
+    pick = lambda q: xs[min(len(xs) - 1, max(0, int(round(q * (len(xs) - 1)))))]
+    return round(statistics.median(xs), 2), round(pick(0.1), 2), round(pick(0.9), 2)
 
 
 class Flusher:
@@ -319,7 +331,9 @@ def main_sweep(args):
             torch.cuda.synchronize()
             n = args.steps
             app = time_kernel_events(db.kv_append, n, flush) * 1e6
-            attn = time_kernel_events(db.attention, n, flush) * 1e6
+            attn_samples = kernel_event_samples(db.attention, n, flush)
+            attn = statistics.mean(attn_samples) * 1e6
+            p50, p10, p90 = percentiles_us(attn_samples)
             fused = time_kernel_events(db.step_fused, n, flush) * 1e6
             warm = time_kernel_events(db.attention, n) * 1e6
             tp = time.perf_counter()
@@ -338,7 +352,9 @@ def main_sweep(args):
             step_us = plan + fused
             row = {"workload": name, "chunk": chunk, "prefix": prefix, "seed": args.seed,
                    "scene": info.scene, "tokens": b.num_tokens,
-                   "attention_us": round(attn, 2), "attention_warm_us": round(warm, 2),
+                   "attention_us": round(attn, 2), "attention_p50_us": p50,
+                   "attention_p10_us": p10, "attention_p90_us": p90,
+                   "attention_warm_us": round(warm, 2),
                    "kv_append_us": round(app, 2), "fused_us": round(fused, 2),
                    "plan_us": round(plan, 2),
                    "step_us": round(step_us, 2),
@@ -1036,11 +1052,12 @@ def main_sweep_md(args):
     lines = []
     for name in workload_names_in(rows):
         lines.append(f"### {name}: {DESCR.get(name, name)}\n")
-        lines.append("| chunk c | prefix u | scene | tokens | attention us (cold) | attention us (warm) | "
+        lines.append("| chunk c | prefix u | scene | tokens | attention us (cold) | "
+                     "cold median [p10, p90] | attention us (warm) | "
                      "kv_append us | fused us | plan us | step us | tokens/s | decode-only us | "
                      "chunk-only us | HBM GB/s (% of 8 TB/s) | MFMA TFLOP/s (% of 2.5 PF) | "
                      "floor us: overlap / sum | attention / floor (overlap, sum) |")
-        lines.append("|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|")
+        lines.append("|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|")
         for r in rows:
             if r["workload"] != name:
                 continue
@@ -1048,6 +1065,8 @@ def main_sweep_md(args):
             dec = segs.get("decode", {}).get("us", "")
             chk = segs.get("chunk", {}).get("us", "")
             mark = " (config)" if own.get(name) == (r["chunk"], r["prefix"]) else ""
+            pct = (f"{r['attention_p50_us']} [{r['attention_p10_us']}, {r['attention_p90_us']}]"
+                   if "attention_p50_us" in r else "")
             hbm = r["hbm_GBps"]
             tf = r["mfma_TFLOPs"]
             # the mixed launch against its floors at the published peaks: perfect
@@ -1062,7 +1081,7 @@ def main_sweep_md(args):
             lines.append(
                 f"| {r['chunk']}{mark} | "
                 f"{r['prefix'] if r['prefix'] is not None else 'drawn'} | {r['scene']} | {r['tokens']} | "
-                f"{r['attention_us']} | {r['attention_warm_us']} | {r['kv_append_us']} | "
+                f"{r['attention_us']} | {pct} | {r['attention_warm_us']} | {r['kv_append_us']} | "
                 f"{r.get('fused_us', '')} | {r['plan_us']} | "
                 f"{r['step_us']} | {r['tokens_per_s']:.3g} | {dec} | {chk} | "
                 f"{hbm} ({hbm / HBM_PEAK_GBS:.0%}) | {tf} ({tf / MFMA_BF16_PEAK_TFLOPS:.0%}) | "
