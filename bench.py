@@ -396,7 +396,8 @@ def hbm_read_probe(gib: int = 4, workgroups: int = 16384, reps: int = 8) -> floa
 
 def main_peaks(args):
     """Achievable peaks of this GPU for the rooflines: HBM read (the library's
-    streaming probe over a 4 GiB buffer, several grid sizes), HBM copy (torch's
+    streaming probe over a 4 GiB buffer, several grid sizes), HBM gather (whole
+    1, 4 and 16 KB chunks of the same buffer in random order), HBM copy (torch's
     device copy of 1 GiB, read + write bytes), and bf16 MFMA (the library's
     register-only v_mfma_f32_16x16x32_bf16 loop, several grid sizes)."""
     import torch
@@ -428,6 +429,28 @@ def main_peaks(args):
             torch.cuda.synchronize()
             best = min(best, a.elapsed_time(b) / 1e3)
         res["mfma_bf16_TFLOPs"][wg] = round(flops / best / 1e12, 1)
+    # gathers of whole chunks in random order over 4 GiB: the decode reads' pattern
+    # (4 KB of one page and kv head per load group); 512 workgroups is the attention
+    # kernel's residency (two per CU)
+    src = torch.ones(1 << 30, dtype=torch.float32, device="cuda")
+    res["hbm_gather_GBps"] = {}
+    for chunk in (1024, 4096, 16384):
+        n = (4 << 30) // chunk
+        idx = torch.randperm(n, device="cuda", dtype=torch.int64).to(torch.int32)
+        for wg in (512, 4096, 16384):
+            out = torch.empty(wg, dtype=torch.int32, device="cuda")
+            best = float("inf")
+            for _ in range(5):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                nbytes = ssa.probe_hbm_gather(src, idx, chunk, out, wg)
+                b.record()
+                torch.cuda.synchronize()
+                best = min(best, a.elapsed_time(b) / 1e3)
+            res["hbm_gather_GBps"][f"{chunk}B_x{wg}"] = round(nbytes / best / 1e9, 1)
+        del idx
+    del src
+    torch.cuda.empty_cache()
     res["hbm_read_best_GBps"] = max(res["hbm_read_GBps"].values())
     res["mfma_bf16_best_TFLOPs"] = max(res["mfma_bf16_TFLOPs"].values())
     res["published"] = {"hbm_GBps": HBM_PEAK_GBS, "mfma_bf16_TFLOPs": MFMA_BF16_PEAK_TFLOPS}

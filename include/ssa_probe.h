@@ -30,6 +30,23 @@ int ssa_probe_hbm_read(const void* src, size_t bytes, uint32_t* out, int32_t wor
                        void* stream);
 
 /*
+ * Gathers whole chunks of `chunk_bytes` (1024, 2048, 4096, 8192 or 16384) from
+ * the device buffer `src` (`src_bytes` long, 16-byte aligned, at least one
+ * chunk): chunk i of the launch is the one at byte chunk_index[i] * chunk_bytes
+ * (chunk_index: n_chunks >= 1 int32 in device memory, read in order; an index
+ * outside [0, src_bytes / chunk_bytes) is clamped into it).  Each wave keeps
+ * 16 KB of 16-byte loads in flight, whole chunks at a time, the pattern of the
+ * attention kernel's decode reads (4 KB of one page and kv head per load
+ * group).  Writes one 32-bit XOR of the data per workgroup to out[workgroups]
+ * (`workgroups` in 1..65536).  Bytes read per launch: n_chunks * chunk_bytes,
+ * plus re-reads of the last chunk that fill the final step of each wave.
+ * Errors: SSA_ERR_ARG, SSA_ERR_NULL, SSA_ERR_HIP.
+ */
+int ssa_probe_hbm_gather(const void* src, size_t src_bytes, const int32_t* chunk_index,
+                         int32_t n_chunks, int32_t chunk_bytes, uint32_t* out, int32_t workgroups,
+                         void* stream);
+
+/*
  * Runs `iters` rounds of 16 independent v_mfma_f32_16x16x32_bf16 chains in
  * each wave of `workgroups` workgroups of 256 threads (iters in 1..2^20,
  * workgroups in 1..65536) on register data, and writes one float per

@@ -1,5 +1,6 @@
-// Probe kernels for gfx950: the achievable HBM read rate and bf16 MFMA rate
-// (include/ssa_probe.h), against which the library's kernels are measured.
+// Probe kernels for gfx950: the achievable HBM read rate (a linear stream and a
+// gather of whole chunks) and bf16 MFMA rate (include/ssa_probe.h), against
+// which the library's kernels are measured.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -33,6 +34,44 @@ __global__ __launch_bounds__(kThreads) void hbm_read_kernel(const u32x4* src, si
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o, 64);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) out[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
+}
+
+// Gather: each wave reads kGatherLoads 1 KB rows per step, made of whole
+// chunks of LPC rows (LPC KB each) at the positions the index array names, in
+// the index array's order (wave w takes chunks w * CPS .., then a grid stride).
+// Indices are clamped into the buffer; past the end of the array a wave
+// re-reads the last chunk, so its step stays whole.
+constexpr int kGatherLoads = 16;  // 16 KB in flight per wave per step
+template <int LPC>
+__global__ __launch_bounds__(kThreads) void hbm_gather_kernel(const uint8_t* src, int64_t src_chunks,
+                                                              const int32_t* index, int32_t n,
+                                                              uint32_t* out) {
+  constexpr int CPS = kGatherLoads / LPC;
+  __shared__ uint32_t part[kThreads / 64];
+  const int lane = threadIdx.x & 63;
+  const int wave = blockIdx.x * (kThreads / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int waves = gridDim.x * (kThreads / 64);
+  u32x4 acc = {0, 0, 0, 0};
+  for (int64_t c0 = (int64_t)wave * CPS; c0 < n; c0 += (int64_t)waves * CPS) {
+    u32x4 v[kGatherLoads];
+#pragma unroll
+    for (int k = 0; k < CPS; ++k) {
+      const int64_t c = c0 + k < n ? c0 + k : n - 1;
+      int64_t id = index[c];
+      id = id < 0 ? 0 : (id >= src_chunks ? src_chunks - 1 : id);
+      const u32x4* row = reinterpret_cast<const u32x4*>(src + id * (LPC * 1024)) + lane;
+#pragma unroll
+      for (int j = 0; j < LPC; ++j) v[k * LPC + j] = __builtin_nontemporal_load(row + j * 64);
+    }
+#pragma unroll
+    for (int j = 0; j < kGatherLoads; ++j) acc ^= v[j];
+  }
+  uint32_t x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o, 64);
+  if (lane == 0) part[threadIdx.x >> 6] = x;
   __syncthreads();
   if (threadIdx.x == 0) out[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
 }
@@ -77,6 +116,31 @@ int ssa_probe_hbm_read(const void* src, size_t bytes, uint32_t* out, int32_t wor
   hipLaunchKernelGGL(hbm_read_kernel, dim3(workgroups), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), static_cast<const u32x4*>(src), bytes / 16,
                      out);
+  return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+}
+
+int ssa_probe_hbm_gather(const void* src, size_t src_bytes, const int32_t* chunk_index,
+                         int32_t n_chunks, int32_t chunk_bytes, uint32_t* out, int32_t workgroups,
+                         void* stream) {
+  if (chunk_bytes != 1024 && chunk_bytes != 2048 && chunk_bytes != 4096 && chunk_bytes != 8192 &&
+      chunk_bytes != 16384)
+    return SSA_ERR_ARG;
+  if (n_chunks < 1 || workgroups < 1 || workgroups > 65536 || src_bytes < (size_t)chunk_bytes)
+    return SSA_ERR_ARG;
+  if (!src || !chunk_index || !out) return SSA_ERR_NULL;
+  if ((uintptr_t)src % 16) return SSA_ERR_ARG;
+  (void)hipGetLastError();
+  const int64_t src_chunks = (int64_t)(src_bytes / (size_t)chunk_bytes);
+  const uint8_t* s = static_cast<const uint8_t*>(src);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const dim3 grid(workgroups), block(kThreads);
+  switch (chunk_bytes) {
+    case 1024: hipLaunchKernelGGL(hbm_gather_kernel<1>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
+    case 2048: hipLaunchKernelGGL(hbm_gather_kernel<2>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
+    case 4096: hipLaunchKernelGGL(hbm_gather_kernel<4>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
+    case 8192: hipLaunchKernelGGL(hbm_gather_kernel<8>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
+    default: hipLaunchKernelGGL(hbm_gather_kernel<16>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
+  }
   return hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
 }
 

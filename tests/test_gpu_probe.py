@@ -1,7 +1,8 @@
 """The probe kernels of include/ssa_probe.h compute what they claim, so that the
 rates measured with them count real work: the read probe's per-workgroup XORs
-combine to the XOR of every word of the buffer (each byte was loaded), and the
-MFMA probe's sum equals the closed form of its MFMA chains."""
+combine to the XOR of every word of the buffer (each byte was loaded), the
+gather probe's to the XOR of exactly the chunks its index names, and the MFMA
+probe's sum equals the closed form of its MFMA chains."""
 import numpy as np
 import pytest
 
@@ -28,6 +29,41 @@ def test_hbm_read_probe_reads_every_word(torch_dev, words, wgs):
     torch.cuda.synchronize()
     got = np.bitwise_xor.reduce(out.cpu().numpy().view(np.uint32))
     assert got == np.bitwise_xor.reduce(host)
+
+
+@pytest.mark.parametrize("chunk_bytes,n,wgs", [(4096, 64, 2), (1024, 512, 3), (16384, 40, 1),
+                                               (2048, 24, 8)])
+def test_hbm_gather_probe_reads_the_named_chunks(torch_dev, chunk_bytes, n, wgs):
+    """Every chunk the index names is read once, an out-of-range index reads the
+    buffer's last chunk, and a wave whose last step runs past the index re-reads
+    the last named chunk: the XOR of the per-workgroup results matches a host
+    model of that schedule."""
+    from paper_2606_05933_amd import ssa
+    torch = torch_dev
+    rng = np.random.default_rng(chunk_bytes + n)
+    src_chunks = n + 5
+    host = rng.integers(0, 2 ** 32, size=src_chunks * chunk_bytes // 4, dtype=np.uint64).astype(
+        np.uint32)
+    index = rng.permutation(src_chunks)[:n].astype(np.int32)
+    index[n // 2] = src_chunks + 100  # clamped to the last chunk of the buffer
+    src = torch.from_numpy(host.view(np.int32)).cuda()
+    idx = torch.from_numpy(index).cuda()
+    out = torch.zeros(wgs, dtype=torch.int32, device="cuda")
+    assert ssa.probe_hbm_gather(src, idx, chunk_bytes, out, wgs) == n * chunk_bytes
+    torch.cuda.synchronize()
+    # host model: wave w reads chunks c0 .. c0 + cps - 1 for c0 = w cps, w cps + waves cps, ...
+    # (a chunk past the end is chunk n - 1 again)
+    cps, waves = 16 // (chunk_bytes // 1024), 4 * wgs
+    words = host.reshape(src_chunks, chunk_bytes // 4)
+    chunk_xor = np.bitwise_xor.reduce(words, axis=1)
+    want = np.uint32(0)
+    for w in range(waves):
+        for c0 in range(w * cps, n, waves * cps):
+            for k in range(cps):
+                c = min(c0 + k, n - 1)
+                want ^= chunk_xor[min(max(int(index[c]), 0), src_chunks - 1)]
+    got = np.bitwise_xor.reduce(out.cpu().numpy().view(np.uint32))
+    assert got == want
 
 
 def test_mfma_probe_matches_the_closed_form(torch_dev):
