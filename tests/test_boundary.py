@@ -307,6 +307,18 @@ def test_launchers_validate_before_any_hip_call():
     nulls = list(args)
     nulls[7] = None  # workspace
     assert L.ssa_append_attention(ctypes.byref(shape), p, fake, *nulls, ws, None, None, None) == -8
+    # In a fused launch the last chunk item resets the counters, so a plan whose chunk
+    # requests have append segments must have chunk items.  A header that says it has none
+    # still passes the plan check (the attention call gets as far as its workspace) but is
+    # refused by the fused call.
+    bad = blob.copy()
+    hdr = bad[:128].view(np.int32)  # int32 7: num_chunk_items
+    assert hdr[7] > 0
+    hdr[7] = 0
+    q = bad.ctypes.data
+    assert L.ssa_mixed_attention(ctypes.byref(shape), q, fake, fake, fake, fake, fake, fake, fake,
+                                 ws - 1, None) == -8
+    assert L.ssa_append_attention(ctypes.byref(shape), q, fake, *args, ws, None, None, None) == -9
 
 
 def test_empty_batch_launches_nothing():
