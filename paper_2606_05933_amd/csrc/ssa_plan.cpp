@@ -43,9 +43,12 @@ constexpr int kOrderChunkFirst = 1;
 constexpr int kOrderInterleave = 2;
 constexpr int kOrderPaired = 3;
 constexpr int kOrderPairedDecodeFirst = 4;
+// automatic order: paired once decode time / chunk time (both estimated) reaches this
+constexpr double kPairedMinRatio = 0.85;
 
 struct Tuning {
   int tile_cols, chunk_split_keys, decode_split_keys, num_cus, num_xcds, mix_order;
+  int auto_order;  // the caller left mix_order at 0: the planner picks it (int: no padding)
 };
 
 int check_shape(const ssa_shape* s) {
@@ -61,7 +64,7 @@ int check_shape(const ssa_shape* s) {
 }
 
 int resolve_tuning(const ssa_tuning* t, Tuning* out) {
-  Tuning r{kDefaultTileCols, 0, 0, kDefaultCus, kDefaultXcds, kOrderChunkFirst};
+  Tuning r{kDefaultTileCols, 0, 0, kDefaultCus, kDefaultXcds, kOrderChunkFirst, 1};
   if (t) {
     if (t->chunk_tile_cols) {
       if (t->chunk_tile_cols != 32 && t->chunk_tile_cols != 64 && t->chunk_tile_cols != 128)
@@ -77,7 +80,10 @@ int resolve_tuning(const ssa_tuning* t, Tuning* out) {
     r.decode_split_keys = t->decode_split_keys;
     if (t->num_cus) r.num_cus = t->num_cus;
     if (t->num_xcds) r.num_xcds = t->num_xcds;
-    if (t->mix_order) r.mix_order = t->mix_order;
+    if (t->mix_order) {
+      r.mix_order = t->mix_order;
+      r.auto_order = 0;
+    }
   }
   *out = r;
   return SSA_OK;
@@ -423,6 +429,19 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   std::vector<uint16_t> bucket(raw.size());
   for (size_t k = 0; k < raw.size(); ++k) bucket[k] = (uint16_t)time_bucket(est_t[k]);
   std::vector<uint32_t> seq;
+  // Automatic launch order.  Pairing a chunk tile with a decode item on every
+  // compute unit pays when the chunk items alone fill both slots of every unit
+  // and the decode part is at least comparable to them.  Measured: about 10%
+  // faster where the estimated decode time (0.7 of the HBM peak) is at least
+  // 0.96 of the chunk time (half the MFMA peak), 4-40% slower at 0.73 and below.
+  if (tu.auto_order) {
+    size_t nchunk = 0;
+    for (const WorkItem& it : raw) nchunk += it.kind == kItemChunk;
+    const double t_dec = in.decode_bytes / kHbmRate;
+    const double t_chk = in.chunk_flops / (kMfmaRatePerCu * tu.num_cus);
+    if (nchunk >= 2 * (size_t)tu.num_cus && t_dec >= kPairedMinRatio * t_chk)
+      tu.mix_order = kOrderPaired;
+  }
   order_items(raw, est_t, bucket, tu, Hkv, &seq);
   p->items.resize(raw.size());
   for (size_t k = 0; k < seq.size(); ++k) {

@@ -199,6 +199,39 @@ def test_scene_and_features_follow_the_paper():
         assert inf.scene == scene
 
 
+def _plan_kinds(name, chunk, tuning=None):
+    """Work-item kinds of a generated workload's plan, in launch order."""
+    from paper_2606_05933_amd import workload
+    b = workload.make_workload(name, seed=0, chunk=chunk)
+    s = b.shape
+    shape = ssa.make_shape(s.hq, s.hkv, s.d, b.num_pages, b.block_table.shape[1],
+                           s.softmax_scale)
+    blob, info = ssa.ssa_plan(shape, b.q_len, b.ctx_len, tuning)
+    hdr = np.frombuffer(blob[:128].tobytes(), dtype=np.int32)
+    off = int(hdr[19])  # off_items
+    items = np.frombuffer(blob[off:off + 48 * info.num_items].tobytes(), np.int32).reshape(-1, 12)
+    return items[:, 0], info
+
+
+def test_automatic_launch_order_pairs_only_decode_heavy_full_chunk_batches():
+    """Left at 0, mix_order pairs chunk and decode items on every unit when the chunk
+    items fill both slots of every unit and the decode part is comparable (l8b at
+    c = 2048); chunk-heavy batches (l70b at c = 1024) and batches with fewer chunk
+    items (l8b at c = 512) keep all chunk items first; an explicit order is kept."""
+    def paired(kinds, info):
+        # paired: the first 256 workgroups are chunk items, the next 256 decode items
+        return bool(info.num_chunk_items >= 512 and (kinds[256:512] != kinds[0]).all()
+                    and (kinds[:256] == kinds[0]).all())
+    k, info = _plan_kinds("l8b", 2048)
+    assert paired(k, info)
+    k, info = _plan_kinds("l8b", 2048, ssa.make_tuning(mix_order=1))
+    assert not paired(k, info) and (k[:512] == k[0]).all()
+    k, info = _plan_kinds("l70b", 1024)
+    assert info.num_chunk_items >= 512 and not paired(k, info)
+    k, info = _plan_kinds("l8b", 512)
+    assert (k[:info.num_chunk_items] == k[0]).all()  # all chunk items first
+
+
 def test_plan_is_deterministic():
     q_len = np.array([300, 1, 1, 1], np.int32)
     ctx_len = np.array([0, 5, 900, 40], np.int32)
