@@ -448,6 +448,16 @@ def main_peaks(args):
                 torch.cuda.synchronize()
                 best = min(best, a.elapsed_time(b) / 1e3)
             res["hbm_gather_GBps"][f"{chunk}B_x{wg}"] = round(nbytes / best / 1e9, 1)
+            if chunk == 4096:  # the same chunks read in the key rows' pattern
+                best = float("inf")
+                for _ in range(5):
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record()
+                    nbytes = ssa.probe_hbm_gather(src, idx, chunk, out, wg, pattern=1)
+                    b.record()
+                    torch.cuda.synchronize()
+                    best = min(best, a.elapsed_time(b) / 1e3)
+                res["hbm_gather_GBps"][f"{chunk}B_keyrows_x{wg}"] = round(nbytes / best / 1e9, 1)
         del idx
     del src
     torch.cuda.empty_cache()

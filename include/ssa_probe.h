@@ -37,14 +37,17 @@ int ssa_probe_hbm_read(const void* src, size_t bytes, uint32_t* out, int32_t wor
  * outside [0, src_bytes / chunk_bytes) is clamped into it).  Each wave keeps
  * 16 KB of 16-byte loads in flight, whole chunks at a time, the pattern of the
  * attention kernel's decode reads (4 KB of one page and kv head per load
- * group).  Writes one 32-bit XOR of the data per workgroup to out[workgroups]
+ * group).  `pattern` 0: each 16-byte load instruction of a wave reads one whole
+ * 1 KB row of the chunk; 1 (4 KB chunks only): it reads 64 B of each of 16
+ * rows of 256 B, the key rows' pattern of the attention kernel's decode loads.
+ * Writes one 32-bit XOR of the data per workgroup to out[workgroups]
  * (`workgroups` in 1..65536).  Bytes read per launch: n_chunks * chunk_bytes,
  * plus re-reads of the last chunk that fill the final step of each wave.
  * Errors: SSA_ERR_ARG, SSA_ERR_NULL, SSA_ERR_HIP.
  */
 int ssa_probe_hbm_gather(const void* src, size_t src_bytes, const int32_t* chunk_index,
-                         int32_t n_chunks, int32_t chunk_bytes, uint32_t* out, int32_t workgroups,
-                         void* stream);
+                         int32_t n_chunks, int32_t chunk_bytes, int32_t pattern, uint32_t* out,
+                         int32_t workgroups, void* stream);
 
 /*
  * Runs `iters` rounds of 16 independent v_mfma_f32_16x16x32_bf16 chains in

@@ -44,7 +44,10 @@ __global__ __launch_bounds__(kThreads) void hbm_read_kernel(const u32x4* src, si
 // Indices are clamped into the buffer; past the end of the array a wave
 // re-reads the last chunk, so its step stays whole.
 constexpr int kGatherLoads = 16;  // 16 KB in flight per wave per step
-template <int LPC>
+// KEY_ROWS (4 KB chunks only): each load instruction reads 64 B of each of 16
+// rows of 256 B instead of one whole 1 KB row, the attention kernel's key-row
+// pattern (lane l: row l % 16, bytes 16 (l / 16) .. of the instruction's 64).
+template <int LPC, bool KEY_ROWS = false>
 __global__ __launch_bounds__(kThreads) void hbm_gather_kernel(const uint8_t* src, int64_t src_chunks,
                                                               const int32_t* index, int32_t n,
                                                               uint32_t* out) {
@@ -61,9 +64,12 @@ __global__ __launch_bounds__(kThreads) void hbm_gather_kernel(const uint8_t* src
       const int64_t c = c0 + k < n ? c0 + k : n - 1;
       int64_t id = index[c];
       id = id < 0 ? 0 : (id >= src_chunks ? src_chunks - 1 : id);
-      const u32x4* row = reinterpret_cast<const u32x4*>(src + id * (LPC * 1024)) + lane;
+      const uint8_t* chunk = src + id * (LPC * 1024);
 #pragma unroll
-      for (int j = 0; j < LPC; ++j) v[k * LPC + j] = __builtin_nontemporal_load(row + j * 64);
+      for (int j = 0; j < LPC; ++j) {
+        const int off = KEY_ROWS ? (lane & 15) * 256 + j * 64 + (lane >> 4) * 16 : j * 1024 + lane * 16;
+        v[k * LPC + j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(chunk + off));
+      }
     }
 #pragma unroll
     for (int j = 0; j < kGatherLoads; ++j) acc ^= v[j];
@@ -120,11 +126,12 @@ int ssa_probe_hbm_read(const void* src, size_t bytes, uint32_t* out, int32_t wor
 }
 
 int ssa_probe_hbm_gather(const void* src, size_t src_bytes, const int32_t* chunk_index,
-                         int32_t n_chunks, int32_t chunk_bytes, uint32_t* out, int32_t workgroups,
-                         void* stream) {
+                         int32_t n_chunks, int32_t chunk_bytes, int32_t pattern, uint32_t* out,
+                         int32_t workgroups, void* stream) {
   if (chunk_bytes != 1024 && chunk_bytes != 2048 && chunk_bytes != 4096 && chunk_bytes != 8192 &&
       chunk_bytes != 16384)
     return SSA_ERR_ARG;
+  if (pattern != 0 && !(pattern == 1 && chunk_bytes == 4096)) return SSA_ERR_ARG;
   if (n_chunks < 1 || workgroups < 1 || workgroups > 65536 || src_bytes < (size_t)chunk_bytes)
     return SSA_ERR_ARG;
   if (!src || !chunk_index || !out) return SSA_ERR_NULL;
@@ -137,7 +144,12 @@ int ssa_probe_hbm_gather(const void* src, size_t src_bytes, const int32_t* chunk
   switch (chunk_bytes) {
     case 1024: hipLaunchKernelGGL(hbm_gather_kernel<1>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
     case 2048: hipLaunchKernelGGL(hbm_gather_kernel<2>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
-    case 4096: hipLaunchKernelGGL(hbm_gather_kernel<4>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
+    case 4096:
+      if (pattern == 1)
+        hipLaunchKernelGGL((hbm_gather_kernel<4, true>), grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out);
+      else
+        hipLaunchKernelGGL(hbm_gather_kernel<4>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out);
+      break;
     case 8192: hipLaunchKernelGGL(hbm_gather_kernel<8>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
     default: hipLaunchKernelGGL(hbm_gather_kernel<16>, grid, block, 0, st, s, src_chunks, chunk_index, n_chunks, out); break;
   }

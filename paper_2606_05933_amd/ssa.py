@@ -164,7 +164,7 @@ def _load():
     lib.ssa_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     lib.ssa_rms_norm.argtypes = [i32, i32, vp, vp, ctypes.c_float, vp, vp]
     lib.ssa_probe_hbm_read.argtypes = [vp, sz, vp, i32, vp]
-    lib.ssa_probe_hbm_gather.argtypes = [vp, sz, vp, i32, i32, vp, i32, vp]
+    lib.ssa_probe_hbm_gather.argtypes = [vp, sz, vp, i32, i32, i32, vp, i32, vp]
     lib.ssa_probe_mfma_bf16.argtypes = [i32, i32, vp, vp]
     lib.ssa_layer_workspace_size.argtypes = [P(SsaShape), vp, P(SsaLayerWeights), P(sz)]
     lib.ssa_layer_forward.argtypes = [P(SsaShape), vp, vp, P(SsaLayerWeights), vp, vp, vp, vp, vp,
@@ -643,15 +643,18 @@ def probe_hbm_read(src, out, workgroups: int, stream=None):
     return nbytes
 
 
-def probe_hbm_gather(src, chunk_index, chunk_bytes: int, out, workgroups: int, stream=None):
+def probe_hbm_gather(src, chunk_index, chunk_bytes: int, out, workgroups: int, stream=None,
+                     pattern: int = 0):
     """ssa_probe_hbm_gather of the chunks chunk_index (int32 device tensor) names
-    in the device tensor src; returns the bytes of the named chunks."""
+    in the device tensor src (pattern 1: the key rows' load pattern, 4 KB
+    chunks); returns the bytes of the named chunks."""
     nbytes = src.numel() * src.element_size()
     _check_dev("chunk_index", chunk_index, chunk_index.numel(), 4)
     _check_dev("out", out, workgroups, 4)
     _check(LIB.ssa_probe_hbm_gather(ctypes.c_void_p(_ptr(src)), ctypes.c_size_t(nbytes),
                                     ctypes.c_void_p(_ptr(chunk_index)), int(chunk_index.numel()),
-                                    int(chunk_bytes), ctypes.c_void_p(_ptr(out)), int(workgroups),
+                                    int(chunk_bytes), int(pattern), ctypes.c_void_p(_ptr(out)),
+                                    int(workgroups),
                                     ctypes.c_void_p(_stream(stream))), "ssa_probe_hbm_gather")
     return chunk_index.numel() * chunk_bytes
 

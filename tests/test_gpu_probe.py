@@ -31,9 +31,10 @@ def test_hbm_read_probe_reads_every_word(torch_dev, words, wgs):
     assert got == np.bitwise_xor.reduce(host)
 
 
-@pytest.mark.parametrize("chunk_bytes,n,wgs", [(4096, 64, 2), (1024, 512, 3), (16384, 40, 1),
-                                               (2048, 24, 8)])
-def test_hbm_gather_probe_reads_the_named_chunks(torch_dev, chunk_bytes, n, wgs):
+@pytest.mark.parametrize("chunk_bytes,n,wgs,pattern", [(4096, 64, 2, 0), (1024, 512, 3, 0),
+                                                       (16384, 40, 1, 0), (2048, 24, 8, 0),
+                                                       (4096, 64, 2, 1), (4096, 100, 3, 1)])
+def test_hbm_gather_probe_reads_the_named_chunks(torch_dev, chunk_bytes, n, wgs, pattern):
     """Every chunk the index names is read once, an out-of-range index reads the
     buffer's last chunk, and a wave whose last step runs past the index re-reads
     the last named chunk: the XOR of the per-workgroup results matches a host
@@ -49,7 +50,7 @@ def test_hbm_gather_probe_reads_the_named_chunks(torch_dev, chunk_bytes, n, wgs)
     src = torch.from_numpy(host.view(np.int32)).cuda()
     idx = torch.from_numpy(index).cuda()
     out = torch.zeros(wgs, dtype=torch.int32, device="cuda")
-    assert ssa.probe_hbm_gather(src, idx, chunk_bytes, out, wgs) == n * chunk_bytes
+    assert ssa.probe_hbm_gather(src, idx, chunk_bytes, out, wgs, pattern=pattern) == n * chunk_bytes
     torch.cuda.synchronize()
     # host model: wave w reads chunks c0 .. c0 + cps - 1 for c0 = w cps, w cps + waves cps, ...
     # (a chunk past the end is chunk n - 1 again)
