@@ -175,6 +175,19 @@ int ssa_plan(const ssa_shape* shape, const int32_t* q_len_host, const int32_t* c
              ssa_plan_info* info);
 
 /*
+ * Optional host-side check of a block table before a launch (pure host code).
+ * The kernels read, for request i, entries block_table[i][0 .. n_i - 1] with
+ * n_i = ceil((u_i + c_i) / P) and take each as a page index without checking
+ * it; an index outside [0, num_pages) would make them read or write outside
+ * the pools.  This call checks exactly those entries of block_table_host
+ * (int32, [num_reqs, max_pages_per_req], a host copy of the table the launch
+ * will use) against the plan's num_pages.  Other entries are not read.
+ * Errors: NULL, the shape errors, PLAN_MISMATCH, PAGES (an entry out of range).
+ */
+int ssa_check_block_table(const ssa_shape* shape, const void* plan_host,
+                          const int32_t* block_table_host);
+
+/*
  * KV append (one kernel): new token j of request i, at position t = u_i + j,
  * is copied bit for bit from k_new/v_new row (q_start_i + j) into page
  * block_table[i][t / P], slot t % P, of k_cache / v_cache.  No other pool

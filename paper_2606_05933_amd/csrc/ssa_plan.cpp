@@ -564,6 +564,22 @@ int ssa_plan_size(const ssa_shape* shape, const int32_t* q_len_host, const int32
   }
 }
 
+int ssa_check_block_table(const ssa_shape* shape, const void* plan_host,
+                          const int32_t* block_table_host) {
+  const ssa::PlanHeader* h = nullptr;
+  int rc = ssa::check_plan(shape, plan_host, &h);
+  if (rc) return rc;
+  if (h->num_reqs > 0 && !block_table_host) return SSA_ERR_NULL;
+  const ssa::ReqEntry* reqs = reinterpret_cast<const ssa::ReqEntry*>(
+      static_cast<const char*>(plan_host) + h->off_reqs);
+  for (int32_t i = 0; i < h->num_reqs; ++i) {
+    const int32_t* row = block_table_host + (size_t)i * h->max_pages_per_req;
+    for (int32_t k = 0; k < reqs[i].n_pages; ++k)
+      if (row[k] < 0 || row[k] >= h->num_pages) return SSA_ERR_PAGES;
+  }
+  return SSA_OK;
+}
+
 int ssa_plan(const ssa_shape* shape, const int32_t* q_len_host, const int32_t* ctx_len_host,
              int32_t num_reqs, const ssa_tuning* tuning, void* plan_host, size_t plan_bytes,
              ssa_plan_info* info) {

@@ -163,6 +163,7 @@ def _load():
     lib.ssa_linear_workspace_size.argtypes = [i32, i32, i32, P(sz)]
     lib.ssa_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     lib.ssa_rms_norm.argtypes = [i32, i32, vp, vp, ctypes.c_float, vp, vp]
+    lib.ssa_check_block_table.argtypes = [P(SsaShape), vp, vp]
     lib.ssa_probe_hbm_read.argtypes = [vp, sz, vp, i32, vp]
     lib.ssa_probe_hbm_gather.argtypes = [vp, sz, vp, i32, i32, i32, vp, i32, vp]
     lib.ssa_probe_mfma_bf16.argtypes = [i32, i32, vp, vp]
@@ -182,7 +183,8 @@ def _load():
 
 LIB = _load()
 
-EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_kv_append",
+EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_check_block_table",
+            "ssa_kv_append",
             "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed",
             "ssa_append_attention", "ssa_predictor_init", "ssa_predictor_add",
             "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
@@ -632,6 +634,14 @@ class LayerWeights:
                                  self.w_gate_up.data_ptr(), self.w_down.data_ptr(),
                                  self.cos_sin.data_ptr(), self.hidden, self.inter,
                                  int(max_position), float(eps))
+
+
+def check_block_table(shape: SsaShape, plan_host, block_table_host) -> None:
+    """ssa_check_block_table on a host copy of the block table (int32 numpy
+    array [num_reqs, max_pages_per_req]); raises SsaError on a bad entry."""
+    bt = np.ascontiguousarray(block_table_host, dtype=np.int32)
+    _check(LIB.ssa_check_block_table(ctypes.byref(shape), ctypes.c_void_p(_ptr(plan_host)),
+                                     ctypes.c_void_p(bt.ctypes.data)), "ssa_check_block_table")
 
 
 def probe_hbm_read(src, out, workgroups: int, stream=None):

@@ -354,6 +354,33 @@ def test_launchers_validate_before_any_hip_call():
     assert L.ssa_append_attention(ctypes.byref(shape), q, fake, *args, ws, None, None, None) == -9
 
 
+def test_block_table_check_covers_exactly_the_entries_the_kernels_read():
+    from paper_2606_05933_amd import workload
+    q_len = np.array([40, 1, 1, 0], np.int32)
+    ctx_len = np.array([5000, 3000, 17, 33], np.int32)
+    b = workload.make_batch(workload.Shape(32, 8, 128), q_len, ctx_len, seed=3)
+    s = b.shape
+    shape = ssa.make_shape(s.hq, s.hkv, s.d, b.num_pages, b.block_table.shape[1], s.softmax_scale)
+    blob, _ = ssa.ssa_plan(shape, q_len, ctx_len, None)
+    bt = b.block_table.copy()
+    ssa.check_block_table(shape, blob, bt)  # the generated table is valid
+    need = (ctx_len + q_len + 15) // 16
+    for i in range(len(q_len)):
+        for bad in (-1, b.num_pages):
+            t = bt.copy()
+            t[i, need[i] - 1] = bad  # the request's last entry that is read
+            with pytest.raises(ssa.SsaError):
+                ssa.check_block_table(shape, blob, t)
+        if need[i] < bt.shape[1]:
+            t = bt.copy()
+            t[i, need[i]:] = -7  # entries past the request's pages are never read
+            ssa.check_block_table(shape, blob, t)
+    assert ssa.LIB.ssa_check_block_table(ctypes.byref(shape), blob.ctypes.data, None) == -1
+    other = shape_of(32, 8, 128, q_len, ctx_len, num_pages=b.num_pages + 1)
+    assert ssa.LIB.ssa_check_block_table(ctypes.byref(other), blob.ctypes.data,
+                                         bt.ctypes.data) == -9
+
+
 def test_empty_batch_launches_nothing():
     shape = ssa.make_shape(8, 2, 64, 10, 1, 0.125)
     blob, info = ssa.ssa_plan(shape, np.zeros(0, np.int32), np.zeros(0, np.int32))
