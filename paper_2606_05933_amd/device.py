@@ -25,15 +25,6 @@ def bits_of(t: torch.Tensor) -> np.ndarray:
     return t.detach().view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def check_block_table(block_table: np.ndarray, q_len, ctx_len, num_pages: int, page: int = 16):
-    """Host-side check that every entry the kernels may read names a real page."""
-    for i, (c, u) in enumerate(zip(q_len, ctx_len)):
-        n = (int(u) + int(c) + page - 1) // page
-        row = block_table[i, :n]
-        if n > block_table.shape[1] or (row < 0).any() or (row >= num_pages).any():
-            raise ValueError(f"block table row {i} names a page outside [0, {num_pages})")
-
-
 class DeviceBatch:
     def __init__(self, b, tuning: ssa.SsaTuning | None = None, device="cuda",
                  plan_on_device: bool = False):
@@ -41,7 +32,6 @@ class DeviceBatch:
         self.plan_on_device = plan_on_device
         self.device = torch.device(device)
         s = b.shape
-        check_block_table(b.block_table, b.q_len, b.ctx_len, b.num_pages, s.page)
         self.shape = ssa.make_shape(s.hq, s.hkv, s.d, b.num_pages, b.max_pages_per_req,
                                     s.softmax_scale, s.page)
         self.tuning = tuning
@@ -83,6 +73,8 @@ class DeviceBatch:
         self._slot = 0
         _, self.info = ssa.ssa_plan(self.shape, b.q_len, b.ctx_len, self.tuning,
                                     out=self._host[0])
+        # every entry the kernels will read names a real page (ssa_check_block_table)
+        ssa.check_block_table(self.shape, self._host[0], b.block_table)
         if self.plan_on_device:
             self._dev[0].copy_(self._host[0])
         self.plan_host, self.plan_dev = self._host[0], self._dev[0]
