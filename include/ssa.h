@@ -140,6 +140,9 @@ typedef struct ssa_tuning {
  *   decode_flops  4*Hq*D*(u+1) summed over the decode set
  *   append_bytes  bytes kv_append reads plus writes: T*Hkv*D*2*2*2
  *   x[0..6]       the paper's batch features x1..x7 (Tab. 1)
+ * A request with c_i = 0 has no new token and runs nothing: it counts in
+ * num_reqs only (not in num_decode_reqs, the features or the scene), as the
+ * scheduler's batch forming leaves it out (ssa_chunker.h).
  */
 typedef struct ssa_plan_info {
   int32_t num_reqs, num_tokens, num_decode_reqs, num_chunk_reqs;

@@ -8,7 +8,7 @@
  * window (T_cur, T_next; Eq. 14-15), choose this iteration's token budget b and
  * the chunk each prefill request gets.
  *
- * Batch forming (the paper's BatchForwarder, "vLLM token allocation"): every
+ * Batch forming (the paper's BatchForwarder, the serving engine's token allocation): every
  * decode request gets one token; the rest of the budget goes to the prefill
  * requests in order, each taking min(its remaining prompt tokens, what is left).
  * The formed batch's features (Tab. 1) and scene (Eq. 3) feed the predictor;
@@ -22,13 +22,17 @@
  * decrease with b; |D| if even that exceeds T).
  *
  * SlidingChunker (Alg. 1): B_cur = TimeToBudget(T_cur), B_next =
- * TimeToBudget(T_next), B_sum = B_cur + B_next; a discrete ternary search over
- * b in [|D|, min(B, B_cur)] for the b that minimises pred(b) + pred(B_sum - b)
- * (Eq. 16), narrowing while the interval is wider than 30; then, of the
- * candidates {lower bound, upper bound, midpoint of the final interval}, the
- * one with the least pred(b) + pred(B_sum - b), ties to the larger budget.
- * The upper bound is capped by B_cur: the printed algorithm searches up to B,
- * which could pick a budget whose own iteration breaks T_cur.
+ * TimeToBudget(T_next), B_sum = B_cur + B_next, and the budget b in
+ * [|D|, min(B, B_cur)] that minimises the window cost pred(b) + pred(B_sum - b)
+ * (Eq. 16), ties to the larger budget.  The paper approximates this argmin with
+ * a discrete ternary search; here it is exact: the window cost is piecewise
+ * quadratic in b (between the budgets where the partially served prefill
+ * request changes, where its chunk crosses 0, 1 or 2 tokens or the largest full
+ * chunk, and where form's clamps act, every Tab. 1 feature is a polynomial of
+ * degree <= 2 in b and the scene is fixed), so each piece's minimum lies at an
+ * end or next to the vertex of its quadratic, and only those budgets are
+ * scored.  The upper bound is capped by B_cur: a budget beyond it would break
+ * this iteration's own bound T_cur.
  *
  * All calls return 0 or a negative SSA_ERR_* code (ssa.h) and write nothing on
  * an error; they allocate nothing.

@@ -23,14 +23,14 @@
  *      set never defined; read as the candidates), and every risky request in
  *      that order is an anchor a:
  *        B_a = TimeToBudget(s_a) (the budget predicted within the anchor's
- *        slack), C_a = min(B, B_a) - |D|; infeasible if C_a <= 0 or r_a > C_a;
+ *        slack), C_a = min(B, B_a) - |D| (Eq. 17); infeasible if C_a <= 0 or r_a > C_a;
  *        S_a = the candidates with s_j >= s_a (a included);
  *        v_j = 1 / (s'_j / sum_{S_a} s' + r_j / sum_{S_a} r) with s' = max(s, eps)
- *        (Eq. 19; slacks of late requests are negative, hence the clamp);
- *        Y = 0/1 knapsack over S_a minus a: most total value within capacity
+ *        (Eq. 18; slacks of late requests are negative, hence the clamp);
+ *        Y = 0/1 knapsack over S_a minus a (Eq. 19): most total value within capacity
  *        C_a - r_a, weights r_j (dynamic programming over integer capacity;
  *        items in C order, a later item replaces an earlier choice only when
- *        strictly better), plus a;
+ *        strictly better), plus a (Eq. 20);
  *        the comparer keeps Y when (|Y|, sum v, sum r) is lexicographically
  *        larger than the best so far (Eq. 21), so the first of equal ones stays.
  *   4. Outcome SSA_CONSTRUCT_BATCH with budget |D| + sum_{Y*} r_j, every chosen

@@ -14,11 +14,18 @@ already in priority order:
   none -> "no risk".  C = candidates by increasing (s, r) (read for the printed
   undefined "sort C"); for each risky anchor a in C order: B_a = TimeToBudget(s_a),
   C_a = min(B, B_a) - |D|, skip if C_a <= 0 or r_a > C_a; S_a = {j in C : s_j >= s_a};
-  v_j = 1 / (s'_j / sum s' + r_j / sum r) over S_a with s' = max(s, eps) (Eq. 19);
-  Y = 0/1 knapsack over S_a \\ {a} within C_a - r_a (Eq. 20), plus a (Eq. 21's set);
+  v_j = 1 / (s'_j / sum s' + r_j / sum r) over S_a with s' = max(s, eps) (Eq. 18);
+  Y = 0/1 knapsack over S_a \\ {a} within C_a - r_a (Eq. 19), plus a (Eq. 20);
   keep Y if (|Y|, sum v, sum r) beats the best so far (Eq. 21, strict).  No
   feasible anchor -> "no anchor".  Otherwise budget |D| + sum r, every chosen
   request given all its remaining tokens (Eq. 22).
+
+Parity unpinned: the third key of Eq. 21 (sum r).  Two anchors with equal slack
+share S_a, Eq. 18's values and their capacity, so they reach the same set; anchors
+with different slack normalise Eq. 18 over different sets, so an exact tie of
+(|Y|, sum v) between different sets needs a numeric coincidence.  No pin state
+with such a tie is known (an exact-arithmetic search of 300,000 small states
+found none), so no test fails when this key is dropped.
 """
 from __future__ import annotations
 

@@ -10,6 +10,7 @@
 //   - append segments for kv_append (new tokens cut at page boundaries);
 //   - the scene of Eq. 3 and the batch features x1..x7 of Tab. 1.
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -37,6 +38,10 @@ constexpr int kMaxChunkSplits = 16;
 // blocks per wave, short enough that long and short contexts balance over the
 // compute units; partial records cost G*(D+2) floats per piece.
 constexpr int kDefaultDecodeSplitKeys = 4096;
+
+// Work items of one launch: their blob section must stay within the int32
+// offsets of the plan header (and the grid within 2^31 workgroups).
+constexpr int64_t kMaxItems = (INT32_MAX - (1 << 20)) / (int64_t)sizeof(WorkItem);
 
 constexpr int kDefaultXcds = 1;
 constexpr int kOrderChunkFirst = 1;
@@ -289,8 +294,12 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
     const int64_t c = q_len[i], u = ctx_len[i];
     p->reqs[i] = ReqEntry{(int32_t)qs, (int32_t)c, (int32_t)u, (int32_t)ceil_div(c + u, P)};
     qs += c;
+    // A request with no new token runs nothing this iteration: it is in no
+    // feature and does not decide the scene (the scheduler's batch forming
+    // leaves it out the same way).
+    if (c == 0) continue;
     in.x[2] += (double)u;
-    if (c <= 1) {
+    if (c == 1) {
       in.num_decode_reqs++;
       in.x[3] += 1;
       in.x[4] += (double)u;
@@ -367,7 +376,14 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   for (int i = 0; i < n; ++i) {
     const int c = q_len[i], u = ctx_len[i];
     if (c > 1) {
-      const int total_cols = c * G;
+      // column n of the request is (token n / G, head n % G); columns and the
+      // item fields that hold them are int32
+      const int64_t total_cols64 = (int64_t)c * G;
+      if (total_cols64 > INT32_MAX) return SSA_ERR_LENGTH;
+      const int total_cols = (int)total_cols64;
+      // at least one item per tile and kv head (splits are checked as they are made)
+      if ((int64_t)raw.size() + ceil_div(total_cols, tu.tile_cols) * Hkv > kMaxItems)
+        return SSA_ERR_LENGTH;
       for (int col0 = 0; col0 < total_cols; col0 += tu.tile_cols) {
         const int ncols = std::min(tu.tile_cols, total_cols - col0);
         const int j_last = (col0 + ncols - 1) / G;
@@ -396,6 +412,7 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
             it.key1 = std::min(kend, (sp + 1) * piece);
             it.group = grp;
             it.split = sp;
+            if ((int64_t)raw.size() >= kMaxItems) return SSA_ERR_LENGTH;
             raw.push_back(it);
             est_t.push_back(4.0 * D * (double)tu.tile_cols * (it.key1 - it.key0) / kMfmaRatePerCu);
           }
@@ -407,6 +424,7 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
       int nsplit = std::max(1, (int)(((int64_t)keys + dec_split / 2) / dec_split));
       const int piece = (int)ceil_div(ceil_div(keys, nsplit), kBlockKeys) * kBlockKeys;
       nsplit = (int)ceil_div(keys, piece);
+      if ((int64_t)raw.size() + (int64_t)nsplit * Hkv > kMaxItems) return SSA_ERR_LENGTH;
       for (int h = 0; h < Hkv; ++h) {
         const int32_t grp = nsplit > 1 ? add_group(nsplit, G) : -1;
         for (int sp = 0; sp < nsplit; ++sp) {
@@ -480,15 +498,23 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   h.num_pages = s->num_pages;
   h.chunk_tile_cols = tu.tile_cols;
   h.softmax_scale = s->softmax_scale;
+  // the blob's section offsets are int32 fields: a plan beyond 2 GiB (or a
+  // grid beyond 2^31 workgroups) is refused
   int64_t off = sizeof(PlanHeader);
-  h.off_reqs = (int32_t)off;
+  const int64_t off_reqs = off;
   off += (int64_t)sizeof(ReqEntry) * n;
-  h.off_items = (int32_t)off;
-  off += (int64_t)sizeof(WorkItem) * p->items.size();
-  h.off_groups = (int32_t)off;
-  off += (int64_t)sizeof(MergeGroup) * p->groups.size();
-  h.off_segments = (int32_t)off;
-  off += (int64_t)sizeof(AppendSeg) * p->segs.size();
+  const int64_t off_items = off;
+  off += (int64_t)sizeof(WorkItem) * (int64_t)p->items.size();
+  const int64_t off_groups = off;
+  off += (int64_t)sizeof(MergeGroup) * (int64_t)p->groups.size();
+  const int64_t off_segments = off;
+  off += (int64_t)sizeof(AppendSeg) * (int64_t)p->segs.size();
+  if (off > INT32_MAX || (int64_t)p->items.size() + (int64_t)p->segs.size() > INT32_MAX)
+    return SSA_ERR_LENGTH;
+  h.off_reqs = (int32_t)off_reqs;
+  h.off_items = (int32_t)off_items;
+  h.off_groups = (int32_t)off_groups;
+  h.off_segments = (int32_t)off_segments;
   h.plan_bytes = off;
   const int64_t tickets = ceil_div(((int64_t)kLaunchCounters + p->groups.size()) * 4, 256) * 256;
   h.ws_partials_off = tickets;
@@ -573,6 +599,7 @@ int ssa_check_block_table(const ssa_shape* shape, const void* plan_host,
   const ssa::ReqEntry* reqs = reinterpret_cast<const ssa::ReqEntry*>(
       static_cast<const char*>(plan_host) + h->off_reqs);
   for (int32_t i = 0; i < h->num_reqs; ++i) {
+    if (reqs[i].q_len == 0) continue;  // no work item or append segment reads this row
     const int32_t* row = block_table_host + (size_t)i * h->max_pages_per_req;
     for (int32_t k = 0; k < reqs[i].n_pages; ++k)
       if (row[k] < 0 || row[k] >= h->num_pages) return SSA_ERR_PAGES;

@@ -149,6 +149,89 @@ std::vector<int> knapsack(const std::vector<int64_t>& w, const std::vector<doubl
   return chosen;
 }
 
+// Eq. 16 over b in [q.nd, hi]: the budget minimising the window cost
+// W(b) = pred(b) + pred(b_sum - b), ties to the larger budget.
+//
+// W is piecewise quadratic in b.  form() hands the budget left after the
+// decodes to the prefill requests in order, so exactly one request is
+// partially served at any budget and its chunk c grows by one per token.
+// While that request is fixed and c stays on one side of the thresholds
+// 0, 1, 2 (not in the batch / decode row / prefill row, Eq. 2) and of the
+// largest full chunk (where x7 = max c switches), every Tab. 1 feature is a
+// polynomial of degree <= 2 in c (x1 = sum c(u + c), x2 = sum c^2) and the
+// scene is fixed, so pred is a fixed quadratic.  The same holds for the
+// second term in b_sum - b, and for the clamps of form() at |D| and B.  The
+// cuts between such pieces are collected below; on every piece the minimum
+// of the quadratic is at an end or next to its vertex, found from three
+// samples.  Every candidate is then scored with the real prediction, so the
+// pick is the exact minimiser up to the rounding of pred itself.
+int window_argmin(const ssa_predictor* p, const Queue& q, int64_t b_sum, int64_t hi,
+                  int64_t* out) {
+  const int64_t lo = q.nd;
+  hi = std::max(hi, lo);
+  // cuts in the budget domain of one pred() term: budget values where a new
+  // piece starts
+  std::vector<int64_t> starts{q.nd, q.nd + 1, q.max_budget, q.max_budget + 1};
+  int64_t before = 0, largest_full = 0;  // tokens of the requests served fully; their max chunk
+  for (int32_t k = 0; k < q.np; ++k) {
+    const int64_t r = q.pf[k].remaining, s0 = q.nd + before;
+    for (int64_t c : {(int64_t)0, (int64_t)1, (int64_t)2, largest_full, largest_full + 1, r, r + 1})
+      if (c >= 0 && c <= r + 1) starts.push_back(s0 + c);
+    before += r;
+    if (r > 1) largest_full = std::max(largest_full, r);
+  }
+  std::vector<int64_t> cuts{lo, hi + 1};
+  for (int64_t s : starts) {
+    cuts.push_back(s);              // first term: b = s
+    cuts.push_back(b_sum - s + 1);  // second term: b_sum - b < s from here on
+    cuts.push_back(b_sum - s);
+  }
+  std::sort(cuts.begin(), cuts.end());
+  cuts.erase(std::unique(cuts.begin(), cuts.end()), cuts.end());
+
+  auto window = [&](int64_t b, double* w) {
+    double t1 = 0.0, t2 = 0.0;
+    int r = pred(p, q, b, &t1);
+    if (!r) r = pred(p, q, b_sum - b, &t2);
+    *w = t1 + t2;
+    return r;
+  };
+  bool have = false;
+  int64_t best = lo;
+  double best_w = 0.0;
+  auto consider = [&](int64_t b) {
+    double w = 0.0;
+    const int r = window(b, &w);
+    if (!r && (!have || w < best_w || (w == best_w && b > best))) {
+      have = true;
+      best = b;
+      best_w = w;
+    }
+    return r;
+  };
+  int rc = SSA_OK;
+  for (size_t i = 0; i + 1 < cuts.size(); ++i) {
+    const int64_t s = std::max(cuts[i], lo), e = std::min(cuts[i + 1] - 1, hi);
+    if (s > e) continue;
+    if ((rc = consider(s)) || (rc = consider(e))) return rc;
+    if (e - s < 2) continue;
+    const int64_t m = s + (e - s) / 2;
+    double ws, wm, we;
+    if ((rc = window(s, &ws)) || (rc = window(m, &wm)) || (rc = window(e, &we))) return rc;
+    // quadratic through the three samples: curvature a, vertex v
+    const double d1 = (wm - ws) / (double)(m - s), d2 = (we - wm) / (double)(e - m);
+    const double a = (d2 - d1) / (double)(e - s);
+    if (!(a > 0.0)) continue;  // linear or concave: the minimum is at an end
+    const double v = 0.5 * ((double)(s + m) - d1 / a);
+    if (!(v > (double)s && v < (double)e)) continue;
+    const int64_t vf = (int64_t)std::floor(v);
+    for (int64_t b = vf - 1; b <= vf + 2; ++b)
+      if (b >= s && b <= e && (rc = consider(b))) return rc;
+  }
+  *out = best;
+  return SSA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -326,39 +409,10 @@ int ssa_sliding_chunker(const ssa_predictor* pred_model, const int32_t* decode_c
   int64_t b_cur = 0, b_next = 0;
   if ((rc = time_to_budget(pred_model, q, t_cur, &b_cur))) return rc;
   if ((rc = time_to_budget(pred_model, q, t_next, &b_next))) return rc;
-  const int64_t b_sum = b_cur + b_next;
-  // window cost of budget b: this iteration plus the next one with the rest
-  auto cost = [&](int64_t b, double* c) {
-    double t1 = 0.0, t2 = 0.0;
-    int r = pred(pred_model, q, b, &t1);
-    if (!r) r = pred(pred_model, q, b_sum - b, &t2);
-    *c = t1 + t2;
-    return r;
-  };
-  int64_t l = n_decode, r = std::min<int64_t>(max_budget, b_cur);
-  const int64_t l0 = l, r0 = r;
-  while (r - l > 30) {
-    const int64_t m1 = l + (r - l) / 3, m2 = r - (r - l) / 3;
-    double c1, c2;
-    if ((rc = cost(m1, &c1)) || (rc = cost(m2, &c2))) return rc;
-    if (c1 <= c2)
-      r = m2 - 1;
-    else
-      l = m1 + 1;
-  }
-  const int64_t cand[3] = {l0, r0, l + (r - l) / 2};
-  int64_t best = l0;
-  double best_cost = 0.0;
-  bool have = false;
-  for (int64_t b : cand) {
-    double c;
-    if ((rc = cost(b, &c))) return rc;
-    if (!have || c < best_cost || (c == best_cost && b > best)) {
-      best = b;
-      best_cost = c;
-      have = true;
-    }
-  }
+  int64_t best = 0;
+  if ((rc = window_argmin(pred_model, q, b_cur + b_next, std::min<int64_t>(max_budget, b_cur),
+                          &best)))
+    return rc;
   double x[SSA_PRED_FEATURES];
   int32_t scene = 0;
   form(q, best, chunk, x, &scene);

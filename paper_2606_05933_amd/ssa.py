@@ -638,8 +638,14 @@ class LayerWeights:
 
 def check_block_table(shape: SsaShape, plan_host, block_table_host) -> None:
     """ssa_check_block_table on a host copy of the block table (int32 numpy
-    array [num_reqs, max_pages_per_req]); raises SsaError on a bad entry."""
+    array [num_reqs, max_pages_per_req]); raises SsaError on a bad entry and
+    ValueError when the array does not have that shape (the library reads
+    num_reqs rows of max_pages_per_req entries)."""
     bt = np.ascontiguousarray(block_table_host, dtype=np.int32)
+    h = _plan_header(plan_host)
+    if bt.ndim != 2 or bt.shape != (h["num_reqs"], shape.max_pages_per_req):
+        raise ValueError(f"block table of shape {bt.shape}, the plan needs "
+                         f"({h['num_reqs']}, {shape.max_pages_per_req})")
     _check(LIB.ssa_check_block_table(ctypes.byref(shape), ctypes.c_void_p(_ptr(plan_host)),
                                      ctypes.c_void_p(bt.ctypes.data)), "ssa_check_block_table")
 

@@ -181,18 +181,20 @@ def test_scene_and_features_follow_the_paper():
     ctx_len = np.array([10, 20, 30, 0, 7], np.int32)
     shape = shape_of(8, 2, 64, q_len, ctx_len)
     _, info = ssa.ssa_plan(shape, q_len, ctx_len)
+    # a request with no new token (c = 0) runs nothing: it is in no feature
     P = q_len > 1
-    Dm = ~P
-    x = [np.sum(q_len[P] * (ctx_len[P] + q_len[P])), np.sum(q_len[P] ** 2), np.sum(ctx_len),
+    Dm = q_len == 1
+    B = q_len > 0
+    x = [np.sum(q_len[P] * (ctx_len[P] + q_len[P])), np.sum(q_len[P] ** 2), np.sum(ctx_len[B]),
          np.sum(Dm), np.sum(ctx_len[Dm]), np.sum(q_len[P]), np.max(q_len[P])]
     assert list(info.x) == [float(v) for v in x]
-    assert info.scene == 3 and info.num_decode_reqs == 3 and info.num_chunk_reqs == 2
+    assert info.scene == 3 and info.num_decode_reqs == 2 and info.num_chunk_reqs == 2
     hq, hkv, d = 8, 2, 64
     cf = sum(4 * hq * d * (c * u + c * (c + 1) / 2) for c, u in zip(q_len[P], ctx_len[P]))
     assert info.chunk_flops == cf
     db = sum((u + 1) * hkv * d * 4 + 2 * hq * d * 2 for c, u in zip(q_len, ctx_len) if c == 1)
     assert info.decode_bytes == db
-    for ql, scene in (([1, 1, 0], 1), ([4, 2], 2), ([0, 0], 0), ([], 0)):
+    for ql, scene in (([1, 1, 0], 1), ([4, 2], 2), ([0, 0], 0), ([], 0), ([4, 0], 2)):
         ql = np.array(ql, np.int32)
         cl = np.zeros_like(ql)
         _, inf = ssa.ssa_plan(shape_of(8, 2, 64, ql, cl), ql, cl)
@@ -355,6 +357,7 @@ def test_launchers_validate_before_any_hip_call():
 
 
 def test_block_table_check_covers_exactly_the_entries_the_kernels_read():
+    # request 3 has no new token: no work item and no append segment reads its row
     from paper_2606_05933_amd import workload
     q_len = np.array([40, 1, 1, 0], np.int32)
     ctx_len = np.array([5000, 3000, 17, 33], np.int32)
@@ -364,8 +367,13 @@ def test_block_table_check_covers_exactly_the_entries_the_kernels_read():
     blob, _ = ssa.ssa_plan(shape, q_len, ctx_len, None)
     bt = b.block_table.copy()
     ssa.check_block_table(shape, blob, bt)  # the generated table is valid
-    need = (ctx_len + q_len + 15) // 16
+    need = np.where(q_len > 0, (ctx_len + q_len + 15) // 16, 0)
     for i in range(len(q_len)):
+        if need[i] == 0:
+            t = bt.copy()
+            t[i, :] = -1  # never read
+            ssa.check_block_table(shape, blob, t)
+            continue
         for bad in (-1, b.num_pages):
             t = bt.copy()
             t[i, need[i] - 1] = bad  # the request's last entry that is read
@@ -376,9 +384,31 @@ def test_block_table_check_covers_exactly_the_entries_the_kernels_read():
             t[i, need[i]:] = -7  # entries past the request's pages are never read
             ssa.check_block_table(shape, blob, t)
     assert ssa.LIB.ssa_check_block_table(ctypes.byref(shape), blob.ctypes.data, None) == -1
+    # the binding refuses a table whose shape the library would read past
+    with pytest.raises(ValueError):
+        ssa.check_block_table(shape, blob, bt[:, :-1])
+    with pytest.raises(ValueError):
+        ssa.check_block_table(shape, blob, bt[:-1])
+
     other = shape_of(32, 8, 128, q_len, ctx_len, num_pages=b.num_pages + 1)
     assert ssa.LIB.ssa_check_block_table(ctypes.byref(other), blob.ctypes.data,
                                          bt.ctypes.data) == -9
+
+
+def test_plan_refuses_sizes_beyond_its_int32_fields():
+    # 2^27 + 1 chunk tokens at G = 16: 2^31 + 16 columns do not fit the items' int32
+    # column fields
+    shape = ssa.make_shape(16, 1, 64, 1 << 20, (1 << 27) // 16 + 2, 0.125)
+    with pytest.raises(ssa.SsaError) as e:
+        ssa.ssa_plan_size(shape, [(1 << 27) + 1], [0])
+    assert e.value.code == -5
+    # a plan blob beyond 2^31 bytes: tiny decode pieces would make over 2^31 / 48
+    # items (refused before they are generated)
+    shape = ssa.make_shape(8, 8, 64, 1 << 20, (1 << 28) // 16 + 1, 0.125)
+    tun = ssa.make_tuning(decode_split_keys=32)
+    with pytest.raises(ssa.SsaError) as e:
+        ssa.ssa_plan_size(shape, [1] * 6, [(1 << 28) - 1] * 6, tun)
+    assert e.value.code == -5
 
 
 def test_empty_batch_launches_nothing():

@@ -1,12 +1,16 @@
 """SlidingChunker and TimeToBudget (Sec. 3.4, Alg. 1, Eq. 14-16).
 
-The oracle (``oracle/chunker.py``, Alg. 1 in the paper's order) is pinned by
-batch forming worked by hand, by brute force (TimeToBudget against a scan of
-every budget; the ternary search against the exact argmin of the window cost),
-and by the B_cur cap.  The library (``ssa_form_batch`` / ``ssa_time_to_budget``
-/ ``ssa_sliding_chunker``) must then take exactly the oracle's decisions: the
-same budget and chunks, the same predicted latency bit for bit, on random
-scheduler states with the same predictor loaded on both sides.  No GPU.
+The oracle (``oracle/chunker.py``: batch forming, TimeToBudget, and Eq. 16's
+argmin over every budget) is pinned by batch forming worked by hand, by
+TimeToBudget against a scan of every budget, by closed forms of the window
+cost (a symmetric convex window splits B_sum evenly, with an exact tie at odd
+B_sum that the larger budget wins; a flat window picks the largest budget) and
+by the B_cur cap.  The library (``ssa_form_batch`` / ``ssa_time_to_budget`` /
+``ssa_sliding_chunker``, an exact piecewise-quadratic search of its own) must
+then reach the oracle's optimum: a window cost no worse than the exhaustive
+minimum, the chunks its budget forms, and the same predicted latency bit for
+bit, on random scheduler states with the same predictor loaded on both sides.
+No GPU.
 """
 import ctypes
 
@@ -73,25 +77,53 @@ def test_time_to_budget_is_the_largest_budget_within_the_limit(seed):
         assert got == (max(fits) if fits else len(dctx))
 
 
-@pytest.mark.parametrize("seed", range(8))
-def test_ternary_search_lands_next_to_the_argmin_of_a_unimodal_window(seed):
-    # only x6 (prefill tokens) and a convex x2 term: pred(b) + pred(S - b) is
-    # convex in b, so Alg. 1's final interval holds the argmin
-    rng = np.random.default_rng(100 + seed)
-    models = {0: [10.0, 0, 2e-5, 0, 0, 0, 1e-2, 0]}
-    dctx = [int(v) for v in rng.integers(1, 4096, size=int(rng.integers(1, 64)))]
-    pf = [(0, int(rng.integers(500, 3000))) for _ in range(int(rng.integers(1, 4)))]
-    B = len(dctx) + 4096
-    b_cur, b_sum, costs = orc.window_costs(models, dctx, pf, B, 120.0, 160.0)
-    best, chunks, t = orc.sliding_chunker(models, dctx, pf, B, 120.0, 160.0)
-    lo_cost = min(costs.values())
-    argmins = [b for b, c in costs.items() if c == lo_cost]
-    # the pick is one of {l0, r0, m}, never worse than the ends, and m lies within
-    # half of the final interval (at most 15) of the minimum
-    assert costs[best] <= costs[len(dctx)] and costs[best] <= costs[min(B, b_cur)]
-    assert best in (len(dctx), min(B, b_cur)) or min(abs(best - a) for a in argmins) <= 16
-    assert chunks == orc.form_batch(dctx, pf, best, B)[0]
-    assert t == orc.pred_budget(models, dctx, pf, best, B)
+@pytest.mark.parametrize("seed", range(4))
+def test_budget_sweep_matches_batch_forming(seed):
+    # the oracle's pred over a whole budget range is the per-budget pred of the
+    # hand-pinned batch forming, bit for bit
+    rng = np.random.default_rng(50 + seed)
+    dctx, pf, B = random_state(rng)
+    budgets = np.arange(0, B + 40)
+    got = orc.preds_over_budgets(MODELS, dctx, pf, budgets, B)
+    ref = [orc.pred_budget(MODELS, dctx, pf, int(b), B) for b in budgets]
+    assert got.tolist() == ref
+
+
+def symmetric_state(b1, b2):
+    """One prefill request with nothing cached, no decodes, and a predictor with
+    only x2 = sum c^2 and x6 = sum c terms: pred(b) = w0 + w2 b^2 + w6 b for
+    b >= 2, so the window cost pred(b) + pred(S - b) is symmetric about S / 2.
+    T_cur and T_next are the predictions at b1 and b2, so B_cur = b1 and
+    B_next = b2 (pred increases with b)."""
+    models = {0: [1.0, 0.0, 1e-5, 0.0, 0.0, 0.0, 1e-3, 0.0]}
+    pf, B = [(0, 6000)], 6000
+    t_cur = orc.pred_budget(models, [], pf, b1, B)
+    t_next = orc.pred_budget(models, [], pf, b2, B)
+    return models, pf, B, t_cur, t_next
+
+
+@pytest.mark.parametrize("b1,b2", [(1001, 500), (1000, 500), (3000, 777), (2500, 2499)])
+def test_symmetric_window_splits_the_sum_evenly_ties_to_the_larger(b1, b2):
+    models, pf, B, t_cur, t_next = symmetric_state(b1, b2)
+    s = b1 + b2
+    best, chunks, _ = orc.sliding_chunker(models, [], pf, B, t_cur, t_next)
+    # even S: S / 2; odd S: (S - 1) / 2 and (S + 1) / 2 cost exactly the same
+    # (the two terms swap), and the larger budget wins
+    assert best == (s + 1) // 2
+    assert chunks == [best]
+    got = ssa.sliding_chunker(library_predictor(models), [], pf, B, t_cur, t_next)
+    assert got[0] == best and got[1] == chunks
+
+
+def test_flat_window_picks_the_largest_budget():
+    # every non-empty batch is predicted at the intercept: the window cost is the
+    # same for every budget (decodes keep both batches non-empty)
+    models = {0: [25.0] + [0.0] * 7}
+    dctx, pf, B = [100, 200, 300], [(0, 50), (7, 900)], 700
+    best, chunks, _ = orc.sliding_chunker(models, dctx, pf, B, 30.0, 30.0)
+    assert best == B and chunks == [50, 647]
+    got = ssa.sliding_chunker(library_predictor(models), dctx, pf, B, 30.0, 30.0)
+    assert got[0] == B and got[1] == chunks
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -109,7 +141,7 @@ def test_chunker_never_exceeds_the_current_window(seed):
 # ----------------------------------------------------- library against oracle
 
 @pytest.mark.parametrize("seed", range(40))
-def test_library_takes_the_oracle_decisions(seed):
+def test_library_reaches_the_oracle_optimum(seed):
     rng = np.random.default_rng(300 + seed)
     dctx, pf, B = random_state(rng)
     p = library_predictor(MODELS)
@@ -119,10 +151,17 @@ def test_library_takes_the_oracle_decisions(seed):
                 tuple(list(v) if isinstance(v, list) else v for v in orc.form_batch(dctx, pf, b, B))
         assert ssa.time_to_budget(p, dctx, pf, B, t_cur) == \
             orc.time_to_budget(MODELS, dctx, pf, B, t_cur)
-        got = ssa.sliding_chunker(p, dctx, pf, B, t_cur, t_next)
+        _, _, budgets, costs = orc.window_costs(MODELS, dctx, pf, B, t_cur, t_next)
         ref = orc.sliding_chunker(MODELS, dctx, pf, B, t_cur, t_next)
-        assert got[0] == ref[0] and got[1] == ref[1]
-        assert got[2] == ref[2]  # same fp64 sum in the same order
+        got = ssa.sliding_chunker(p, dctx, pf, B, t_cur, t_next)
+        assert budgets[0] <= got[0] <= budgets[-1]
+        lo = float(costs.min())
+        mine = float(costs[got[0] - budgets[0]])
+        assert mine <= lo + 1e-9 * max(1.0, abs(lo)), (got[0], ref[0], mine, lo)
+        if np.sum(costs <= lo + 1e-9 * max(1.0, abs(lo))) == 1:
+            assert got[0] == ref[0]
+        assert got[1] == orc.form_batch(dctx, pf, got[0], B)[0]
+        assert got[2] == orc.pred_budget(MODELS, dctx, pf, got[0], B)  # same fp64 sum, same order
 
 
 def test_library_rejects_bad_arguments():
@@ -148,3 +187,22 @@ def test_library_rejects_bad_arguments():
                                  ctypes.byref(b), ch, ctypes.byref(t)) == -13
     assert L.ssa_sliding_chunker(ctypes.byref(p.p), d, 2, pf, 1, 10, 50.0, 50.0,
                                  ctypes.byref(b), ch, None) == 0  # t_pred is optional
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_plan_features_equal_batch_forming(seed):
+    # the predictor is fitted on the planner's features of launched batches and
+    # queried on batch forming's features: one rule for both, c = 0 and c = 1
+    # prefill rows included
+    rng = np.random.default_rng(900 + seed)
+    dctx, pf, B = random_state(rng)
+    pf = pf + [(int(rng.integers(0, 4000)), 1), (int(rng.integers(0, 4000)), 0)]
+    rng.shuffle(pf)
+    for b in (len(dctx), len(dctx) + 1, len(dctx) + 2, (len(dctx) + B) // 2, B):
+        chunks, x, scene = ssa.form_batch(dctx, pf, b, B)
+        q_len = [1] * len(dctx) + list(chunks)
+        ctx = list(dctx) + [c for c, _ in pf]
+        shape = ssa.make_shape(8, 2, 64, 1 << 20, 2048, 0.125)
+        _, info = ssa.ssa_plan(shape, q_len, ctx)
+        assert list(info.x) == list(x)
+        assert info.scene == scene
