@@ -6,15 +6,19 @@ host planning (routing by Eq. 2, work items) into a pinned device-mapped plan
 buffer and one ``ssa_append_attention`` launch (kv_append and the mixed
 attention of all requests in one kernel; the same results, bit for bit, as
 ``ssa_kv_append`` followed by ``ssa_mixed_attention``).  The default
-workload is the Llama-3-8B-shaped mixed batch (32 q / 8 kv heads, D = 128, page
-16; one 512-token chunk on a 2048-token prefix plus 64 decodes with contexts
-uniform in [512, 4096]), synthetic and seeded; inputs are resident in HBM before
-the timed region starts.
+workload is the largest configuration that fits one GPU, the Llama-3-70B-shaped
+layer (64 q / 8 kv heads, D = 128, page 16; one 1024-token chunk on a
+32768-token prefix plus 32 decodes with contexts uniform in [8192, 32768]),
+synthetic and seeded; inputs are resident in HBM before the timed region
+starts.
 
 Printed on stdout, as the last line: one JSON object with the metric (µs per
-iteration), the dominant kernel's roofline (live timing of the fused launch,
-from events the kernel stamps itself, against MI355X's 8 TB/s HBM peak), and
-the CPU oracle timed on this host (a reported baseline, not the target).
+iteration of back-to-back steps), the fused launch's roofline (live timing from
+events the kernel stamps itself; bound by whichever floor is larger, the chunk
+flops at the bf16 MFMA peak or the algorithmic bytes at the HBM peak, with the
+overlap floor and each segment's own fraction beside it), the same launch with
+a cold cache, the Llama-3-8B-shaped line for context, and the CPU oracle timed
+on this host on a bounded sample (a reported baseline, not the target).
 
 Other modes (all single GPU):
   --sweep OUT        latency-vs-chunk-size table of every workload (JSON lines)
@@ -67,7 +71,8 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 TIME_EVERY = 4  # timed steps whose kernel stamps its start and end
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_05933_amd", "csrc", "ssa_kernels.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_append_attention_l8b.json")
+def traffic_file(workload):
+    return os.path.join(ROOT, "profiles", f"traffic_append_attention_{workload}.json")
 
 DESCR = {
     "tiny": "tiny mixed: 8q/8kv/D64, 1 chunk (u=192,c=64) + 4 decodes u in {128,256,384,512}",
@@ -147,39 +152,118 @@ def segment_stats(db, n, flush=None):
             "mfma_frac": round(info.chunk_flops / us / 1e6 / MFMA_BF16_PEAK_TFLOPS, 4)}
 
 
-def cpu_baseline(b, min_seconds=10.0, max_reps=30):
-    """The fp64 oracle (kv_append + attention) of the same batch on this host's cores."""
-    import numpy as np
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_sample(b, stride):
+    """(rows, heads, work of the sample, work of the whole batch): every decode
+    row and every stride-th row of each chunk (its last row included), all q
+    heads; work counts the (query, key) pairs the oracle visits."""
+    starts = np.concatenate([[0], np.cumsum(b.q_len)]).astype(np.int64)
+    rows, work, total = [], 0, 0
+    for i in range(b.num_reqs):
+        c, u = int(b.q_len[i]), int(b.ctx_len[i])
+        total += c * (u + 1) + c * (c - 1) // 2
+        pick = range(c) if c <= 1 else sorted(set(range(0, c, stride)) | {c - 1})
+        for j in pick:
+            rows.append(starts[i] + j)
+            work += u + j + 1
+    hq = b.shape.hq
+    rows = np.repeat(np.array(rows, dtype=np.int64), hq)
+    heads = np.tile(np.arange(hq, dtype=np.int32), len(rows) // hq)
+    return rows, heads, work, total
+
+
+def cpu_baseline(b, target_s=15.0, threads=0):
+    """The fp64 oracle on this host's cores (threads = 0: all the job has): the
+    kv_append scatter into copies of the pools (the copy not timed), then
+    attention of a bounded sample of the batch's rows, scaled to the whole
+    iteration by the (query, key) pairs the oracle visits.  The stride of the
+    sampled chunk rows is chosen from a short calibration run so that the
+    sample takes about target_s seconds."""
     from oracle import oracle
     s = b.shape
-    times, used = [], 0
-    t_start = time.perf_counter()
-    while len(times) < max_reps and (time.perf_counter() - t_start < min_seconds or len(times) < 3):
-        kc = b.k_cache.copy()
-        vc = b.v_cache.copy()
-        t0 = time.perf_counter()
-        oracle.kv_append_inplace(s.hkv, s.d, s.page, b.q_len, b.ctx_len, b.block_table, b.k_new,
-                                 b.v_new, kc, vc)
-        _, used = oracle.attention(s.hq, s.hkv, s.d, s.page, s.softmax_scale, b.q_len, b.ctx_len,
-                                   b.block_table, b.q, kc, vc)
-        times.append(time.perf_counter() - t0)
-        del kc, vc
-    med = statistics.median(times)
-    return {"value": round(med * 1e6, 1), "unit": "us/iter", "cores": int(used), "kind": "oracle",
-            "sample": f"the whole {b.name} iteration (kv_append + attention of all "
-                      f"{b.num_tokens} new tokens), fp64, median of {len(times)} runs",
-            "tokens_per_s": round(b.num_tokens / med, 1)}
+    kc, vc = b.k_cache.copy(), b.v_cache.copy()
+    t0 = time.perf_counter()
+    oracle.kv_append_inplace(s.hkv, s.d, s.page, b.q_len, b.ctx_len, b.block_table, b.k_new,
+                             b.v_new, kc, vc)
+    t_app = time.perf_counter() - t0
+
+    def run(stride):
+        rows, heads, work, total = oracle_sample(b, stride)
+        t = time.perf_counter()
+        _, used = oracle.attention_rows(s.hq, s.hkv, s.d, s.page, s.softmax_scale, b.q_len,
+                                        b.ctx_len, b.block_table, b.q, kc, vc, rows, heads,
+                                        threads=threads)
+        return time.perf_counter() - t, used, work, total, len(rows) // s.hq
+
+    max_c = max(1, int(b.q_len.max())) if b.num_reqs else 1
+    stride = max(1, max_c // 4)
+    dt, used, work, total, nrows = run(stride)  # calibration
+    if work < total and dt < target_s:
+        # chunk-row work scales as 1 / stride; decode rows are always in
+        rate = work / max(dt, 1e-9)
+        stride = max(1, int(stride * (work / rate) / target_s))
+        dt, used, work, total, nrows = run(stride)
+    t_iter = t_app + dt * total / work
+    return {"value": round(t_iter * 1e6, 1), "unit": "us/iter", "cores": int(used),
+            "kind": "oracle", "cpu": cpu_model(),
+            "sample": f"{b.name}: kv_append of all {b.num_tokens} new rows, then attention of "
+                      f"{nrows} of the {b.num_tokens} rows (every decode row, every "
+                      f"{stride}th chunk row and the last), all {s.hq} q heads, fp64, "
+                      f"{dt:.1f} s; scaled by the (query, key) pairs visited ({work} of {total})",
+            "tokens_per_s": round(b.num_tokens / t_iter, 1)}
 
 
-def traffic_bytes():
-    """HBM bytes per fused launch from committed rocprofv3 counter runs, if they
-    were taken on the current kernel source."""
-    if not os.path.exists(TRAFFIC_FILE):
+def traffic_bytes(workload):
+    """HBM bytes per fused launch from committed rocprofv3 counter runs on this
+    workload, if they were taken on the current kernel source."""
+    f = traffic_file(workload)
+    if not os.path.exists(f):
         return None
-    t = json.load(open(TRAFFIC_FILE))
+    t = json.load(open(f))
     if t.get("kernel_source_sha256") != sha256_file(KERNEL_SRC):
         return None
     return (t["fetch_kib"] / t["copy_fetch_factor"] + t["write_kib"] / t["copy_write_factor"]) * 1024
+
+
+def fused_line(db, steps, warmup):
+    """Back-to-back steps (host plan into the free slot + one fused launch):
+    wall time per step, the average fused kernel time from events the kernel
+    stamps itself on every TIME_EVERY-th step, and host time per step."""
+    import torch
+    for _ in range(warmup):
+        db.replan_host()
+        db.step_fused()
+    torch.cuda.synchronize()
+    timed = list(range(0, steps, TIME_EVERY))
+    evs = {i: [torch.cuda.Event(enable_timing=True) for _ in range(2)] for i in timed}
+    for step_evs in evs.values():
+        for e in step_evs:
+            e.record()  # creates the HIP events
+    host_s = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        tp = time.perf_counter()
+        db.replan_host()   # host plan into the other (device-mapped) plan slot
+        if i in evs:
+            db.step_fused(events=(evs[i][0], evs[i][1]))
+        else:
+            db.step_fused()
+        host_s.append(time.perf_counter() - tp)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fused_s = statistics.mean(e[0].elapsed_time(e[1]) for e in evs.values()) / 1e3
+    return wall / steps, fused_s, statistics.mean(host_s)
 
 
 def main_bench(args):
@@ -195,82 +279,89 @@ def main_bench(args):
     log(f"[bench] items={info.num_items} (chunk {info.num_chunk_items}, decode "
         f"{info.num_decode_items}) groups={info.num_merge_groups} scene={info.scene}")
 
-    def step():
-        db.replan_host()
-        db.step_fused()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # The kernel stamps these events itself (start and end of the launch), so
-    # timing adds no packet to the stream.  Every TIME_EVERY-th timed step is
-    # stamped; the others carry only the end stamp that marks their plan slot
-    # free, as a serving loop's iterations do.
-    timed = list(range(0, args.steps, TIME_EVERY))
-    evs = {i: [torch.cuda.Event(enable_timing=True) for _ in range(2)] for i in timed}
-    for step_evs in evs.values():
-        for e in step_evs:
-            e.record()  # creates the HIP events
-    host_s = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        tp = time.perf_counter()
-        db.replan_host()   # host plan into the other (device-mapped) plan slot
-        if i in evs:
-            db.step_fused(events=(evs[i][0], evs[i][1]))
-        else:
-            db.step_fused()
-        host_s.append(time.perf_counter() - tp)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall / args.steps * 1e3
-    fused_s = statistics.mean(e[0].elapsed_time(e[1]) for e in evs.values()) / 1e3
-    # context, after the timed region: the same iteration as two launches
+    # the timed region: K back-to-back steps
+    step_s, fused_s, host_s = fused_line(db, args.steps, args.warmup)
+    assert db.status() == 0, "the fused launch reported an error"
+    # context, after the timed region: the same launch with a cold cache, and the
+    # iteration as two launches
+    flush = Flusher()
+    cold = kernel_event_samples(db.step_fused, 10, flush)
+    cold_p50, cold_p10, cold_p90 = percentiles_us(cold)
     app_s = time_kernel_events(db.kv_append, 20)
     attn_s = time_kernel_events(db.attention, 20)
-    # host cost of planning alone (no copy, no launch)
     tp = time.perf_counter()
     for _ in range(200):
         db._bound[0][0]()
     plan_s = (time.perf_counter() - tp) / 200
-    log(f"[bench] step {ms_per_step * 1e3:.1f} us, fused launch {fused_s * 1e6:.1f} us "
-        f"(as two launches: kv_append {app_s * 1e6:.1f} us, attention {attn_s * 1e6:.1f} us), "
-        f"host per step {statistics.mean(host_s) * 1e6:.1f} us, plan {plan_s * 1e6:.1f} us")
+    log(f"[bench] step {step_s * 1e6:.1f} us, fused launch {fused_s * 1e6:.1f} us warm, "
+        f"{cold_p50:.1f} us cold (as two launches: kv_append {app_s * 1e6:.1f} us, attention "
+        f"{attn_s * 1e6:.1f} us), host per step {host_s * 1e6:.1f} us, plan {plan_s * 1e6:.1f} us")
 
-    # algorithmic bytes: every K/V byte attention reads once, plus the append
-    # (new rows read once and written once)
+    # each segment alone (Eq. 3's pure scenes), cold cache
+    segs = {}
+    for label, keep in (("decode", b.q_len == 1), ("chunk", b.q_len > 1)):
+        if keep.any() and not keep.all():
+            sb = DeviceBatch(workload.sub_batch(b, keep))
+            sb.step()
+            torch.cuda.synchronize()
+            segs[label] = segment_stats(sb, 10, flush)
+            del sb
+            torch.cuda.empty_cache()
+    log("[bench] segments alone (cold): "
+        + ", ".join(f"{k} {v['us']} us" for k, v in segs.items()))
+
+    # roofline of the fused launch: its algorithmic bytes (every K/V byte read
+    # once, the append's rows read and written once) at the HBM peak and its
+    # chunk flops at the bf16 MFMA peak; the larger floor names the bound
     alg_bytes = info.decode_bytes + info.chunk_bytes + info.append_bytes
-    achieved = alg_bytes / fused_s / 1e9
-    tb = traffic_bytes()
-    hbm_read = hbm_read_probe()
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": None if tb is None else round(tb),
-                "kernel": "append_attention", "algorithmic_bytes": round(alg_bytes),
-                "kernel_us": round(fused_s * 1e6, 2),
-                "achievable_peak": round(hbm_read, 1),
-                "frac_of_achievable": round(achieved / hbm_read, 4)}
+    t_hbm = alg_bytes / (HBM_PEAK_GBS * 1e9)
+    t_mfma = info.chunk_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    tb = traffic_bytes(args.workload)
+    if t_mfma > t_hbm:
+        achieved = info.chunk_flops / fused_s / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved, 1),
+                    "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
+    else:
+        achieved = alg_bytes / fused_s / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    floor = max(t_hbm, t_mfma)
+    roofline.update({
+        "traffic": None if tb is None else round(tb),
+        "kernel": "append_attention", "kernel_us": round(fused_s * 1e6, 2),
+        "algorithmic_bytes": round(alg_bytes), "algorithmic_flops": round(info.chunk_flops),
+        "hbm_GBps": round(alg_bytes / fused_s / 1e9, 1),
+        "hbm_frac": round(alg_bytes / fused_s / 1e9 / HBM_PEAK_GBS, 4),
+        "overlap_floor_us": round(floor * 1e6, 2),
+        "frac_of_overlap_floor": round(floor / fused_s, 4),
+        "sum_of_floors_us": round((t_hbm + t_mfma) * 1e6, 2),
+        "chunk_segment_mfma_frac": segs.get("chunk", {}).get("mfma_frac"),
+        "decode_segment_hbm_frac": segs.get("decode", {}).get("hbm_frac"),
+    })
 
+    # the Llama-3-8B-shaped line (the previous headline), back-to-back steps
     extra = {}
-    if args.extras:
-        flush = Flusher()
-        extra["attention_cold_us"] = round(time_kernel_events(db.attention, 20, flush) * 1e6, 2)
-        dec = workload.sub_batch(b, b.q_len == 1)
-        pre = workload.sub_batch(b, b.q_len > 1)
-        dd, dp = DeviceBatch(dec), DeviceBatch(pre)
-        dd.step(), dp.step()
-        torch.cuda.synchronize()
-        extra["pure_decode"] = segment_stats(dd, 20, flush)
-        extra["pure_prefill"] = segment_stats(dp, 20, flush)
-        del dd, dp, flush
+    if args.workload != "l8b" and not args.no_extra_line:
+        del db, flush
+        torch.cuda.empty_cache()
+        b8 = workload.make_workload("l8b", seed=args.seed)
+        d8 = DeviceBatch(b8)
+        s8, f8, _ = fused_line(d8, 20, 5)
+        i8 = d8.info
+        by8 = i8.decode_bytes + i8.chunk_bytes + i8.append_bytes
+        extra["l8b"] = {"workload": DESCR["l8b"], "us_per_iter": round(s8 * 1e6, 2),
+                        "fused_us": round(f8 * 1e6, 2),
+                        "hbm_GBps": round(by8 / f8 / 1e9, 1),
+                        "hbm_frac": round(by8 / f8 / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"[bench] l8b: step {s8 * 1e6:.1f} us, fused {f8 * 1e6:.1f} us")
+        del d8
         torch.cuda.empty_cache()
 
     res = {
-        "metric": METRIC, "value": round(ms_per_step * 1e3, 2), "unit": "us/iter",
+        "metric": METRIC, "value": round(step_s * 1e6, 2), "unit": "us/iter",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5), "higher_is_better": False, "scaling": "weak",
+        "ms_per_step": round(step_s * 1e3, 5), "higher_is_better": False, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) bf16 Q/K/V, seeded random block tables; stands in "
                 "for the paper's ShareGPT/arXiv request mixes)",
@@ -278,17 +369,26 @@ def main_bench(args):
                    "num_tokens": b.num_tokens, "num_reqs": b.num_reqs,
                    "chunk_tokens": int(b.q_len[b.q_len > 1].sum()),
                    "decode_reqs": int((b.q_len == 1).sum())},
-        "tokens_per_s": round(b.num_tokens / (ms_per_step / 1e3), 1),
+        "tokens_per_s": round(b.num_tokens / step_s, 1),
         "fused_us": round(fused_s * 1e6, 2),
+        "fused_cold_us": {"p50": cold_p50, "p10": cold_p10, "p90": cold_p90},
         "two_launch": {"kv_append_us": round(app_s * 1e6, 2), "attention_us": round(attn_s * 1e6, 2)},
         "plan_us": round(plan_s * 1e6, 2),
-        "host_us_per_step": round(statistics.mean(host_s) * 1e6, 2),
+        "host_us_per_step": round(host_s * 1e6, 2),
+        "segments_cold": segs,
         "roofline": roofline,
     }
     res.update(extra)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on this host")
         res["cpu_baseline"] = cpu_baseline(b)
+        # single-thread references on the two small configurations
+        one = {}
+        for name in ("tiny", "l8b"):
+            bs = workload.make_workload(name, seed=args.seed)
+            r = cpu_baseline(bs, target_s=3.0, threads=1)
+            one[name] = {"us_per_iter": r["value"], "sample": r["sample"]}
+        res["cpu_baseline"]["one_thread"] = one
     print(json.dumps(res), flush=True)
 
 
@@ -1137,15 +1237,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="l8b")
+    ap.add_argument("--workload", default="l70b")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--chunk", type=int, default=None)
     ap.add_argument("--prefix", type=int, default=None)
     ap.add_argument("--scene", choices=["mixed", "decode", "prefill"], default="mixed")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extras", action="store_true",
-                    help="also time the attention launch with a cold cache and each segment alone "
-                         "(extra launches of the same kernels on other batches)")
+    ap.add_argument("--no-extra-line", action="store_true",
+                    help="skip the Llama-3-8B-shaped line reported beside the default one")
     ap.add_argument("--sweep", metavar="OUT", default=None)
     ap.add_argument("--sweep-workloads", default=None)
     ap.add_argument("--copy-probe", action="store_true")

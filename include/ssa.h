@@ -118,6 +118,11 @@ typedef struct ssa_shape {
  *                    distinct units, the next num_cus on their second slots),
  *                    4 = as 3, then the other decode items, then the other
  *                    chunk items
+ *   append_wait_polls  ssa_append_attention: polls (about 0.25 us each) before a
+ *                    chunk item's wait for the rows appended in the same launch
+ *                    gives up and sets SSA_STATUS_WAIT_TIMEOUT (default 2^21,
+ *                    about half a second; a test sets a small value to force
+ *                    the time-out from the host)
  */
 typedef struct ssa_tuning {
   int32_t chunk_tile_cols;
@@ -126,7 +131,31 @@ typedef struct ssa_tuning {
   int32_t num_cus;
   int32_t num_xcds;
   int32_t mix_order;
+  int32_t append_wait_polls;
 } ssa_tuning;
+
+/*
+ * Workspace status word.  The int32 at byte SSA_WS_STATUS_OFFSET of the
+ * workspace collects error bits that the kernels of ssa_mixed_attention and
+ * ssa_append_attention set (device-scope atomic OR) and never clear: the
+ * launch still finishes, every workgroup exits, but the outputs it names may
+ * be wrong.  Zero it with the rest of the workspace before first use; read it
+ * (after the launch has completed) to check a launch, and zero it again after
+ * a report.
+ *   SSA_STATUS_WAIT_TIMEOUT   a chunk item of ssa_append_attention gave up
+ *                             waiting for the workgroups that append this
+ *                             launch's rows (the launch ran on, possibly with
+ *                             stale key rows): the in-order dispatch that the
+ *                             fused launch relies on did not hold, or
+ *                             append_wait_polls was too small
+ *   SSA_STATUS_PLAN_MISMATCH  the plan bytes a kernel read at plan_dev do not
+ *                             carry the magic number and hash of plan_host (the
+ *                             device copy is stale or was overwritten): the
+ *                             kernel wrote nothing
+ */
+#define SSA_WS_STATUS_OFFSET 8
+#define SSA_STATUS_WAIT_TIMEOUT 1
+#define SSA_STATUS_PLAN_MISMATCH 2
 
 /*
  * What ssa_plan derived from the batch.  Byte and flop counts are the
@@ -212,8 +241,9 @@ int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* pla
  * ssa_kv_append of the same plan must have run before it on the stream.
  * workspace: device memory of at least the plan's workspace size (never less
  * than 256 bytes), zero-filled by the caller once before its first use; each
- * call leaves its counters at zero again.  Calls that share a workspace must
- * not overlap in time.
+ * call leaves its counters at zero again, and reports errors in the status
+ * word (SSA_WS_STATUS_OFFSET).  Calls that share a workspace must not overlap
+ * in time.
  * Errors: NULL, the shape errors, PLAN_MISMATCH, WORKSPACE, HIP.
  */
 int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const void* plan_dev,

@@ -135,6 +135,7 @@ struct AttnArgs {
   // chunk items in the grid (the only ones that read rows appended in the
   // launch); 0 for a plain attention launch
   int append_wgs, num_chunk_items;
+  int wait_polls;  // polls before the wait for appended rows gives up
   // fused launch: this iteration's new key / value rows ([T, Hkv, D])
   const uint16_t* k_new;
   const uint16_t* v_new;
@@ -163,26 +164,37 @@ __device__ __forceinline__ void st16_dev(void* p, u32x4 v) {
 
 // Workspace words of a fused launch (ahead of the merge tickets): appending
 // workgroups that have finished, chunk items that have finished.  Both are
-// zero at rest; the last chunk item to finish resets them.
+// zero at rest; the last chunk item to finish takes the launch's counts back
+// off them.  Then the status word: sticky error bits (SSA_STATUS_* in ssa.h).
 constexpr int kCounterAppended = 0, kCounterAttended = 1;
+
+__device__ __forceinline__ void report(uint8_t* ws, int bits) {
+  __hip_atomic_fetch_or(reinterpret_cast<int*>(ws) + kWsStatusWord, bits, __ATOMIC_RELAXED,
+                        __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // Wait (a fused launch) until every appending workgroup has published its
 // rows.  They come first in the grid and never wait, and workgroups are
-// dispatched in index order, so the wait ends; the bound (about half a second)
-// is a safety exit.  One lane per wave polls: hundreds of waiting workgroups
-// polling the one counter word with every lane would slow the very stores
-// they wait for.
+// dispatched in index order, so the wait ends.  The bound (about half a second
+// by default) is a safety exit: on it the wait reports SSA_STATUS_WAIT_TIMEOUT
+// and the launch runs on (no hang, possibly stale rows).  One lane per wave
+// polls: hundreds of waiting workgroups polling the one counter word with
+// every lane would slow the very stores they wait for.
 __device__ __forceinline__ void wait_appended(const AttnArgs& a) {
   if (a.append_wgs == 0) return;
   int* counters = reinterpret_cast<int*>(a.ws);
   const int me = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   const int poller = __builtin_amdgcn_readfirstlane(me);
-  for (int spin = 0; spin < (1 << 21); ++spin) {
+  for (int spin = 0;; ++spin) {
     int done = 0;
     if (me == poller)
       done = __hip_atomic_load(&counters[kCounterAppended], __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
     if (__builtin_amdgcn_readfirstlane(done) >= a.append_wgs) break;
+    if (spin >= a.wait_polls) {
+      if (me == poller) report(a.ws, SSA_STATUS_WAIT_TIMEOUT);
+      break;
+    }
     __builtin_amdgcn_s_sleep(8);
   }
 }
@@ -1117,7 +1129,10 @@ __global__ __launch_bounds__(kThreads, 2) void mixed_attention_kernel(AttnArgs a
   // workgroup's item are independent loads.
   const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
   const WorkItem it = reinterpret_cast<const WorkItem*>(a.plan + a.off_items)[blockIdx.x];
-  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
+  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) {
+    if (threadIdx.x == 0) report(a.ws, SSA_STATUS_PLAN_MISMATCH);
+    return;
+  }
   attention_wg<D, false>(a, it, lds);
 }
 
@@ -1265,7 +1280,10 @@ __global__ __launch_bounds__(kThreads, 2) void append_attention_kernel(AttnArgs 
   int* counters = reinterpret_cast<int*>(a.ws);
   if ((int)blockIdx.x < a.append_wgs) {
     const AppendSeg sg = reinterpret_cast<const AppendSeg*>(a.plan + ap.off_segments)[blockIdx.x];
-    if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
+    if (hdr->magic != kPlanMagic || hdr->hash != a.hash) {
+      if (threadIdx.x == 0) report(a.ws, SSA_STATUS_PLAN_MISMATCH);
+      return;
+    }
     append_segment_staged<D>(ap, sg, a.bt, a.hkv, a.maxp, lds);
     vm_wait<0>();  // this thread's device-scope stores have completed
     __syncthreads();
@@ -1276,7 +1294,10 @@ __global__ __launch_bounds__(kThreads, 2) void append_attention_kernel(AttnArgs 
   }
   const WorkItem it =
       reinterpret_cast<const WorkItem*>(a.plan + a.off_items)[(int)blockIdx.x - a.append_wgs];
-  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) return;
+  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) {
+    if (threadIdx.x == 0) report(a.ws, SSA_STATUS_PLAN_MISMATCH);
+    return;
+  }
   attention_wg<D, true>(a, it, lds);
   // Decode items never read the appended rows: only chunk items count, so the
   // many decode workgroups of a batch end without a device-scope atomic.
@@ -1286,9 +1307,14 @@ __global__ __launch_bounds__(kThreads, 2) void append_attention_kernel(AttnArgs 
     const int prev = __hip_atomic_fetch_add(&counters[kCounterAttended], 1, __ATOMIC_RELAXED,
                                             __HIP_MEMORY_SCOPE_AGENT);
     if (prev == a.num_chunk_items - 1) {
-      wait_appended(a);  // no appending workgroup still to count
-      __hip_atomic_store(&counters[kCounterAppended], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&counters[kCounterAttended], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // Take this launch's counts back off the counters: subtraction (not a
+      // store of zero) returns them to their values at launch whatever the
+      // timing, even if an appending workgroup counts after a timed-out wait.
+      wait_appended(a);
+      __hip_atomic_fetch_sub(&counters[kCounterAppended], a.append_wgs, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_sub(&counters[kCounterAttended], a.num_chunk_items, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -1365,6 +1391,7 @@ int attention_args(const ssa_shape* shape, const void* plan_host, const void* pl
   a->maxp = h->max_pages_per_req;
   a->append_wgs = 0;
   a->num_chunk_items = h->num_chunk_items;
+  a->wait_polls = h->wait_polls;
   a->k_new = nullptr;
   a->v_new = nullptr;
   return SSA_OK;

@@ -52,7 +52,7 @@ constexpr int kOrderPairedDecodeFirst = 4;
 constexpr double kPairedMinRatio = 0.85;
 
 struct Tuning {
-  int tile_cols, chunk_split_keys, decode_split_keys, num_cus, num_xcds, mix_order;
+  int tile_cols, chunk_split_keys, decode_split_keys, num_cus, num_xcds, mix_order, wait_polls;
   int auto_order;  // the caller left mix_order at 0: the planner picks it (int: no padding)
 };
 
@@ -69,7 +69,7 @@ int check_shape(const ssa_shape* s) {
 }
 
 int resolve_tuning(const ssa_tuning* t, Tuning* out) {
-  Tuning r{kDefaultTileCols, 0, 0, kDefaultCus, kDefaultXcds, kOrderChunkFirst, 1};
+  Tuning r{kDefaultTileCols, 0, 0, kDefaultCus, kDefaultXcds, kOrderChunkFirst, kDefaultWaitPolls, 1};
   if (t) {
     if (t->chunk_tile_cols) {
       if (t->chunk_tile_cols != 32 && t->chunk_tile_cols != 64 && t->chunk_tile_cols != 128)
@@ -81,6 +81,8 @@ int resolve_tuning(const ssa_tuning* t, Tuning* out) {
     if (t->num_cus < 0 || t->num_cus > 4096) return SSA_ERR_TUNING;
     if (t->num_xcds < 0 || t->num_xcds > 64) return SSA_ERR_TUNING;
     if (t->mix_order < 0 || t->mix_order > 4) return SSA_ERR_TUNING;
+    if (t->append_wait_polls < 0) return SSA_ERR_TUNING;
+    if (t->append_wait_polls) r.wait_polls = t->append_wait_polls;
     r.chunk_split_keys = t->chunk_split_keys;
     r.decode_split_keys = t->decode_split_keys;
     if (t->num_cus) r.num_cus = t->num_cus;
@@ -498,6 +500,7 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   h.num_pages = s->num_pages;
   h.chunk_tile_cols = tu.tile_cols;
   h.softmax_scale = s->softmax_scale;
+  h.wait_polls = tu.wait_polls;
   // the blob's section offsets are int32 fields: a plan beyond 2 GiB (or a
   // grid beyond 2^31 workgroups) is refused
   int64_t off = sizeof(PlanHeader);

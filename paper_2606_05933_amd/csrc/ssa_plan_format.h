@@ -5,8 +5,9 @@
 //   [PlanHeader 128 B][ReqEntry x num_reqs][WorkItem x num_items]
 //   [MergeGroup x num_groups][AppendSeg x num_segments]
 //
-// The workspace holds kLaunchCounters int32 words for a fused launch and one
-// int32 ticket per merge group (all zero at rest), padded to 256 bytes, then,
+// The workspace holds kLaunchCounters int32 words (a fused launch's two
+// counters, the sticky status word of ssa.h, one spare) and one int32 ticket
+// per merge group (counters and tickets zero at rest), padded to 256 bytes, then,
 // at ws_partials_off, fp32 partial results:
 // for merge group g and split s, a record of ncols * (D + 2) floats at float
 // offset ws_off + s * ncols * (D + 2): m[ncols], l[ncols], o[ncols][D].
@@ -16,12 +17,14 @@
 namespace ssa {
 
 constexpr uint32_t kPlanMagic = 0x31415353u;  // "SSA1"
-constexpr uint32_t kPlanVersion = 2;
+constexpr uint32_t kPlanVersion = 3;
 constexpr int kBlockKeys = 32;  // keys per attention block: two 16-slot pages
 constexpr int kWaves = 4;       // waves per workgroup
 constexpr int kThreads = 256;   // threads per workgroup
 constexpr int kChunkWaveCols = 32;  // columns a wave owns in a chunk tile
-constexpr int kLaunchCounters = 2;  // workspace words ahead of the merge tickets
+constexpr int kLaunchCounters = 4;  // workspace words ahead of the merge tickets
+constexpr int kWsStatusWord = 2;    // the status word among them (ssa.h)
+constexpr int kDefaultWaitPolls = 1 << 21;
 
 enum ItemKind : int32_t { kItemChunk = 0, kItemDecode = 1 };
 
@@ -39,7 +42,8 @@ struct PlanHeader {
   int64_t plan_bytes;       // total blob size
   float softmax_scale;
   int32_t num_chunk_segments;  // segments of chunk requests (c > 1): the first ones
-  int32_t reserved[2];
+  int32_t wait_polls;          // polls before a fused launch's wait for appended rows gives up
+  int32_t reserved;
 };
 static_assert(sizeof(PlanHeader) == 128, "plan header size");
 

@@ -148,5 +148,22 @@ class DeviceBatch:
         self._bound[self._slot][3](start, stop)
         self._done[self._slot] = stop
 
+    def status(self) -> int:
+        """The workspace's status word (ssa.h: SSA_STATUS_* bits) after the
+        launches issued so far have completed."""
+        torch.cuda.synchronize(self.device)
+        o = ssa.SSA_WS_STATUS_OFFSET
+        return int(self.workspace[o:o + 4].view(torch.int32).item())
+
+    def clear_status(self):
+        o = ssa.SSA_WS_STATUS_OFFSET
+        self.workspace[o:o + 4].zero_()
+
+    def launch_words(self) -> np.ndarray:
+        """The fused launch's counters, the status word and the merge tickets
+        (int32, host copy): every word but the status is zero at rest."""
+        n = ssa.WS_LAUNCH_WORDS + self.info.num_merge_groups
+        return self.workspace[:4 * n].view(torch.int32).cpu().numpy()
+
     def out_f32(self) -> np.ndarray:
         return self.out.float().cpu().numpy()

@@ -22,6 +22,11 @@ LIB_PATH = os.path.join(_HERE, "libssa.so")
 
 SSA_OK = 0
 SSA_ERR_NULL, SSA_ERR_WORKSPACE, SSA_ERR_HIP, SSA_ERR_ARG = -1, -8, -10, -13
+# the workspace's status word (ssa.h): byte offset and error bits
+SSA_WS_STATUS_OFFSET = 8
+SSA_STATUS_WAIT_TIMEOUT, SSA_STATUS_PLAN_MISMATCH = 1, 2
+# workspace words ahead of the merge tickets (two counters, the status word, one spare)
+WS_LAUNCH_WORDS = 4
 SCENES = {0: "empty", 1: "pure decode", 2: "pure prefill", 3: "mixed"}
 
 
@@ -41,7 +46,8 @@ class SsaShape(ctypes.Structure):
 class SsaTuning(ctypes.Structure):
     _fields_ = [("chunk_tile_cols", ctypes.c_int32), ("chunk_split_keys", ctypes.c_int32),
                 ("decode_split_keys", ctypes.c_int32), ("num_cus", ctypes.c_int32),
-                ("num_xcds", ctypes.c_int32), ("mix_order", ctypes.c_int32)]
+                ("num_xcds", ctypes.c_int32), ("mix_order", ctypes.c_int32),
+                ("append_wait_polls", ctypes.c_int32)]
 
 
 PRED_FEATURES, PRED_MODELS, PRED_MOMENTS = 7, 4, 45
@@ -327,9 +333,9 @@ def make_shape(hq, hkv, d, num_pages, max_pages_per_req, scale, page_size=16) ->
 
 
 def make_tuning(chunk_tile_cols=0, chunk_split_keys=0, decode_split_keys=0, num_cus=0,
-                num_xcds=0, mix_order=0):
+                num_xcds=0, mix_order=0, append_wait_polls=0):
     return SsaTuning(int(chunk_tile_cols), int(chunk_split_keys), int(decode_split_keys),
-                     int(num_cus), int(num_xcds), int(mix_order))
+                     int(num_cus), int(num_xcds), int(mix_order), int(append_wait_polls))
 
 
 def _lens(a):

@@ -60,6 +60,7 @@ def full_parity(b, tuning=None, plan_on_device=False):
     assert np.array_equal(bits_of(db.v_cache).reshape(vc.shape), vc), "V pool image differs"
     ref, _ = oracle.batch_attention(b, kc, vc)
     assert_close(db.out_f32(), ref, b.name)
+    assert db.status() == 0, f"status word {db.status()}"
     return db
 
 
@@ -85,6 +86,26 @@ SMALL = [
     (8, 8, 64, [(2048, 0), (1, 1)]),                                  # long chunk from empty
     (32, 8, 128, [(1, 65535), (1, 12287), (40, 20000)]),              # many decode pieces
 ]
+
+
+def test_repeat_launches_are_bitwise_identical_and_reset_tickets(torch_dev):
+    """1000 launches with merge groups: every output the same bytes, and the
+    tickets back at zero after each (the last arriver of a group resets it)."""
+    import torch
+    from paper_2606_05933_amd import ssa
+    b = small(32, 8, 128, [(300, 1500), (1, 3000), (1, 5000)], seed=3, name="repeat")
+    db = run(b, ssa.make_tuning(chunk_split_keys=512, decode_split_keys=256))
+    assert db.info.num_merge_groups > 0
+    first = db.out.clone()
+    for k in range(1000):
+        db.out.zero_()
+        db.attention()
+        if k % 100 == 99:
+            torch.cuda.synchronize()
+            assert torch.equal(db.out.view(torch.int16), first.view(torch.int16)), k
+            assert not db.launch_words().any(), k
+    torch.cuda.synchronize()
+    assert not db.launch_words().any()
 
 
 @pytest.mark.parametrize("case", range(len(SMALL)))
@@ -192,35 +213,125 @@ def sampled_parity(b, n_chunk_rows=24, heads_per_row=4, seed=0):
 
 
 @pytest.mark.parametrize("name,chunk,prefix", [
-    ("multi", None, None), ("l70b", None, None),
-    ("l8b_sweep", 2048, 6144), ("l8b_sweep", 128, 0), ("l8b_sweep", 1024, 2048),
-    ("l8b_sweep", 2048, 0), ("l8b_sweep", 256, 6144), ("multi", 1024, None),
-    ("l70b", 2048, None), ("l8b", 2048, None), ("l70b_tp8", None, None),
+    ("multi", 1024, None), ("l70b", 2048, None), ("l8b", 2048, None),
 ])
-def test_full_size_sampled_parity(torch_dev, name, chunk, prefix):
+def test_extra_sweep_rows_sampled_parity(torch_dev, name, chunk, prefix):
+    """Latency-table rows beyond the five configurations (chunk sizes of the
+    sweep): the oracle at sampled (row, head) pairs."""
     from paper_2606_05933_amd import workload
     b = workload.make_workload(name, seed=0, chunk=chunk, prefix=prefix)
     b.name = f"{name}(c={chunk},u={prefix})"
     sampled_parity(b)
 
 
-def test_repeat_launches_are_bitwise_identical_and_reset_tickets(torch_dev):
+def both_paths_parity(b):
+    """One oracle evaluation, checked against both launch paths on fresh
+    (poisoned) pools: ssa_kv_append + ssa_mixed_attention, and the fused
+    ssa_append_attention.  Pool images bit for bit, every output element within
+    the bars, the two paths' outputs identical bit for bit, status word zero."""
+    import time
     import torch
-    from paper_2606_05933_amd import ssa
-    b = small(32, 8, 128, [(300, 1500), (1, 3000), (1, 5000)], seed=3, name="repeat")
-    db = run(b, ssa.make_tuning(chunk_split_keys=512, decode_split_keys=256))
-    assert db.info.num_merge_groups > 0
-    first = db.out.clone()
-    for k in range(200):
-        db.out.zero_()
-        db.attention()
-        if k % 50 == 49:
-            torch.cuda.synchronize()
-            assert torch.equal(db.out.view(torch.int16), first.view(torch.int16)), k
-    torch.cuda.synchronize()
-    ng = db.info.num_merge_groups
-    counters_and_tickets = db.workspace[: 4 * (2 + ng)].view(torch.int32)
-    assert int(counters_and_tickets.abs().sum()) == 0
+    from oracle import oracle
+    from paper_2606_05933_amd.device import DeviceBatch, bits_of
+    t0 = time.time()
+    kc, vc = oracle.batch_kv_append(b)
+    ref, used = oracle.batch_attention(b, kc, vc)
+    say(f"    oracle {time.time() - t0:.1f} s on {used} threads")
+    outs = []
+    for fused in (False, True):
+        say(f"[gpu {'fused' if fused else 'two launches'}] {b.name} reqs={b.num_reqs} "
+            f"T={b.num_tokens} hq/hkv/d={b.shape.hq}/{b.shape.hkv}/{b.shape.d} seed={b.seed}")
+        db = DeviceBatch(b)
+        if fused:
+            db.step_fused()
+        else:
+            db.step()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits_of(db.k_cache).reshape(kc.shape), kc), "K pool image differs"
+        assert np.array_equal(bits_of(db.v_cache).reshape(vc.shape), vc), "V pool image differs"
+        assert_close(db.out_f32(), ref, b.name + (" fused" if fused else ""))
+        assert db.status() == 0 and not db.launch_words().any()
+        outs.append(db.out.clone())
+        del db
+        torch.cuda.empty_cache()
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16)), "fused != two launches"
+
+
+# Every element of every configuration at full size: the 15 (prefix, chunk) rows
+# of the chunk-size sweep, the multi-chunk batch, the 70B-shaped layer and one
+# GPU's share of it under 8-way head parallelism.
+FULL_SIZE = ([("l8b_sweep", c, u) for u in (0, 2048, 6144) for c in (128, 256, 512, 1024, 2048)]
+             + [("multi", None, None), ("l70b", None, None), ("l70b_tp8", None, None)])
+
+
+@pytest.mark.parametrize("name,chunk,prefix", FULL_SIZE)
+def test_full_size_parity_both_paths(torch_dev, name, chunk, prefix):
+    from paper_2606_05933_amd import workload
+    b = workload.make_workload(name, seed=0, chunk=chunk, prefix=prefix)
+    b.name = f"{name}(c={chunk},u={prefix})"
+    both_paths_parity(b)
+
+
+def test_random_small_batches_both_paths(torch_dev):
+    """100 seeded random batches: group size 1..16, head dim 64 or 128, 1..6
+    requests with c in [0, 300] (a third of them decodes) and u in [0, 5000],
+    random block tables; both launch paths against the oracle, stopping at the
+    first failure (the draw is printed before it runs)."""
+    import torch
+    from oracle import oracle
+    from paper_2606_05933_amd import workload
+    from paper_2606_05933_amd.device import DeviceBatch, bits_of
+    rng = np.random.default_rng(2606)
+    for k in range(100):
+        G = int(rng.integers(1, 17))
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        d = int(rng.choice([64, 128]))
+        n = int(rng.integers(1, 7))
+        c = [1 if rng.random() < 0.33 else int(rng.integers(0, 301)) for _ in range(n)]
+        u = [int(rng.integers(0, 5001)) for _ in range(n)]
+        if sum(c) == 0:
+            c[0] = 1
+        b = workload.make_batch(workload.Shape(G * hkv, hkv, d), c, u, seed=k, spare_pages=5,
+                                name=f"draw{k}")
+        say(f"[gpu draw {k}] G={G} hkv={hkv} d={d} c={c} u={u}")
+        kc, vc = oracle.batch_kv_append(b)
+        ref, _ = oracle.batch_attention(b, kc, vc)
+        db = DeviceBatch(b)
+        db.step()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits_of(db.k_cache).reshape(kc.shape), kc), f"draw {k}: K pool"
+        assert np.array_equal(bits_of(db.v_cache).reshape(vc.shape), vc), f"draw {k}: V pool"
+        assert_close(db.out_f32(), ref, f"draw {k}")
+        two = db.out.clone()
+        fz = DeviceBatch(b)
+        fz.step_fused()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits_of(fz.k_cache).reshape(kc.shape), kc), f"draw {k}: fused K pool"
+        assert torch.equal(fz.out.view(torch.int16), two.view(torch.int16)), f"draw {k}: fused"
+        assert db.status() == 0 and fz.status() == 0
+
+
+def test_request_order_permutation_permutes_the_rows(torch_dev):
+    """Reordering the requests of a batch (their rows, block-table rows and
+    lengths) reorders the output rows and changes no byte of them: each
+    request's work items and merge order depend only on its own (c, u)."""
+    import torch
+    from paper_2606_05933_amd import workload
+    from paper_2606_05933_amd.device import DeviceBatch
+    b = workload.make_workload("multi", seed=5)
+    perm = np.random.default_rng(77).permutation(b.num_reqs)
+    pb = workload.sub_batch(b, perm)
+    outs = []
+    for x in (b, pb):
+        db = DeviceBatch(x)
+        db.step_fused()
+        torch.cuda.synchronize()
+        assert db.status() == 0
+        outs.append(db.out.view(torch.int16).cpu().numpy())
+        del db
+    starts = np.concatenate([[0], np.cumsum(b.q_len)])
+    rows = np.concatenate([np.arange(starts[i], starts[i + 1]) for i in perm])
+    assert np.array_equal(outs[1], outs[0][rows])
 
 
 def test_timed_launches_stamp_the_kernels_and_match_untimed(torch_dev):
@@ -263,6 +374,8 @@ def fused_parity(b, tuning=None, plan_on_device=False):
     assert np.array_equal(bits_of(db.v_cache).reshape(vc.shape), vc), "V pool image differs"
     ref, _ = oracle.batch_attention(b, kc, vc)
     assert_close(db.out_f32(), ref, b.name + " fused")
+    assert db.status() == 0, f"status word {db.status()}"
+    assert not db.launch_words().any()
     fused = db.out.clone()
     two = DeviceBatch(b, tuning, plan_on_device=plan_on_device)
     two.step()
@@ -310,5 +423,33 @@ def test_fused_repeated_from_poisoned_pools(torch_dev):
         db.step_fused()
         torch.cuda.synchronize()
         assert torch.equal(db.out.view(torch.int16), ref.view(torch.int16)), k
-    ng = db.info.num_merge_groups
-    assert int(db.workspace[: 4 * (2 + ng)].view(torch.int32).abs().sum()) == 0
+    assert not db.launch_words().any()
+
+
+def test_fused_wait_time_out_is_reported_and_every_workgroup_exits(torch_dev):
+    """The fused launch's wait for appended rows is bounded.  Forced from the
+    host (the appended-rows counter preset far below zero, so the count never
+    arrives within the launch, and a wait of 64 polls), every chunk item gives
+    up, the launch still completes, the status word says so, and the counters
+    end where they started (the last chunk item subtracts the launch's counts).
+    No kernel faults or hangs: every wait has an exit."""
+    import torch
+    from paper_2606_05933_amd import ssa, workload
+    from paper_2606_05933_amd.device import DeviceBatch
+    b = workload.make_workload("tiny", seed=2)
+    db = DeviceBatch(b, ssa.make_tuning(append_wait_polls=64))
+    assert db.info.num_chunk_items > 0 and db.info.num_append_segments > 0
+    preset = -(1 << 20)
+    db.workspace[0:4].view(torch.int32).fill_(preset)
+    torch.cuda.synchronize()
+    db.step_fused()
+    st = db.status()
+    say(f"    status after the forced time-out: {st}")
+    assert st & ssa.SSA_STATUS_WAIT_TIMEOUT
+    words = db.launch_words()
+    assert words[0] == preset and words[1] == 0
+    # cleared, the same workspace serves a normal launch again
+    db.workspace.zero_()
+    db.plan(ssa.make_tuning())
+    db.step_fused()
+    assert db.status() == 0 and not db.launch_words().any()
