@@ -209,9 +209,13 @@ def cpu_baseline(b, target_s=15.0, threads=0):
     stride = max(1, max_c // 4)
     dt, used, work, total, nrows = run(stride)  # calibration
     if work < total and dt < target_s:
-        # chunk-row work scales as 1 / stride; decode rows are always in
+        # decode rows are always in the sample; the chunk rows' work scales as
+        # 1 / stride: pick the stride whose sample takes about target_s
         rate = work / max(dt, 1e-9)
-        stride = max(1, int(stride * (work / rate) / target_s))
+        dec = sum(int(u) + 1 for c, u in zip(b.q_len, b.ctx_len) if c == 1)
+        chunk_all = total - dec
+        room = target_s * rate - dec
+        stride = max(1, int(np.ceil(chunk_all / room))) if room > 0 else max_c
         dt, used, work, total, nrows = run(stride)
     t_iter = t_app + dt * total / work
     return {"value": round(t_iter * 1e6, 1), "unit": "us/iter", "cores": int(used),

@@ -473,7 +473,7 @@ __device__ __forceinline__ float max8(const float (&s)[8]) {
 
 struct SmBlock {
   float s[8];
-  float lmax, lb;
+  float lb;
   u32x4 pk;
 };
 
@@ -506,7 +506,6 @@ __device__ __forceinline__ SmBlock softmax_begin(f32x4 s0, f32x4 s1, int lim, fl
 #pragma unroll
     for (int e = 0; e < 8; ++e) b.s[e] = (e <= lim) ? b.s[e] : kNegInf;
   }
-  b.lmax = max8(b.s);
   b.pk = sm_form<MASKED>(b.s, lim, c, st.m, b.lb);
   return b;
 }
@@ -514,8 +513,15 @@ __device__ __forceinline__ SmBlock softmax_begin(f32x4 s0, f32x4 s1, int lim, fl
 template <int MT, bool MASKED>
 __device__ __forceinline__ bf16x8 softmax_end(SmBlock& b, int lim, float c, float inv_c,
                                               ColState& st, f32x4 (&o)[MT]) {
-  if (__builtin_amdgcn_ballot_w64(b.lmax > st.thr)) {
-    const float cmax = wave_max_cols(b.lmax);
+  // A logit above thr gives a probability above 2^kRescaleThreshold = 256, and
+  // then the lane's sum of its rounded probabilities is at least 256 (bf16
+  // rounding is monotone): the cheap test on the sum, which is formed anyway,
+  // admits every block that may raise a reference (and, rarely, some that do
+  // not: those leave every column as it was).  While a reference is still
+  // -inf its probabilities are +inf, so a column's first visible block always
+  // enters.
+  if (__builtin_amdgcn_ballot_w64(b.lb >= 256.f)) {
+    const float cmax = wave_max_cols(max8(b.s));
     const bool raise = cmax > st.thr;  // the same for every lane of a column
     const float m_new = raise ? cmax * c : st.m;
     const float alpha = raise ? __builtin_amdgcn_exp2f(st.m - m_new) : 1.f;
@@ -581,15 +587,14 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   const float c = a.scale_log2;
   const float inv_c = 1.f / c;
 
-  // this wave's columns: [wc0, wc1)
+  // this wave's columns start at wc0; the tile's end is colend
   const int colend = it.col0 + it.ncols;
   const int wc0 = it.col0 + w * kChunkWaveCols;
-  const int wc1 = min(wc0 + kChunkWaveCols, colend);
-  const bool wave_has = wc0 < colend;
-  const int wpmin = wave_has ? u + wc0 / G : 0;                     // smallest position
-  const int wkend = wave_has ? min(it.key1, u + (wc1 - 1) / G + 1) : it.key0;
-  const int nb = (it.key1 - it.key0 + 31) / 32;                     // blocks of the item
-  const int nbw = (wkend - it.key0 + 31) / 32;                      // blocks this wave uses
+  const int nb = (it.key1 - it.key0 + 31) / 32;  // blocks of the item
+  // Blocks [0, b_vis) are visible to every column of the tile (their last key
+  // is at most the tile's smallest position): they need no causal mask.
+  const int vis = u + it.col0 / G + 1 - it.key0;
+  const int b_vis = vis <= 0 ? 0 : min(nb, vis >> 5);
 
   bf16x8 qop[NT][KK];
   int pos[NT];
@@ -599,7 +604,9 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     if (col < colend) {
       const int j = col / G;
       const int hg = col - j * G;
-      pos[nt] = u + j;
+      // the last key this column may see in this item: its own position, or
+      // the item's last key when the item is a piece of the key range
+      pos[nt] = min(u + j, it.key1 - 1);
       const uint16_t* qrow = a.q + ((size_t)(rq.q_start + j) * a.hq + it.kvh * G + hg) * D;
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) qop[nt][kk] = as_bf16x8(ld16(qrow + kk * 32 + g * 8));
@@ -728,7 +735,6 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     }
   };
   auto lim_of = [&](int nt, int kb) { return pos[nt] - (kb + 8 * g); };
-  auto masked = [&](int kb) { return kb + 31 > wpmin; };
   // SM(b,0) as one unit (prologue)
   auto softmax_tile0 = [&](auto masked_t, int kb) {
     constexpr bool M = decltype(masked_t)::value;
@@ -755,38 +761,35 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     interleave_stream<MT, 2, kReadAhead>();
     p0 = softmax_end<MT, M>(sb, lim, c, inv_c, cs[0], o[0]);
   };
-  auto iteration = [&](auto sv_t, int b) {
-    constexpr int SV = decltype(sv_t)::value;
-    const char* stv = lds + SV * C::STAGE;
-    const char* stk = lds + ((SV + 1) % kChunkStages) * C::STAGE;
-    const int kb = it.key0 + b * 32;
-    if (masked(kb))
-      step_a(std::true_type{}, stk, kb);
-    else
-      step_a(std::false_type{}, stk, kb);
-    if (b + 1 < nbw) {
-      if (masked(kb + 32))
-        step_b(std::true_type{}, stv, kb + 32);
-      else
-        step_b(std::false_type{}, stv, kb + 32);
-    } else {
-      pv2(stv);  // the wave's last block
-    }
-  };
   // Every iteration issues the same number of LDS copies per thread (the
   // fetch is clamped to the last block), so the copies still allowed in
   // flight at a barrier are an exact count: the barrier ending iteration b
   // needs blocks up to b+2 (read by iteration b+1) and leaves the fetches of
-  // the S-3 most recent iterations outstanding.  The block after the current
-  // one is zeroed past the request's end if needed (it has landed).
-  constexpr int kInFlight = (kChunkStages - 3) * 2 * C::LOADS;
-  auto block = [&](auto coh_t, auto sv_t, int b) {
+  // the S-3 most recent iterations outstanding.
+  constexpr int S = kChunkStages;
+  constexpr int kInFlight = (S - 3) * 2 * C::LOADS;
+  // Iteration b (stage SV = b % S): fetch block b+S-1 (clamped to the last
+  // block) into the stage of block b-1, zero the value tail of the block read
+  // next once it has landed, then step A (QK of block b+1, softmax of block b
+  // for tile 1) and step B (PV of block b, softmax of block b+1 for tile 0).
+  // Every wave runs every iteration, with no data-dependent branch around the
+  // MFMAs: an accumulator then has exactly one use, its next MFMA, and each
+  // MFMA accumulates in place.  Blocks past the item's last one are masked for
+  // every column (their stages hold copies of the last block, value tails
+  // zeroed: a zero probability times a zero value adds nothing).
+  auto block = [&](auto masked_t, auto sv_t, int b, bool coh) {
     constexpr int SV = decltype(sv_t)::value;
-    constexpr int S = kChunkStages;
-    dma(coh_t, it.key0 + min(b + S - 1, nb - 1) * 32, lds + ((SV + S - 1) % S) * C::STAGE);
-    const int kn = it.key0 + (b + 1) * 32;
-    if (b + 1 < nb && kn + 32 > nvalid) zero_tail(kn, lds + ((SV + 1) % S) * C::STAGE);
-    if (b < nbw) iteration(sv_t, b);
+    const int bf = min(b + S - 1, nb - 1);
+    char* fst = lds + ((SV + S - 1) % S) * C::STAGE;
+    if (FUSED && coh)
+      dma(std::true_type{}, it.key0 + bf * 32, fst);
+    else
+      dma(std::false_type{}, it.key0 + bf * 32, fst);
+    const int kn = it.key0 + min(b + 1, nb - 1) * 32;
+    if (kn + 32 > nvalid) zero_tail(kn, lds + ((SV + 1) % S) * C::STAGE);
+    const int kb = it.key0 + b * 32;
+    step_a(masked_t, lds + ((SV + 1) % S) * C::STAGE, kb);
+    step_b(masked_t, lds + SV * C::STAGE, kb + 32);
     vm_wait<kInFlight>();
     __syncthreads();
   };
@@ -796,66 +799,50 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   // does not see) and stall on them inside the loop.
   lds_dma_wait();
   // Block index of the first block holding keys >= u, and the first loop
-  // step (a multiple of the stage count, so that both loops below start at
-  // stage 0) from which the copies are device-scope: at or before the step
-  // that fetches that block.
-  constexpr int S = kChunkStages;
+  // step (a multiple of the stage count) from which the copies are
+  // device-scope: at or before the step that fetches that block.
   const int first_new = u > it.key0 ? (u - it.key0) / 32 : 0;
   const int b_coh = FUSED ? min(nb, max(0, first_new - (S - 1)) / S * S) : nb;
   const bool coh_prologue = FUSED && first_new <= S - 2;
   if (coh_prologue) wait_appended(a);
-  if (nb > 0) {
-    if (coh_prologue) {
+  if (coh_prologue) {
 #pragma unroll
-      for (int k = 0; k < S - 1; ++k)
-        dma(std::true_type{}, it.key0 + min(k, nb - 1) * 32, lds + k * C::STAGE);
-    } else {
+    for (int k = 0; k < S - 1; ++k)
+      dma(std::true_type{}, it.key0 + min(k, nb - 1) * 32, lds + k * C::STAGE);
+  } else {
 #pragma unroll
-      for (int k = 0; k < S - 1; ++k)
-        dma(std::false_type{}, it.key0 + min(k, nb - 1) * 32, lds + k * C::STAGE);
-    }
+    for (int k = 0; k < S - 1; ++k)
+      dma(std::false_type{}, it.key0 + min(k, nb - 1) * 32, lds + k * C::STAGE);
   }
   vm_wait<kInFlight>();  // blocks 0 and 1 have landed
   __syncthreads();
-  if (nb > 0 && it.key0 + 32 > nvalid) {
+  if (it.key0 + 32 > nvalid) {
     zero_tail(it.key0, lds);
     __syncthreads();
   }
-  if (nbw > 0) {  // QK(0,0), QK(0,1), SM(0,0)
-    qk2(lds, s0, s1);
-    if (masked(it.key0))
-      p0 = softmax_tile0(std::true_type{}, it.key0);
-    else
-      p0 = softmax_tile0(std::false_type{}, it.key0);
-  }
-  static_assert(kChunkStages >= 3 && kChunkStages <= 5, "pipeline depth");
-  // steps [b, end): end is nb or a multiple of the stage count
-  int b = 0;
-  auto run = [&](auto coh_t, int end) {
-    while (b < end) {
-      block(coh_t, Stage<0>{}, b);
-      if (++b >= end) break;
-      block(coh_t, Stage<1>{}, b);
-      if (++b >= end) break;
-      block(coh_t, Stage<2>{}, b);
-      if (++b >= end) break;
-      if (kChunkStages >= 4) {
-        block(coh_t, Stage<(kChunkStages >= 4 ? 3 : 0)>{}, b);
-        if (++b >= end) break;
-      }
-      if (kChunkStages >= 5) {
-        block(coh_t, Stage<(kChunkStages >= 5 ? 4 : 0)>{}, b);
-        ++b;
-      }
-    }
+  // QK(0,0), QK(0,1), SM(0,0)
+  qk2(lds, s0, s1);
+  if (b_vis >= 1)
+    p0 = softmax_tile0(std::false_type{}, it.key0);
+  else
+    p0 = softmax_tile0(std::true_type{}, it.key0);
+  static_assert(kChunkStages == 4, "the loop runs trips of four stages");
+  // Trips of S iterations: unmasked while both blocks an iteration softmaxes
+  // (b and b+1) are visible to every column, then masked up to the item's
+  // block count rounded up to a trip.  One exit per loop, after whole trips.
+  const int n_um = b_vis >= 1 ? (b_vis - 1) / S * S : 0;
+  const int nb_pad = (nb + S - 1) / S * S;
+  auto trip = [&](auto masked_t, int b0) {
+    if (FUSED && b0 == b_coh && b_coh < nb && !coh_prologue) wait_appended(a);
+    const bool coh = FUSED && b0 >= b_coh && b_coh < nb;
+    block(masked_t, Stage<0>{}, b0, coh);
+    block(masked_t, Stage<1>{}, b0 + 1, coh);
+    block(masked_t, Stage<2>{}, b0 + 2, coh);
+    block(masked_t, Stage<3>{}, b0 + 3, coh);
   };
-  run(std::false_type{}, b_coh);
-  if constexpr (FUSED) {
-    if (b < nb) {
-      if (!coh_prologue) wait_appended(a);
-      run(std::true_type{}, nb);
-    }
-  }
+  int b = 0;
+  for (; b < n_um; b += S) trip(std::false_type{}, b);
+  for (; b < nb_pad; b += S) trip(std::true_type{}, b);
   lds_dma_wait();  // no copy may land after this workgroup has left
 
   // epilogue
