@@ -106,10 +106,11 @@ typedef struct ssa_shape {
  *                    b mod num_xcds), and work items that read the same K/V
  *                    (one request and kv head of a chunk) go to one die
  *                    (default 1: off; on MI355X it measured no faster)
- *   mix_order        0 = chosen by the planner (default): 3 when the chunk items
- *                    number at least 2 * num_cus and the decode part's estimated
- *                    time (its bytes at 0.7 of the HBM peak) is at least 0.85 of
- *                    the chunk part's (its flops at half the MFMA peak), else 1;
+ *   mix_order        0 = chosen by the planner (default): when the chunk items
+ *                    number at least 2 * num_cus, 3 if the decode part's
+ *                    estimated time (its bytes at 0.7 of the HBM peak) is at
+ *                    least 0.85 of the chunk part's (its flops at half the MFMA
+ *                    peak), 4 if it is at least 0.25 of it; else 1;
  *                    1 = all chunk items (longest first) before the decode
  *                    items, 2 = the two kinds interleaved, 3 = paired:
  *                    the first num_cus chunk items, then decode items for the

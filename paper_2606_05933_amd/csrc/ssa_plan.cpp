@@ -50,6 +50,8 @@ constexpr int kOrderPaired = 3;
 constexpr int kOrderPairedDecodeFirst = 4;
 // automatic order: paired once decode time / chunk time (both estimated) reaches this
 constexpr double kPairedMinRatio = 0.85;
+// automatic order: paired, then the other decode items first, from this ratio up
+constexpr double kPairedDecodeFirstRatio = 0.25;
 
 struct Tuning {
   int tile_cols, chunk_split_keys, decode_split_keys, num_cus, num_xcds, mix_order, wait_polls;
@@ -449,11 +451,18 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   std::vector<uint16_t> bucket(raw.size());
   for (size_t k = 0; k < raw.size(); ++k) bucket[k] = (uint16_t)time_bucket(est_t[k]);
   std::vector<uint32_t> seq;
-  // Automatic launch order.  Pairing a chunk tile with a decode item on every
-  // compute unit pays when the chunk items alone fill both slots of every unit
-  // and the decode part is at least comparable to them.  Measured: about 10%
-  // faster where the estimated decode time (0.7 of the HBM peak) is at least
-  // 0.96 of the chunk time (half the MFMA peak), 4-40% slower at 0.73 and below.
+  // Automatic launch order, for batches whose chunk items alone fill both
+  // slots of every compute unit (otherwise all chunk items first):
+  //  * the decode part comparable to the chunk part (estimated decode time, at
+  //    0.7 of the HBM peak, at least 0.85 of the chunk time at half the MFMA
+  //    peak): one chunk and one decode item on every unit, the rest
+  //    interleaved (measured about 10% faster on such batches);
+  //  * a smaller but still sizeable decode part (ratio 0.25 .. 0.85): one
+  //    chunk item on every unit beside the decode items, then the other chunk
+  //    items, which take the slots the decode items free (measured 5-10%
+  //    faster than all chunk items first on the 70B-shaped layer, ratio 0.56,
+  //    where interleaving the rest is 20% slower: a long chunk tile that
+  //    starts late is the launch's tail).
   if (tu.auto_order) {
     size_t nchunk = 0;
     for (const WorkItem& it : raw) nchunk += it.kind == kItemChunk;
@@ -461,6 +470,8 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
     const double t_chk = in.chunk_flops / (kMfmaRatePerCu * tu.num_cus);
     if (nchunk >= 2 * (size_t)tu.num_cus && t_dec >= kPairedMinRatio * t_chk)
       tu.mix_order = kOrderPaired;
+    else if (nchunk >= 2 * (size_t)tu.num_cus && t_dec >= kPairedDecodeFirstRatio * t_chk)
+      tu.mix_order = kOrderPairedDecodeFirst;
   }
   order_items(raw, est_t, bucket, tu, Hkv, &seq);
   p->items.resize(raw.size());

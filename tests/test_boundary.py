@@ -218,7 +218,8 @@ def _plan_kinds(name, chunk, tuning=None):
 def test_automatic_launch_order_pairs_only_decode_heavy_full_chunk_batches():
     """Left at 0, mix_order pairs chunk and decode items on every unit when the chunk
     items fill both slots of every unit and the decode part is comparable (l8b at
-    c = 2048); chunk-heavy batches (l70b at c = 1024) and batches with fewer chunk
+    c = 2048); with a smaller decode part (l70b at c = 1024) the other decode items
+    follow the pairs and the other chunk items come last; batches with fewer chunk
     items (l8b at c = 512) keep all chunk items first; an explicit order is kept."""
     def paired(kinds, info):
         # paired: the first 256 workgroups are chunk items, the next 256 decode items
@@ -228,8 +229,12 @@ def test_automatic_launch_order_pairs_only_decode_heavy_full_chunk_batches():
     assert paired(k, info)
     k, info = _plan_kinds("l8b", 2048, ssa.make_tuning(mix_order=1))
     assert not paired(k, info) and (k[:512] == k[0]).all()
+    # chunk-heavy with a sizeable decode part (l70b at c = 1024, estimated ratio
+    # 0.56): one chunk item per unit beside the decode items, the decode items
+    # next, the other chunk items last
     k, info = _plan_kinds("l70b", 1024)
-    assert info.num_chunk_items >= 512 and not paired(k, info)
+    assert info.num_chunk_items == 512 and paired(k, info)
+    assert (k[512:512 + info.num_decode_items - 256] == 1).all() and (k[-256:] == 0).all()
     k, info = _plan_kinds("l8b", 512)
     assert (k[:info.num_chunk_items] == k[0]).all()  # all chunk items first
 
