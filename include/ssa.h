@@ -180,6 +180,9 @@ typedef struct ssa_plan_info {
   int32_t num_append_segments, scene;
   double decode_bytes, chunk_bytes, chunk_flops, decode_flops, append_bytes;
   double x[7];
+  int64_t ws_zero_bytes;  /* leading workspace bytes that must be zero at rest
+                             (counters, status word, merge tickets); the rest
+                             holds split records */
 } ssa_plan_info;
 
 /* Static description of an error code ("ok" for SSA_OK, "unknown" otherwise). */
@@ -241,10 +244,13 @@ int ssa_kv_append(const ssa_shape* shape, const void* plan_host, const void* pla
  * (fp32 accumulation).  Reads the chunk's own keys from the pools, so
  * ssa_kv_append of the same plan must have run before it on the stream.
  * workspace: device memory of at least the plan's workspace size (never less
- * than 256 bytes), zero-filled by the caller once before its first use; each
- * call leaves its counters at zero again, and reports errors in the status
- * word (SSA_WS_STATUS_OFFSET).  Calls that share a workspace must not overlap
- * in time.
+ * than 256 bytes).  Its first ws_zero_bytes bytes (ssa_plan_info) must be zero
+ * when a call starts: zero-fill them before the first call, and again when the
+ * workspace passes to a plan with a larger ws_zero_bytes (the bytes past a
+ * plan's ws_zero_bytes hold its split records).  Each call leaves its counters
+ * and tickets at zero again, and reports errors in the status word
+ * (SSA_WS_STATUS_OFFSET).  Calls that share a workspace must not overlap in
+ * time.
  * Errors: NULL, the shape errors, PLAN_MISMATCH, WORKSPACE, HIP.
  */
 int ssa_mixed_attention(const ssa_shape* shape, const void* plan_host, const void* plan_dev,

@@ -1383,7 +1383,43 @@ int attention_args(const ssa_shape* shape, const void* plan_host, const void* pl
   a->v_new = nullptr;
   return SSA_OK;
 }
+
+// Validated arguments of a fused launch (SSA_OK, or the error to return).
+int append_attention_args(const ssa_shape* shape, const void* plan_host, const void* plan_dev,
+                          const uint16_t* q, const uint16_t* k_new, const uint16_t* v_new,
+                          uint16_t* k_cache, uint16_t* v_cache, const int32_t* block_table,
+                          uint16_t* out, void* workspace, size_t workspace_bytes,
+                          const PlanHeader** hp, AttnArgs* a, AppendArgs* ap) {
+  int rc = attention_args(shape, plan_host, plan_dev, q, k_cache, v_cache, block_table, out,
+                          workspace, workspace_bytes, hp, a);
+  if (rc || (*hp)->num_items == 0) return rc;
+  const PlanHeader* h = *hp;
+  if (h->num_segments > 0 && (!k_new || !v_new)) return SSA_ERR_NULL;
+  // the last chunk item resets the counters: appending workgroups need one
+  if (h->num_chunk_segments > 0 && h->num_chunk_items == 0) return SSA_ERR_PLAN_MISMATCH;
+  a->append_wgs = h->num_chunk_segments;
+  a->k_new = k_new;
+  a->v_new = v_new;
+  *ap = AppendArgs{k_new, v_new, k_cache, v_cache, h->off_segments};
+  return SSA_OK;
+}
+
+int launch_append_attention(const PlanHeader* h, AttnArgs& a, AppendArgs& ap, void* stream,
+                            void* start_event, void* stop_event) {
+  (void)clear_and_check();
+  void* args[] = {&a, &ap};
+  const void* fn = h->head_dim == 128
+                       ? reinterpret_cast<const void*>(&append_attention_kernel<128>)
+                       : reinterpret_cast<const void*>(&append_attention_kernel<64>);
+  hipError_t e = hipExtLaunchKernel(fn, dim3(a.append_wgs + h->num_items), dim3(kThreads), args,
+                                    0, static_cast<hipStream_t>(stream),
+                                    static_cast<hipEvent_t>(start_event),
+                                    static_cast<hipEvent_t>(stop_event), 0);
+  return e == hipSuccess && hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+}
+
 }  // namespace
+
 
 extern "C" {
 
@@ -1424,26 +1460,11 @@ int ssa_append_attention(const ssa_shape* shape, const void* plan_host, const vo
                          void* start_event, void* stop_event) {
   const PlanHeader* h = nullptr;
   AttnArgs a;
-  int rc = attention_args(shape, plan_host, plan_dev, q, k_cache, v_cache, block_table, out,
-                          workspace, workspace_bytes, &h, &a);
+  AppendArgs ap;
+  int rc = append_attention_args(shape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
+                                 block_table, out, workspace, workspace_bytes, &h, &a, &ap);
   if (rc || h->num_items == 0) return rc;
-  if (h->num_segments > 0 && (!k_new || !v_new)) return SSA_ERR_NULL;
-  // the last chunk item resets the counters: appending workgroups need one
-  if (h->num_chunk_segments > 0 && h->num_chunk_items == 0) return SSA_ERR_PLAN_MISMATCH;
-  a.append_wgs = h->num_chunk_segments;
-  a.k_new = k_new;
-  a.v_new = v_new;
-  AppendArgs ap{k_new, v_new, k_cache, v_cache, h->off_segments};
-  (void)clear_and_check();
-  void* args[] = {&a, &ap};
-  const void* fn = h->head_dim == 128
-                       ? reinterpret_cast<const void*>(&append_attention_kernel<128>)
-                       : reinterpret_cast<const void*>(&append_attention_kernel<64>);
-  hipError_t e = hipExtLaunchKernel(fn, dim3(a.append_wgs + h->num_items), dim3(kThreads), args,
-                                    0, static_cast<hipStream_t>(stream),
-                                    static_cast<hipEvent_t>(start_event),
-                                    static_cast<hipEvent_t>(stop_event), 0);
-  return e == hipSuccess && hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
+  return launch_append_attention(h, a, ap, stream, start_event, stop_event);
 }
 
 }  // extern "C"

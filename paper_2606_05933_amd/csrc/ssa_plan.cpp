@@ -533,6 +533,7 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   const int64_t tickets = ceil_div(((int64_t)kLaunchCounters + p->groups.size()) * 4, 256) * 256;
   h.ws_partials_off = tickets;
   h.ws_bytes = tickets + ws_floats * 4;
+  in.ws_zero_bytes = tickets;
 
   uint64_t hv = 1469598103934665603ull;
   int32_t fields[8] = {Hq, Hkv, D, P, s->num_pages, s->max_pages_per_req, n, 0};

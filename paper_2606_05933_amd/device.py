@@ -80,6 +80,9 @@ class DeviceBatch:
         self.plan_host, self.plan_dev = self._host[0], self._dev[0]
         if not hasattr(self, "workspace") or self.workspace.numel() < ws_bytes:
             self.workspace = torch.zeros(max(ws_bytes, 256), dtype=torch.uint8, device=self.device)
+        else:
+            # another plan's split records may lie where this plan's tickets are
+            self.workspace.zero_()
         # calls bound once per slot (on the stream current now): an iteration
         # only crosses into the library
         self._info_scratch = ssa.SsaPlanInfo()

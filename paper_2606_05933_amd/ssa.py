@@ -92,7 +92,7 @@ class SsaPlanInfo(ctypes.Structure):
         "num_chunk_items", "num_decode_items", "num_merge_groups", "num_append_segments",
         "scene")] + [(n, ctypes.c_double) for n in (
             "decode_bytes", "chunk_bytes", "chunk_flops", "decode_flops", "append_bytes")] + [
-        ("x", ctypes.c_double * 7)]
+        ("x", ctypes.c_double * 7), ("ws_zero_bytes", ctypes.c_int64)]
 
     def as_dict(self):
         d = {n: getattr(self, n) for n, _ in self._fields_ if n != "x"}
