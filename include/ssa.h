@@ -306,6 +306,29 @@ int ssa_append_attention(const ssa_shape* shape, const void* plan_host, const vo
                          uint16_t* out, void* workspace, size_t workspace_bytes, void* stream,
                          void* start_event, void* stop_event);
 
+/*
+ * ssa_append_attention without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The launch's counters, status word,
+ * merge tickets and split records live in a scratch array of the library,
+ * 32 MiB per GPU, held by each GPU the library runs on until the process ends;
+ * the call allocates nothing.  On a device's first call the library takes the
+ * array's device address (hipGetSymbolAddress); whenever a call's plan needs
+ * a larger zeroed prefix (ssa_plan_info.ws_zero_bytes) than the previous
+ * call's left, a small fill kernel on the same stream clears it first.
+ *   Arguments, results and errors: those of ssa_append_attention without
+ *   workspace / workspace_bytes; SSA_ERR_WORKSPACE if the plan needs more than
+ *   the 32 MiB scratch (its workspace size from ssa_plan_size).  The status
+ *   word is the scratch's own and is not visible to the caller.
+ *   Every call on one GPU shares that GPU's scratch: calls that overlap in
+ *   time on one GPU (two streams, two threads) race and must not be issued.
+ */
+int ssa_append_attention_static(const ssa_shape* shape, const void* plan_host,
+                                const void* plan_dev, const uint16_t* q, const uint16_t* k_new,
+                                const uint16_t* v_new, uint16_t* k_cache, uint16_t* v_cache,
+                                const int32_t* block_table, uint16_t* out, void* stream,
+                                void* start_event, void* stop_event);
+
 #ifdef __cplusplus
 }
 #endif

@@ -40,6 +40,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 #include "../../include/ssa.h"
@@ -1420,6 +1422,65 @@ int launch_append_attention(const PlanHeader* h, AttnArgs& a, AppendArgs& ap, vo
 
 }  // namespace
 
+// ------------------------------------------- the allocation-free entry point
+
+// Scratch of ssa_append_attention_static: the fused launch's counters, status
+// word, merge tickets and split records, in place of a caller's workspace.
+// One copy per GPU (held until the process ends); every call on a GPU shares
+// it.  In host code the name is a stand-in, not a device address: the
+// per-device address comes from hipGetSymbolAddress.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+struct ScratchState {
+  void* ptr = nullptr;    // device address of `scratch` on this device
+  int64_t clean = 0;      // leading bytes that are zero at rest
+};
+std::mutex g_scratch_mutex;
+ScratchState g_scratch[kMaxScratchDevices];
+
+__global__ __launch_bounds__(kThreads) void clear_words_kernel(uint32_t* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kThreads)
+    p[i] = 0u;
+}
+
+// The current device's scratch address, its first zero_bytes bytes zero when
+// the launch that follows on `stream` starts.  Set-up happens on a device's
+// first call (with that device current).  A call's split records start at
+// its zero_bytes, so after it exactly that prefix is zero at rest (the kernel
+// resets its counters and tickets); a later call with a larger prefix first
+// clears the difference with a fill kernel on the same stream (no memset: a
+// caller may capture the calls in a graph).
+int scratch_for_launch(int64_t zero_bytes, hipStream_t stream, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return SSA_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  ScratchState& st = g_scratch[dev];
+  if (!st.ptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return SSA_ERR_HIP;
+    }
+    st.ptr = p;
+    st.clean = 0;
+  }
+  if (zero_bytes > st.clean) {
+    const int64_t words = (zero_bytes + 3) / 4;
+    const int64_t grid = std::min<int64_t>((words + kThreads - 1) / kThreads, 1024);
+    (void)clear_and_check();
+    hipLaunchKernelGGL(clear_words_kernel, dim3((unsigned)grid), dim3(kThreads), 0, stream,
+                       static_cast<uint32_t*>(st.ptr), words);
+    if (hipGetLastError() != hipSuccess) return SSA_ERR_HIP;
+  }
+  st.clean = zero_bytes;
+  *out = st.ptr;
+  return SSA_OK;
+}
+}  // namespace
 
 extern "C" {
 
@@ -1464,6 +1525,30 @@ int ssa_append_attention(const ssa_shape* shape, const void* plan_host, const vo
   int rc = append_attention_args(shape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
                                  block_table, out, workspace, workspace_bytes, &h, &a, &ap);
   if (rc || h->num_items == 0) return rc;
+  return launch_append_attention(h, a, ap, stream, start_event, stop_event);
+}
+
+int ssa_append_attention_static(const ssa_shape* shape, const void* plan_host,
+                                const void* plan_dev, const uint16_t* q, const uint16_t* k_new,
+                                const uint16_t* v_new, uint16_t* k_cache, uint16_t* v_cache,
+                                const int32_t* block_table, uint16_t* out, void* stream,
+                                void* start_event, void* stop_event) {
+  const PlanHeader* h = nullptr;
+  AttnArgs a;
+  AppendArgs ap;
+  // every argument is checked before any HIP call: the scratch stands in as a
+  // workspace of its size at a placeholder address until it is resolved
+  int rc = check_plan(shape, plan_host, &h);
+  if (rc) return rc;
+  if (h->ws_bytes > (int64_t)kScratchBytes) return SSA_ERR_WORKSPACE;
+  rc = append_attention_args(shape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
+                             block_table, out, reinterpret_cast<void*>(kScratchBytes),
+                             kScratchBytes, &h, &a, &ap);
+  if (rc || h->num_items == 0) return rc;
+  void* ws = nullptr;
+  rc = scratch_for_launch(h->ws_partials_off, static_cast<hipStream_t>(stream), &ws);
+  if (rc) return rc;
+  a.ws = static_cast<uint8_t*>(ws);
   return launch_append_attention(h, a, ap, stream, start_event, stop_event);
 }
 

@@ -153,6 +153,9 @@ def _load():
     lib.ssa_append_attention.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                          vp, vp, vp]
     lib.ssa_append_attention.restype = ctypes.c_int
+    lib.ssa_append_attention_static.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                vp, vp]
+    lib.ssa_append_attention_static.restype = ctypes.c_int
     dp = P(ctypes.c_double)
     lib.ssa_predictor_init.argtypes = [P(SsaPredictor), ctypes.c_int32]
     lib.ssa_predictor_add.argtypes = [P(SsaPredictor), dp, ctypes.c_int32, ctypes.c_double]
@@ -192,7 +195,8 @@ LIB = _load()
 EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_check_block_table",
             "ssa_kv_append",
             "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed",
-            "ssa_append_attention", "ssa_predictor_init", "ssa_predictor_add",
+            "ssa_append_attention", "ssa_append_attention_static", "ssa_predictor_init",
+            "ssa_predictor_add",
             "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
             "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor",
             "ssa_rope_append", "ssa_linear_workspace_size", "ssa_linear", "ssa_rms_norm",
@@ -741,6 +745,32 @@ def bind_append_attention(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new,
             vp(_ptr(block_table)), vp(_ptr(out)), vp(_ptr(workspace)), ctypes.c_size_t(ws_bytes),
             vp(_stream(stream)))
     return BoundCall(LIB.ssa_append_attention, "ssa_append_attention", args, timed=True)
+
+
+def append_attention_static(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache,
+                            v_cache, block_table, out, stream=None, events=(None, None)):
+    """ssa_append_attention_static: the fused launch with the library's own
+    per-GPU scratch in place of a workspace (nothing is allocated)."""
+    h = _plan_header(plan_host)
+    T, n = h["num_tokens"], h["num_reqs"]
+    qrow = shape.num_q_heads * shape.head_dim
+    row = shape.num_kv_heads * shape.head_dim
+    pool = shape.num_pages * shape.num_kv_heads * shape.page_size * shape.head_dim
+    _check_dev("q", q, T * qrow, 2)
+    _check_dev("out", out, T * qrow, 2)
+    _check_dev("k_new", k_new, T * row, 2)
+    _check_dev("v_new", v_new, T * row, 2)
+    _check_dev("k_cache", k_cache, pool, 2)
+    _check_dev("v_cache", v_cache, pool, 2)
+    _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+    vp = ctypes.c_void_p
+    start, stop = events
+    _check(LIB.ssa_append_attention_static(
+        ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)), vp(_ptr(q)),
+        vp(_ptr(k_new)), vp(_ptr(v_new)), vp(_ptr(k_cache)), vp(_ptr(v_cache)),
+        vp(_ptr(block_table)), vp(_ptr(out)), vp(_stream(stream)),
+        vp(None if start is None else start.cuda_event),
+        vp(None if stop is None else stop.cuda_event)), "ssa_append_attention_static")
 
 
 def bind_plan(shape: SsaShape, q_len, ctx_len, tuning, out, info: SsaPlanInfo) -> BoundCall:
