@@ -228,6 +228,34 @@ __device__ __forceinline__ u32x4 keep_first(u32x4 v, int keep) {
   return r;
 }
 
+// 16-byte load into registers issued as inline assembly: the compiler does
+// not track it, and the caller waits for it with an exact count
+// (wait_loads) before any use.
+__device__ __forceinline__ u32x4 ld16_async(const void* p) {
+  u32x4 r;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return r;
+}
+// s_waitcnt vmcnt(N) that also makes the registers of the loads it waits for
+// valid for their uses (which the compiler may not schedule above it).
+template <int N, int M>
+__device__ __forceinline__ void wait_loads(u32x4 (&v)[M]) {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  if constexpr (M == 8)
+    asm volatile("s_waitcnt vmcnt(%8)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]),
+                   "+v"(v[6]), "+v"(v[7])
+                 : "n"(N)
+                 : "memory");
+  else if constexpr (M == 4)
+    asm volatile("s_waitcnt vmcnt(%4)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3])
+                 : "n"(N)
+                 : "memory");
+  else
+    static_assert(M == 4 || M == 8, "value fragments per block");
+}
+
 // XOR swizzle of the 16-byte chunk index of key row `key` in the LDS K block.
 // One ds_read_b128 of a K operand reads the same chunk of 16 rows, keys
 // 8*(r/4) + r%4 (+4 for the second half), r = 0..15; the swizzle sends them to
@@ -890,12 +918,6 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
 
 // --------------------------------------------------------------- decode splits
 
-template <int D>
-struct DecodeRegs {
-  bf16x8 k[2][Cfg<D>::KK];
-  u32x4 v[Cfg<D>::MT];
-};
-
 // v with its 16-bit element j (0..7; any other j: unchanged) replaced by e.
 __device__ __forceinline__ u32x4 set_elem(u32x4 v, int j, uint32_t e) {
   u32x4 r;
@@ -956,31 +978,56 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
       if (lane < C::CPR) kx = ld16(a.k_new + new_off + lane * 8);
     }
   }
-  auto load = [&](DecodeRegs<D>& R, int kb) {
+  // Key rows pass through LDS: each wave owns two stages of one 32-key block
+  // (the chunk path's swizzled row layout), filled with global_load_lds so
+  // that every load instruction reads whole key rows; the MFMA operands are
+  // then read from LDS in the permuted-key layout.  Value rows (dim-major
+  // pages) load straight into registers, 16 bytes of 8 slots of one dim per
+  // lane.  Both are issued as inline assembly and waited for with exact
+  // counts: one block's KLOADS copies and MT loads stay in flight while the
+  // block before it is computed.
+  constexpr int KLOADS = C::K_STAGE / 1024;
+  char* kst = lds + w * 2 * C::K_STAGE;
+  int kgo[KLOADS], kch[KLOADS];
+#pragma unroll
+  for (int r = 0; r < KLOADS; ++r) {
+    const int key = r * C::KROWS_PER_LOAD + lane / C::CPR;
+    kch[r] = (lane % C::CPR) ^ kswz<D>(key);
+    kgo[r] = (key & 15) * D + kch[r] * 8;
+  }
+  const int key0p = 8 * (r16 >> 2) + (r16 & 3);
+  const int swz = kswz<D>(key0p);
+  int kaddr[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) kaddr[kk] = key0p * C::K_ROW + (((kk * 4 + g) ^ swz) << 4);
+
+  auto issue = [&](int stage, int kb, u32x4 (&v)[MT]) {
     const int lp0 = kb >> 4;
     const int pg0 = bt[lp0];
     const int pg1 = (lp0 + 1 < rq.n_pages) ? bt[lp0 + 1] : pg0;
     const bool patch = has_new && kb + 32 > rq.ctx_len;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int key = 8 * (r16 >> 2) + 4 * h + (r16 & 3);
-      const uint16_t* src = a.kc + (size_t)((key >> 4) ? pg1 : pg0) * page_stride + head_off +
-                            (key & 15) * D + g * 8;
-      if (FUSED && patch && kb + key == rq.ctx_len) src = a.k_new + new_off + g * 8;
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) R.k[h][kk] = as_bf16x8(ld16(src + kk * 32));
+    for (int r = 0; r < KLOADS; ++r) {
+      const int key = r * C::KROWS_PER_LOAD + lane / C::CPR;
+      const uint16_t* src =
+          a.kc + (size_t)((key >> 4) ? pg1 : pg0) * page_stride + head_off + kgo[r];
+      if (FUSED && patch && kb + key == rq.ctx_len) src = a.k_new + new_off + kch[r] * 8;
+      dma16(src, kst + stage * C::K_STAGE + r * 1024);
     }
-    const uint16_t* src = a.vc + (size_t)((g >> 1) ? pg1 : pg0) * page_stride + head_off +
-                          r16 * 16 + (g & 1) * 8;
+    const uint16_t* vs = a.vc + (size_t)((g >> 1) ? pg1 : pg0) * page_stride + head_off +
+                         r16 * 16 + (g & 1) * 8;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) R.v[mt] = ld16(src + mt * 16 * 16);
+    for (int mt = 0; mt < MT; ++mt) v[mt] = ld16_async(vs + mt * 16 * 16);
   };
-  auto compute = [&](DecodeRegs<D>& R, int kb) {
+  // kb: the block's first key (past the item's keys for a padding block,
+  // whose stage and registers hold a copy of the last block: all masked)
+  auto compute = [&](int stage, int kb, u32x4 (&v)[MT]) {
+    const char* stk = kst + stage * C::K_STAGE;
     f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      s0 = mfma(R.k[0][kk], qop[kk], s0);
-      s1 = mfma(R.k[1][kk], qop[kk], s1);
+      s0 = mfma(as_bf16x8(ld16(stk + kaddr[kk])), qop[kk], s0);
+      s1 = mfma(as_bf16x8(ld16(stk + kaddr[kk] + 4 * C::K_ROW)), qop[kk], s1);
     }
     const float sv[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
     bf16x8 pop;
@@ -994,43 +1041,45 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
         for (int i = 0; i < 4; ++i) pk[i] = __builtin_amdgcn_ds_bpermute(4 * (r16 + 16 * i), (int)vpk);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
-          R.v[mt] = set_elem(R.v[mt], j, mt < 4 ? pk[mt] & 0xFFFFu : pk[mt & 3] >> 16);
+          v[mt] = set_elem(v[mt], j, mt < 4 ? pk[mt] & 0xFFFFu : pk[mt & 3] >> 16);
       }
     }
     if (kb + 32 > key1) {
       const int lim = key1 - (kb + 8 * g);  // key e of the lane group valid iff e < lim
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) R.v[mt] = keep_first(R.v[mt], lim);
+      for (int mt = 0; mt < MT; ++mt) v[mt] = keep_first(v[mt], lim);
       const unsigned valid = lim <= 0 ? 0u : (lim >= 8 ? 0xFFu : (1u << lim) - 1u);
       pop = softmax_step<MT, true>(sv, valid, a.scale_log2, m_run, l_run, o);
     } else {
       pop = softmax_step<MT, false>(sv, 0xFFu, a.scale_log2, m_run, l_run, o);
     }
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) o[mt] = mfma(as_bf16x8(R.v[mt]), pop, o[mt]);
+    for (int mt = 0; mt < MT; ++mt) o[mt] = mfma(as_bf16x8(v[mt]), pop, o[mt]);
   };
 
-  // Wave w takes blocks w, w+4, ...  The next block's loads are issued before
-  // the current block is computed; they are unconditional (clamped to the last
-  // block, an L2 hit, once the wave runs out) so that the code stays straight
-  // and the memory-counter waits only cover the block being computed.
+  // Wave w takes blocks w, w+4, ..., in pairs: every wave runs at least one
+  // pair, padded with masked blocks (loads clamped to the item's last block),
+  // so the loop has one exit and its accumulators one use each.  The next
+  // block's loads are issued before the current one is computed.
   const int nb = (key1 - it.key0 + 31) / 32;
-  DecodeRegs<D> R0, R1;
   const int wave = __builtin_amdgcn_readfirstlane(w);
-  int b = wave;
-  if (b < nb) {
-    load(R0, it.key0 + b * 32);
-    for (;;) {
-      load(R1, it.key0 + min(b + kWaves, nb - 1) * 32);
-      compute(R0, it.key0 + b * 32);
-      b += kWaves;
-      if (b >= nb) break;
-      load(R0, it.key0 + min(b + kWaves, nb - 1) * 32);
-      compute(R1, it.key0 + b * 32);
-      b += kWaves;
-      if (b >= nb) break;
-    }
+  const int nbw = nb > wave ? (nb - wave + kWaves - 1) / kWaves : 0;
+  const int n2 = nbw <= 2 ? 2 : (nbw + 1) / 2 * 2;
+  auto kb_load = [&](int i) { return it.key0 + min(wave + i * kWaves, nb - 1) * 32; };
+  auto kb_of = [&](int i) { return it.key0 + (wave + i * kWaves) * 32; };
+  constexpr int kIssue = KLOADS + MT;
+  vm_wait<0>();  // q and the new row have landed: the waits below count exactly
+  u32x4 v0[MT], v1[MT];
+  issue(0, kb_load(0), v0);
+  for (int i = 0; i < n2; i += 2) {
+    issue(1, kb_load(i + 1), v1);
+    wait_loads<kIssue>(v0);
+    compute(0, kb_of(i), v0);
+    issue(0, kb_load(i + 2), v0);
+    wait_loads<kIssue>(v1);
+    compute(1, kb_of(i + 1), v1);
   }
+  vm_wait<0>();  // the last (unused) copies have landed before LDS is reused
   l_run = wave_sum_cols(l_run);
   if constexpr (FUSED) {
     if (has_new && wave == 0) {
@@ -1046,7 +1095,9 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
     }
   }
 
-  // merge the 4 waves through LDS: per wave m[16], l[16], o[D][16]
+  // merge the 4 waves through LDS: per wave m[16], l[16], o[D][16] (over the
+  // staging area: every wave has left its loop)
+  __syncthreads();
   float* sm = reinterpret_cast<float*>(lds);
   float* wm = sm + w * (32 + 16 * D);
   if (g == 0) {
