@@ -920,17 +920,6 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
 
 // --------------------------------------------------------------- decode splits
 
-// v with its 16-bit element j (0..7; any other j: unchanged) replaced by e.
-__device__ __forceinline__ u32x4 set_elem(u32x4 v, int j, uint32_t e) {
-  u32x4 r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t lo = (v[i] & 0xFFFF0000u) | e, hi = (v[i] & 0x0000FFFFu) | (e << 16);
-    r[i] = j == 2 * i ? lo : (j == 2 * i + 1 ? hi : v[i]);
-  }
-  return r;
-}
-
 template <int D, bool FUSED>
 __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
                             char* lds) {
@@ -962,22 +951,33 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   // vector-memory wait before the K/V loads).  A page past the request's last
   // one is read from the first page instead (in bounds); keys from it are at or
   // beyond key1, so their logits are masked and their values zeroed in compute.
-  // In a fused launch the row of key u is taken from the new rows instead of
-  // the pool, and this item (the one of its kv head that holds key u) also
-  // appends it to the pool: no other workgroup reads that slot in the launch,
-  // so the decode never waits.
-  const bool has_new = FUSED && rq.q_len > 0 && it.key0 <= rq.ctx_len && rq.ctx_len < key1;
-  const size_t new_off = ((size_t)rq.q_start * a.hkv + it.kvh) * D;
-  // The new row in registers, loaded by every wave without waiting for it:
-  // vpk holds value dims lane (low half) and lane + 64 (high half, D = 128);
-  // kx, in lanes below D / 8, 16 bytes of the key row.
-  uint32_t vpk = 0;
-  u32x4 kx = {0, 0, 0, 0};
+  //
+  // In a fused launch the item that holds key u (its last key: u + 1 = key1)
+  // appends the request's new row to the pool itself, before its loop: the
+  // wave that owns the item's last block stores the key row and the value
+  // column of slot u and waits for the stores, so its own later reads of that
+  // block see them (the waves of a workgroup share one CU and its L1).  No
+  // other workgroup reads the slot in the launch, and other waves of this one
+  // read it only as masked padding, so the decode never waits on another
+  // workgroup and computes exactly what it computes after a separate append.
+  const int nb = (key1 - it.key0 + 31) / 32;
+  const int wave = __builtin_amdgcn_readfirstlane(w);
   if constexpr (FUSED) {
-    if (has_new) {
-      vpk = a.v_new[new_off + lane];
-      if (D > 64) vpk |= (uint32_t)a.v_new[new_off + 64 + lane] << 16;
-      if (lane < C::CPR) kx = ld16(a.k_new + new_off + lane * 8);
+    const bool has_new = rq.q_len > 0 && it.key0 <= rq.ctx_len && rq.ctx_len < key1;
+    if (has_new && wave == (nb - 1) % kWaves) {
+      const size_t new_off = ((size_t)rq.q_start * a.hkv + it.kvh) * D;
+      const size_t pg = (size_t)bt[rq.ctx_len >> 4] * page_stride + head_off;
+      const int slot = rq.ctx_len & 15;
+      uint16_t* kp = const_cast<uint16_t*>(a.kc) + pg;
+      uint16_t* vp = const_cast<uint16_t*>(a.vc) + pg;
+      if (lane < C::CPR) st16(kp + slot * D + lane * 8, ld16(a.k_new + new_off + lane * 8));
+      uint16_t vn[D / 64];
+#pragma unroll
+      for (int k = 0; k < D / 64; ++k) vn[k] = a.v_new[new_off + k * 64 + lane];
+#pragma unroll
+      for (int k = 0; k < D / 64; ++k) vp[(k * 64 + lane) * 16 + slot] = vn[k];
+      asm volatile("" ::: "memory");  // the stores are issued before the wait
+      vm_wait<0>();
     }
   }
   // Key rows pass through LDS: each wave owns two stages of one 32-key block
@@ -1007,14 +1007,11 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
     const int lp0 = kb >> 4;
     const int pg0 = bt[lp0];
     const int pg1 = (lp0 + 1 < rq.n_pages) ? bt[lp0 + 1] : pg0;
-    const bool patch = has_new && kb + 32 > rq.ctx_len;
 #pragma unroll
     for (int r = 0; r < KLOADS; ++r) {
       const int key = r * C::KROWS_PER_LOAD + lane / C::CPR;
-      const uint16_t* src =
-          a.kc + (size_t)((key >> 4) ? pg1 : pg0) * page_stride + head_off + kgo[r];
-      if (FUSED && patch && kb + key == rq.ctx_len) src = a.k_new + new_off + kch[r] * 8;
-      dma16(src, kst + stage * C::K_STAGE + r * 1024);
+      dma16(a.kc + (size_t)((key >> 4) ? pg1 : pg0) * page_stride + head_off + kgo[r],
+            kst + stage * C::K_STAGE + r * 1024);
     }
     const uint16_t* vs = a.vc + (size_t)((g >> 1) ? pg1 : pg0) * page_stride + head_off +
                          r16 * 16 + (g & 1) * 8;
@@ -1033,19 +1030,6 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
     }
     const float sv[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
     bf16x8 pop;
-    if constexpr (FUSED) {
-      if (has_new && kb + 32 > rq.ctx_len) {
-        // the lane's 8 value slots are keys kb + 8 g .. kb + 8 g + 7; its dims
-        // r16 + 16 mt sit in lane r16 + 16 (mt % 4), half mt / 4, of vpk
-        const int j = rq.ctx_len - (kb + 8 * g);
-        uint32_t pk[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) pk[i] = __builtin_amdgcn_ds_bpermute(4 * (r16 + 16 * i), (int)vpk);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-          v[mt] = set_elem(v[mt], j, mt < 4 ? pk[mt] & 0xFFFFu : pk[mt & 3] >> 16);
-      }
-    }
     if (kb + 32 > key1) {
       const int lim = key1 - (kb + 8 * g);  // key e of the lane group valid iff e < lim
 #pragma unroll
@@ -1063,14 +1047,12 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   // pair, padded with masked blocks (loads clamped to the item's last block),
   // so the loop has one exit and its accumulators one use each.  The next
   // block's loads are issued before the current one is computed.
-  const int nb = (key1 - it.key0 + 31) / 32;
-  const int wave = __builtin_amdgcn_readfirstlane(w);
   const int nbw = nb > wave ? (nb - wave + kWaves - 1) / kWaves : 0;
   const int n2 = nbw <= 2 ? 2 : (nbw + 1) / 2 * 2;
   auto kb_load = [&](int i) { return it.key0 + min(wave + i * kWaves, nb - 1) * 32; };
   auto kb_of = [&](int i) { return it.key0 + (wave + i * kWaves) * 32; };
   constexpr int kIssue = KLOADS + MT;
-  vm_wait<0>();  // q and the new row have landed: the waits below count exactly
+  vm_wait<0>();  // q has landed: the waits below count exactly
   u32x4 v0[MT], v1[MT];
   issue(0, kb_load(0), v0);
   for (int i = 0; i < n2; i += 2) {
@@ -1083,20 +1065,6 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   }
   vm_wait<0>();  // the last (unused) copies have landed before LDS is reused
   l_run = wave_sum_cols(l_run);
-  if constexpr (FUSED) {
-    if (has_new && wave == 0) {
-      // append the new row: key row and the value column of slot u (a fused
-      // launch passes pools it may write)
-      const size_t pg = (size_t)bt[rq.ctx_len >> 4] * page_stride + head_off;
-      const int slot = rq.ctx_len & 15;
-      uint16_t* kp = const_cast<uint16_t*>(a.kc) + pg;
-      uint16_t* vp = const_cast<uint16_t*>(a.vc) + pg;
-      if (lane < C::CPR) st16(kp + slot * D + lane * 8, kx);
-      vp[lane * 16 + slot] = (uint16_t)vpk;
-      if (D > 64) vp[(lane + 64) * 16 + slot] = (uint16_t)(vpk >> 16);
-    }
-  }
-
   // merge the 4 waves through LDS: per wave m[16], l[16], o[D][16] (over the
   // staging area: every wave has left its loop)
   __syncthreads();
