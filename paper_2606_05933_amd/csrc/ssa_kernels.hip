@@ -396,55 +396,102 @@ struct RecordReader {
     return __builtin_bit_cast(
         float, __builtin_amdgcn_raw_buffer_load_b32(rsrc, (int)(float_off * 4), 0, kCachePolicySc1));
   }
+  // four floats at a 16-byte aligned float offset
+  __device__ f32x4 quad(int64_t float_off) const {
+    return __builtin_bit_cast(
+        f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)(float_off * 4), 0, kCachePolicySc1));
+  }
 };
 
 // Last arriver of a merge group: combine the split records in split order.
+// Thread t takes the (column, four dims) units t, t + 256, ...: U of them per
+// pass, consecutive lanes on consecutive 16-byte pieces of o.  The merge is
+// latency bound (the records come from the device coherence point), so each
+// round issues the loads of F splits for all U units before it uses any:
+// first the maxima, then the weighted sums in split order.
+template <int D, int U, int F1, int F2>
+__device__ void merge_pass(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
+                           const RecordReader& rd, int C, int S, int u0) {
+  constexpr int UPC = D / 4;  // units per column
+  const int units = C * UPC;
+  const int64_t rec = rec_floats(C, D), o_off = rec_o_off(C);
+  int col[U], d0[U];
+#pragma unroll
+  for (int j = 0; j < U; ++j) {
+    const int idx = min(u0 + j * kThreads + (int)threadIdx.x, units - 1);
+    col[j] = idx / UPC;
+    d0[j] = (idx % UPC) * 4;
+  }
+  float M[U];
+#pragma unroll
+  for (int j = 0; j < U; ++j) M[j] = kNegInf;
+  for (int s0 = 0; s0 < S; s0 += F1) {
+    float ms[F1][U];
+#pragma unroll
+    for (int f = 0; f < F1; ++f)
+#pragma unroll
+      for (int j = 0; j < U; ++j) ms[f][j] = s0 + f < S ? rd((s0 + f) * rec + col[j]) : kNegInf;
+#pragma unroll
+    for (int f = 0; f < F1; ++f)
+#pragma unroll
+      for (int j = 0; j < U; ++j) M[j] = fmaxf(M[j], ms[f][j]);
+  }
+  float L[U];
+  f32x4 acc[U];
+#pragma unroll
+  for (int j = 0; j < U; ++j) {
+    L[j] = 0.f;
+    acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int s0 = 0; s0 < S; s0 += F2) {
+    float ms[F2][U], ls[F2][U];
+    f32x4 os[F2][U];
+#pragma unroll
+    for (int f = 0; f < F2; ++f) {
+      const int64_t r = (int64_t)(s0 + f) * rec;
+      const bool in = s0 + f < S;
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        ms[f][j] = in ? rd(r + col[j]) : kNegInf;
+        ls[f][j] = in ? rd(r + C + col[j]) : 0.f;
+        os[f][j] = in ? rd.quad(r + o_off + (int64_t)col[j] * D + d0[j]) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int f = 0; f < F2; ++f) {
+      if (s0 + f >= S) break;
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const float w = (ms[f][j] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(ms[f][j] - M[j]);
+        L[j] += w * ls[f][j];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc[j][k] += w * os[f][j][k];
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < U; ++j) {
+    if (u0 + j * kThreads + (int)threadIdx.x >= units) break;
+    const float inv = 1.f / L[j];
+    int row, head;
+    col_target(it, rq, a.G, col[j], row, head);
+    store_bf16x4(a.out + ((size_t)row * a.hq + head) * D + d0[j], acc[j][0] * inv,
+                 acc[j][1] * inv, acc[j][2] * inv, acc[j][3] * inv);
+  }
+}
+
 template <int D>
 __device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
                             const MergeGroup& grp) {
   const RecordReader rd(reinterpret_cast<const float*>(a.ws + a.ws_partials_off) + grp.ws_off);
   const int C = grp.ncols, S = grp.nsplit;
-  const int64_t rec = (int64_t)C * (D + 2);
-  for (int idx = threadIdx.x; idx < C * (D / 4); idx += kThreads) {
-    const int col = idx / (D / 4);
-    const int d0 = (idx % (D / 4)) * 4;
-    // the splits' maxima, eight in flight
-    float M = kNegInf;
-    for (int s0 = 0; s0 < S; s0 += 8) {
-      float ms[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) ms[j] = s0 + j < S ? rd((s0 + j) * rec + col) : kNegInf;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) M = fmaxf(M, ms[j]);
-    }
-    // weights and sums in split order, four splits' records in flight
-    float L = 0.f;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < S; s0 += 4) {
-      float ms[4], ls[4], os[4][4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int64_t r = (int64_t)(s0 + j) * rec;
-        const bool in = s0 + j < S;
-        ms[j] = in ? rd(r + col) : kNegInf;
-        ls[j] = in ? rd(r + C + col) : 0.f;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) os[j][k] = in ? rd(r + 2 * C + (int64_t)col * D + d0 + k) : 0.f;
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (s0 + j >= S) break;
-        const float w = (ms[j] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(ms[j] - M);
-        L += w * ls[j];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) acc[k] += w * os[j][k];
-      }
-    }
-    const float inv = 1.f / L;
-    int row, head;
-    col_target(it, rq, a.G, col, row, head);
-    store_bf16x4(a.out + ((size_t)row * a.hq + head) * D + d0, acc[0] * inv, acc[1] * inv,
-                 acc[2] * inv, acc[3] * inv);
+  const int units = C * (D / 4);
+  if (units >= 4 * kThreads) {
+    // chunk tiles: few splits, many units
+    for (int u0 = 0; u0 < units; u0 += 4 * kThreads) merge_pass<D, 4, 4, 2>(a, it, rq, rd, C, S, u0);
+  } else {
+    // decode splits and narrow tiles: many splits, few units
+    for (int u0 = 0; u0 < units; u0 += kThreads) merge_pass<D, 1, 8, 8>(a, it, rq, rd, C, S, u0);
   }
 }
 
@@ -898,7 +945,7 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + a.off_groups)[it.group];
     const int Cn = grp.ncols;
     float* rec = reinterpret_cast<float*>(a.ws + a.ws_partials_off) + grp.ws_off +
-                 (int64_t)it.split * Cn * (D + 2);
+                 (int64_t)it.split * rec_floats(Cn, D);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int col = wc0 + nt * 16 + r16;
@@ -912,7 +959,7 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj)
-          st_dev(rec + 2 * Cn + (int64_t)cl * D + mt * 16 + 4 * g + jj, o[nt][mt][jj]);
+          st_dev(rec + rec_o_off(Cn) + (int64_t)cl * D + mt * 16 + 4 * g + jj, o[nt][mt][jj]);
     }
     finish_split<D>(a, it, rq, lds);
   }
@@ -1084,7 +1131,7 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   if (it.group >= 0) {
     const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + a.off_groups)[it.group];
     rec = reinterpret_cast<float*>(a.ws + a.ws_partials_off) + grp.ws_off +
-          (int64_t)it.split * G * (D + 2);
+          (int64_t)it.split * rec_floats(G, D);
   }
   for (int idx = tid; idx < G * (D / 4); idx += kThreads) {
     const int col = idx % G;
@@ -1108,7 +1155,7 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
         st_dev(rec + G + col, L);
       }
 #pragma unroll
-      for (int k = 0; k < 4; ++k) st_dev(rec + 2 * G + (int64_t)col * D + d0 + k, acc[k]);
+      for (int k = 0; k < 4; ++k) st_dev(rec + rec_o_off(G) + (int64_t)col * D + d0 + k, acc[k]);
     } else {
       const float inv = 1.f / L;
       store_bf16x4(a.out + ((size_t)rq.q_start * a.hq + it.kvh * G + col) * D + d0,

@@ -372,7 +372,7 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   int64_t ws_floats = 0;
   auto add_group = [&](int nsplit, int ncols) {
     MergeGroup g{nsplit, ncols, ws_floats};
-    ws_floats += (int64_t)nsplit * ncols * (D + 2);
+    ws_floats += (int64_t)nsplit * rec_floats(ncols, D);
     p->groups.push_back(g);
     return (int32_t)p->groups.size() - 1;
   };

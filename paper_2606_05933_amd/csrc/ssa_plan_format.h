@@ -9,15 +9,17 @@
 // counters, the sticky status word of ssa.h, one spare) and one int32 ticket
 // per merge group (counters and tickets zero at rest), padded to 256 bytes, then,
 // at ws_partials_off, fp32 partial results:
-// for merge group g and split s, a record of ncols * (D + 2) floats at float
-// offset ws_off + s * ncols * (D + 2): m[ncols], l[ncols], o[ncols][D].
+// for merge group g and split s, a record of rec_floats(ncols, D) floats at
+// float offset ws_off + s * rec_floats(ncols, D): m[ncols], l[ncols], padding
+// to a multiple of four floats, o[ncols][D] (so that every o row, like every
+// record, starts 16-byte aligned).
 #pragma once
 #include <stdint.h>
 
 namespace ssa {
 
 constexpr uint32_t kPlanMagic = 0x31415353u;  // "SSA1"
-constexpr uint32_t kPlanVersion = 3;
+constexpr uint32_t kPlanVersion = 4;
 constexpr int kBlockKeys = 32;  // keys per attention block: two 16-slot pages
 constexpr int kWaves = 4;       // waves per workgroup
 constexpr int kThreads = 256;   // threads per workgroup
@@ -25,6 +27,10 @@ constexpr int kChunkWaveCols = 32;  // columns a wave owns in a chunk tile
 constexpr int kLaunchCounters = 4;  // workspace words ahead of the merge tickets
 constexpr int kWsStatusWord = 2;    // the status word among them (ssa.h)
 constexpr int kDefaultWaitPolls = 1 << 21;
+
+// Float offset of o in a partial record of ncols columns, and the record's size.
+constexpr int64_t rec_o_off(int ncols) { return ((int64_t)2 * ncols + 3) / 4 * 4; }
+constexpr int64_t rec_floats(int ncols, int d) { return rec_o_off(ncols) + (int64_t)ncols * d; }
 
 enum ItemKind : int32_t { kItemChunk = 0, kItemDecode = 1 };
 
