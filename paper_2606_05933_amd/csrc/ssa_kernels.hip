@@ -714,11 +714,11 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) kaddr[kk] = key0 * C::K_ROW + (((kk * 4 + g) ^ sw) << 4);
   // Value pages sit in LDS page-major, as in HBM: page half h of the block,
-  // row d, 16 slots (32 bytes).  The two 16-byte halves of a row are swapped
-  // when vswz(d) is set, so that the A-operand reads of one MFMA (16 rows,
-  // one half each) hit distinct bank slots.
-  auto vswz = [](int d) { return ((d >> 2) ^ (d >> 3)) & 1; };
-  const int vaddr = C::K_STAGE + (g >> 1) * C::V_PAGE + r16 * 32 + (((g & 1) ^ vswz(r16)) << 4);
+  // row d, 16 slots (32 bytes), unswizzled.  A lane reads 16 bytes of row r16:
+  // measured with the LDS bank-conflict counter, this pattern (rows 32 bytes
+  // apart, halves by lane group) is conflict-free on gfx950, while swapping
+  // the halves of some rows costs a second pass on every read.
+  const int vaddr = C::K_STAGE + (g >> 1) * C::V_PAGE + r16 * 32 + ((g & 1) << 4);
 
   // Staging of one 32-key block, global -> LDS without registers
   // (global_load_lds_dwordx4): load r of wave w fills 1 KB of the stage,
@@ -737,7 +737,7 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     const int ch = (lane % C::CPR) ^ kswz<D>(key);
     kgo[r] = (key & 15) * D + ch * 8;
     const int d = (m * 32) % D + (lane >> 1);
-    vgo[r] = d * 16 + (((lane & 1) ^ vswz(d)) << 3);
+    vgo[r] = d * 16 + ((lane & 1) << 3);
   }
   // In a fused launch the blocks from the first one holding keys >= u on are
   // copied at device scope (COH), after one wait for the appending workgroups
@@ -767,7 +767,7 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
     for (int k = 0; k < D / 64; ++k) {
       const int idx = tid + k * kThreads;  // (page half, row, 16-byte half)
       const int h = idx / (2 * D), d = (idx >> 1) % D, j = idx & 1;
-      const int keep = nv - (h * 16 + ((j ^ vswz(d)) << 3));
+      const int keep = nv - (h * 16 + (j << 3));
       char* p = stage + C::K_STAGE + h * C::V_PAGE + d * 32 + j * 16;
       if (keep < 8) st16(p, keep <= 0 ? u32x4{0, 0, 0, 0} : keep_first(ld16(p), keep));
     }
