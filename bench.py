@@ -23,7 +23,11 @@ on this host on a bounded sample (a reported baseline, not the target).
 Other modes (all single GPU):
   --sweep OUT        latency-vs-chunk-size table of every workload (JSON lines)
   --copy-probe       plain 1 GiB device copies (the scale of the traffic counters)
-  --only-attention   time the attention launch alone (for counter runs)
+  --only-attention   time the attention launch alone (for counter runs; with
+                     --fused, the fused launch); --workload, --scene pick the batch
+  --pmc-md OUT --pmc-md-dir DIR --pmc-kernel K --pmc-cmd CMD
+                     markdown summary of the rocprofv3 counter passes (PMC_PASSES),
+                     kernel trace and copy-probe scale collected under DIR
   --traffic-json OUT --traffic-json-inputs F W CF CW
                      HBM traffic summary from rocprofv3 FETCH_SIZE / WRITE_SIZE CSVs
   --sweep-md JSONL   markdown tables of a --sweep file
@@ -596,13 +600,125 @@ def main_only_attention(args):
     elif args.scene == "prefill":
         b = workload.sub_batch(b, b.q_len > 1)
     db = DeviceBatch(b)
-    db.kv_append()
-    torch.cuda.synchronize()
-    us = time_kernel_events(db.attention, args.steps) * 1e6
     info = db.info
-    print(json.dumps({"workload": args.workload, "scene": args.scene, "attention_us": round(us, 2),
-                      "algorithmic_bytes": info.decode_bytes + info.chunk_bytes,
+    if args.fused:
+        # the fused launch appends the rows itself: the algorithmic bytes add them
+        us = time_kernel_events(db.step_fused, args.steps) * 1e6
+        assert db.status() == 0, "the fused launch reported an error"
+        kernel, nbytes = "append_attention_kernel", info.decode_bytes + info.chunk_bytes + info.append_bytes
+    else:
+        db.kv_append()
+        torch.cuda.synchronize()
+        us = time_kernel_events(db.attention, args.steps) * 1e6
+        kernel, nbytes = "mixed_attention_kernel", info.decode_bytes + info.chunk_bytes
+    print(json.dumps({"workload": args.workload, "scene": args.scene, "kernel": kernel,
+                      "kernel_us": round(us, 2), "algorithmic_bytes": nbytes,
                       "chunk_flops": info.chunk_flops, "launches": args.steps}), flush=True)
+
+
+# Counter passes of a --pmc-md summary: rocprofv3 collects one pass per run
+# (per-block counter limits), each into DIR/<pass>/run_counter_collection.csv.
+PMC_PASSES = {
+    "a": "SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_MFMA SQ_BUSY_CU_CYCLES "
+         "SQ_INSTS_VALU SQ_ACTIVE_INST_VALU SQ_WAVES GRBM_GUI_ACTIVE",
+    "b": "SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_WAIT_INST_LDS "
+         "SQ_INSTS_VALU_TRANS_F32 SQ_WAVE_CYCLES GRBM_GUI_ACTIVE",
+    "c": "FETCH_SIZE",
+    "d": "WRITE_SIZE",
+}
+NUM_XCC, NUM_SIMD = 8, 1024  # MI355X: 8 dies, 256 CUs x 4 SIMDs
+
+
+def _pmc_means(path, kernel):
+    """Per-dispatch sums of every counter of the kernel's dispatches, averaged."""
+    import collections
+    import csv
+    per = collections.defaultdict(lambda: collections.defaultdict(float))
+    for r in csv.DictReader(open(path)):
+        if kernel in r["Kernel_Name"]:
+            per[r["Dispatch_Id"]][r["Counter_Name"]] += float(r["Counter_Value"])
+    if not per:
+        raise SystemExit(f"no dispatches of {kernel} in {path}")
+    names = set().union(*[set(d) for d in per.values()])
+    return {k: statistics.mean(d[k] for d in per.values()) for k in names}, len(per)
+
+
+def main_pmc_md(args):
+    """Markdown summary of the counter passes of one kernel (see PMC_PASSES),
+    its kernel-trace statistics and the copy probe's traffic scale."""
+    import csv
+    d, kernel = args.pmc_md_dir, args.pmc_kernel
+    m, nd = {}, {}
+    for p in PMC_PASSES:
+        vals, n = _pmc_means(os.path.join(d, p, "run_counter_collection.csv"), kernel)
+        m.update(vals)
+        nd[p] = n
+    stats = [r for r in csv.DictReader(open(os.path.join(d, "t", "run_kernel_stats.csv")))
+             if kernel in r["Name"]]
+    if not stats:
+        raise SystemExit(f"no trace statistics of {kernel}")
+    calls = int(stats[0]["Calls"])
+    dur_ns = float(stats[0]["AverageNs"])
+    cf, _ = _pmc_means(os.path.join(d, "e", "run_counter_collection.csv"), "copyBuffer")
+    cw, _ = _pmc_means(os.path.join(d, "f", "run_counter_collection.csv"), "copyBuffer")
+    copy_kib = float(1 << 20)
+    f_fac, w_fac = cf["FETCH_SIZE"] / copy_kib, cw["WRITE_SIZE"] / copy_kib
+    run = None
+    for line in open(os.path.join(d, "t.log")):
+        if line.startswith("{"):
+            run = json.loads(line)
+    gui = m["GRBM_GUI_ACTIVE"] / NUM_XCC  # cycles of one die while the kernel ran
+    clock = gui / dur_ns
+    mops = m.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512
+    busy = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui * NUM_SIMD)
+    fetch = m["FETCH_SIZE"] * 1024 / f_fac
+    write = m["WRITE_SIZE"] * 1024 / w_fac
+    alg_bytes = run["algorithmic_bytes"] if run else None
+    alg_flops = run["chunk_flops"] if run else None
+    cmd = args.pmc_cmd
+    rows = [
+        ("dispatches (trace / counter passes a, b, c, d)", f"{calls} / {nd['a']}, {nd['b']}, {nd['c']}, {nd['d']}"),
+        ("kernel duration, trace average", f"{dur_ns / 1e3:.1f} us"),
+        ("GRBM_GUI_ACTIVE per die", f"{gui:.4g} cycles -> clock {clock:.3f} GHz"),
+        ("MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES / (GUI per die x 1024 SIMDs)", f"{busy:.3f}"),
+        ("MFMA flops: 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16", f"{mops:.4g}"
+         + (f" (algorithmic {alg_flops:.4g})" if alg_flops else "")),
+        ("MFMA rate over the trace duration", f"{mops / dur_ns / 1e3:.1f} TFLOP/s = "
+         f"{mops / dur_ns / 1e3 / MFMA_BF16_PEAK_TFLOPS:.3f} of {MFMA_BF16_PEAK_TFLOPS:.0f}"
+         f" ({mops / dur_ns / 1e3 / (MFMA_BF16_PEAK_TFLOPS * clock / 2.4):.3f} of the peak at {clock:.2f} GHz)"),
+        ("SQ_INSTS_MFMA / SQ_WAVES", f"{m['SQ_INSTS_MFMA']:.4g} / {m['SQ_WAVES']:.0f}"),
+        ("SQ_BUSY_CU_CYCLES / (GUI per die x 256 CUs)", f"{m['SQ_BUSY_CU_CYCLES'] / (gui * 256):.3f}"),
+        ("VALU instructions, SQ_ACTIVE_INST_VALU (quad-cycles)", f"{m['SQ_INSTS_VALU']:.4g}, {m['SQ_ACTIVE_INST_VALU']:.4g}"),
+        ("transcendental f32 instructions", f"{m['SQ_INSTS_VALU_TRANS_F32']:.4g}"),
+        ("LDS instructions", f"{m['SQ_INSTS_LDS']:.4g}"),
+        ("LDS bank-conflict cycles / LDS active cycles", f"{m['SQ_LDS_BANK_CONFLICT']:.4g} / "
+         f"{m['SQ_LDS_IDX_ACTIVE']:.4g} = {m['SQ_LDS_BANK_CONFLICT'] / max(m['SQ_LDS_IDX_ACTIVE'], 1):.3f}"),
+        ("bank-conflict cycles per LDS instruction", f"{m['SQ_LDS_BANK_CONFLICT'] / max(m['SQ_INSTS_LDS'], 1):.2f}"),
+        ("FETCH_SIZE, WRITE_SIZE (KiB per dispatch)", f"{m['FETCH_SIZE']:.6g}, {m['WRITE_SIZE']:.6g}"),
+        ("copy probe scale (counter KiB per KiB copied): fetch, write", f"{f_fac:.4f}, {w_fac:.4f}"),
+        ("HBM bytes per dispatch (scaled): fetch + write", f"{fetch / 1e6:.1f} + {write / 1e6:.1f} MB"
+         + (f" (algorithmic {alg_bytes / 1e6:.1f} MB, ratio {(fetch + write) / alg_bytes:.3f})" if alg_bytes else "")),
+        ("HBM rate over the trace duration", f"{(fetch + write) / dur_ns:.0f} GB/s = "
+         f"{(fetch + write) / dur_ns / HBM_PEAK_GBS:.3f} of {HBM_PEAK_GBS:.0f}"),
+    ]
+    out = [f"# {args.pmc_title}", "",
+           f"Kernel `{kernel}`; counters averaged over its dispatches.  Workload: "
+           + (DESCR.get(run['workload'], run['workload']) + f", scene {run['scene']}" if run else "?") + ".", "",
+           "| quantity | value |", "|---|---|"]
+    out += [f"| {k} | {v} |" for k, v in rows]
+    out += ["", "Commands (from the repository root, after `cd /tmp && export TMPDIR=/tmp` and back):", "", "```"]
+    for p, cs in PMC_PASSES.items():
+        out.append(f"rocprofv3 --pmc {cs} -d DIR/{p} -o run --output-format csv -- {cmd}")
+    out.append(f"rocprofv3 --kernel-trace --stats -d DIR/t -o run --output-format csv -- {cmd} > DIR/t.log")
+    out.append("rocprofv3 --pmc FETCH_SIZE -d DIR/e -o run --output-format csv -- python3 bench.py --copy-probe --steps 3")
+    out.append("rocprofv3 --pmc WRITE_SIZE -d DIR/f -o run --output-format csv -- python3 bench.py --copy-probe --steps 3")
+    out.append(f"python3 bench.py --pmc-md OUT.md --pmc-md-dir DIR --pmc-kernel {kernel} "
+               f"--pmc-cmd '{cmd}' --pmc-title '{args.pmc_title}'")
+    out += ["```", ""]
+    text = "\n".join(out)
+    with open(args.pmc_md, "w") as f:
+        f.write(text)
+    print(text)
 
 
 def _pmc_rows(path, counter):
@@ -1253,6 +1369,14 @@ def main():
     ap.add_argument("--sweep-workloads", default=None)
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--only-attention", action="store_true")
+    ap.add_argument("--fused", action="store_true",
+                    help="with --only-attention: time the fused launch instead")
+    ap.add_argument("--pmc-md", metavar="OUT", default=None,
+                    help="markdown summary of rocprofv3 counter passes (see PMC_PASSES)")
+    ap.add_argument("--pmc-md-dir", default=None)
+    ap.add_argument("--pmc-kernel", default="mixed_attention_kernel")
+    ap.add_argument("--pmc-cmd", default="python3 bench.py --only-attention")
+    ap.add_argument("--pmc-title", default="Counter summary")
     ap.add_argument("--traffic-json", metavar="OUT", default=None,
                     help="write the HBM traffic summary from four rocprofv3 counter CSVs")
     ap.add_argument("--traffic-json-inputs", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH",
@@ -1285,6 +1409,8 @@ def main():
         return main_traffic_json(args)
     if args.sweep_md:
         return main_sweep_md(args)
+    if args.pmc_md:
+        return main_pmc_md(args)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU: this attention path has no multi-GPU mode "

@@ -856,14 +856,11 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   // MFMA accumulates in place.  Blocks past the item's last one are masked for
   // every column (their stages hold copies of the last block, value tails
   // zeroed: a zero probability times a zero value adds nothing).
-  auto block = [&](auto masked_t, auto sv_t, int b, bool coh) {
+  auto block = [&](auto masked_t, auto coh_t, auto sv_t, int b) {
     constexpr int SV = decltype(sv_t)::value;
     const int bf = min(b + S - 1, nb - 1);
     char* fst = lds + ((SV + S - 1) % S) * C::STAGE;
-    if (FUSED && coh)
-      dma(std::true_type{}, it.key0 + bf * 32, fst);
-    else
-      dma(std::false_type{}, it.key0 + bf * 32, fst);
+    dma(coh_t, it.key0 + bf * 32, fst);
     const int kn = it.key0 + min(b + 1, nb - 1) * 32;
     if (kn + 32 > nvalid) zero_tail(kn, lds + ((SV + 1) % S) * C::STAGE);
     const int kb = it.key0 + b * 32;
@@ -909,19 +906,37 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
   // Trips of S iterations: unmasked while both blocks an iteration softmaxes
   // (b and b+1) are visible to every column, then masked up to the item's
   // block count rounded up to a trip.  One exit per loop, after whole trips.
+  // In a fused launch the trips from b_coh on (when it lies inside the item)
+  // copy at device scope, after one wait; each (masked, coherent) kind of trip
+  // has a loop of its own, so no trip branches on either.
   const int n_um = b_vis >= 1 ? (b_vis - 1) / S * S : 0;
   const int nb_pad = (nb + S - 1) / S * S;
-  auto trip = [&](auto masked_t, int b0) {
-    if (FUSED && b0 == b_coh && b_coh < nb && !coh_prologue) wait_appended(a);
-    const bool coh = FUSED && b0 >= b_coh && b_coh < nb;
-    block(masked_t, Stage<0>{}, b0, coh);
-    block(masked_t, Stage<1>{}, b0 + 1, coh);
-    block(masked_t, Stage<2>{}, b0 + 2, coh);
-    block(masked_t, Stage<3>{}, b0 + 3, coh);
+  const int nc_end = (FUSED && b_coh < nb) ? b_coh : nb_pad;  // end of the plain trips
+  auto trip = [&](auto masked_t, auto coh_t, int b0) {
+    block(masked_t, coh_t, Stage<0>{}, b0);
+    block(masked_t, coh_t, Stage<1>{}, b0 + 1);
+    block(masked_t, coh_t, Stage<2>{}, b0 + 2);
+    block(masked_t, coh_t, Stage<3>{}, b0 + 3);
   };
+  using No = std::false_type;
+  using Yes = std::true_type;  // trip(masked?, coherent?, first block)
+  bool waited = coh_prologue;
   int b = 0;
-  for (; b < n_um; b += S) trip(std::false_type{}, b);
-  for (; b < nb_pad; b += S) trip(std::true_type{}, b);
+  for (const int e = min(n_um, nc_end); b < e; b += S) trip(No{}, No{}, b);
+  if constexpr (FUSED) {
+    if (b < n_um) {
+      if (!waited) wait_appended(a);
+      waited = true;
+      for (; b < n_um; b += S) trip(No{}, Yes{}, b);
+    }
+  }
+  for (; b < nc_end; b += S) trip(Yes{}, No{}, b);
+  if constexpr (FUSED) {
+    if (b < nb_pad) {
+      if (!waited) wait_appended(a);
+      for (; b < nb_pad; b += S) trip(Yes{}, Yes{}, b);
+    }
+  }
   lds_dma_wait();  // no copy may land after this workgroup has left
 
   // epilogue
