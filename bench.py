@@ -601,6 +601,8 @@ def main_only_attention(args):
         b = workload.sub_batch(b, b.q_len > 1)
     db = DeviceBatch(b)
     info = db.info
+    for _ in range(3):  # warm-up launches (the trace statistics include them)
+        db.step_fused() if args.fused else db.attention()
     if args.fused:
         # the fused launch appends the rows itself: the algorithmic bytes add them
         us = time_kernel_events(db.step_fused, args.steps) * 1e6
@@ -746,8 +748,8 @@ def main_traffic_json(args):
            "kernel_source_sha256": sha256_file(KERNEL_SRC),
            "fetch_kib": round(f_kib, 1), "write_kib": round(w_kib, 1), "dispatches": [n_f, n_w],
            "copy_fetch_factor": round(cf / copy_kib, 4), "copy_write_factor": round(cw / copy_kib, 4),
-           "commands": ["rocprofv3 --pmc FETCH_SIZE --output-format csv -- python3 bench.py --no-cpu-baseline",
-                        "rocprofv3 --pmc WRITE_SIZE --output-format csv -- python3 bench.py --no-cpu-baseline",
+           "commands": [f"rocprofv3 --pmc FETCH_SIZE --output-format csv -- {args.pmc_cmd}",
+                        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -- {args.pmc_cmd}",
                         "rocprofv3 --pmc FETCH_SIZE --output-format csv -- python3 bench.py --copy-probe --steps 3",
                         "rocprofv3 --pmc WRITE_SIZE --output-format csv -- python3 bench.py --copy-probe --steps 3"]}
     out["traffic_bytes"] = round((out["fetch_kib"] / out["copy_fetch_factor"]
