@@ -45,6 +45,15 @@ int ssa_rope_append(const ssa_shape* shape, const void* plan_host, const void* p
                     uint16_t* q_out, uint16_t* k_cache, uint16_t* v_cache,
                     const int32_t* block_table, void* stream);
 
+/*
+ * The rotary table of ssa_rope_append, on the host: out [max_position, d] fp32
+ * (caller's buffer), row p = cos(p t_i) for i < d/2, then sin(p t_i), with
+ * t_i = base^(-2i/d); angles and functions in fp64, each entry rounded once to
+ * fp32.  Errors: SSA_ERR_NULL (out); SSA_ERR_ARG (max_position < 1, d < 2 or
+ * odd, base <= 1 or not finite).  Allocates nothing.
+ */
+int ssa_rope_table(int32_t max_position, int32_t d, double base, float* out);
+
 /* Epilogues of ssa_linear. */
 enum {
   SSA_EPILOGUE_NONE = 0,     /* out = x W^T                                   [M, N] */

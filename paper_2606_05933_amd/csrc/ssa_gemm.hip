@@ -30,46 +30,15 @@
 #include <algorithm>
 
 #include "../../include/ssa_layer.h"
+#include "ssa_device.h"
 
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+using namespace ssa_dev;
 
 constexpr int kNormThreads = 256;
 constexpr int BK = 64;  // K block: one 128-byte LDS row per operand row
 constexpr int kXcds = 8;
 constexpr float kLog2e = 1.4426950408889634f;
-
-// One wave-wide global -> LDS copy: lane i's 16 bytes from g land at l + 16 i
-// (l wave-uniform).  Readers wait for it explicitly (vm_wait, then a barrier).
-__device__ __forceinline__ void dma16(const void* g, const char* l) {
-  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)l;
-  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(a) : "memory");
-}
-// s_waitcnt vmcnt(N): all but this wave's N most recent vector-memory
-// operations have completed.
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-__device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-__device__ __forceinline__ uint32_t pack2(float a, float b) {
-  f32x2 v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-}
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // Split partials cross workgroups and XCDs (whose L2s are not coherent with
 // each other): device-scope 8-byte stores, device-coherent loads (below), a

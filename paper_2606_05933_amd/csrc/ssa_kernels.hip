@@ -45,6 +45,7 @@
 #include <type_traits>
 
 #include "../../include/ssa.h"
+#include "ssa_device.h"
 #include "ssa_plan_format.h"
 
 namespace ssa {
@@ -53,42 +54,12 @@ int check_plan(const ssa_shape* s, const void* plan_host, const PlanHeader** out
 
 namespace {
 using namespace ssa;
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+using namespace ssa_dev;
 
 // Block-table and plan reads go through the constant address space: the
 // kernels never write them, and wave-uniform reads then become scalar loads,
 // which are not ordered with the vector loads of K/V pages.
 typedef const __attribute__((address_space(4))) int32_t cint32;
-
-// One wave-wide global -> LDS copy of 16 bytes per lane (gfx950
-// global_load_lds_dwordx4): lane i's 16 bytes from g land at LDS address
-// l + 16 i.  It is issued as inline assembly so that the compiler's memory
-// counter tracking does not make later reads of *other* LDS stages wait for
-// it; every reader of the destination waits explicitly (lds_dma_wait before
-// the barrier that publishes the stage).
-// COHERENT reads at device scope (sc1): rows appended in the same launch.
-template <bool COHERENT = false>
-__device__ __forceinline__ void dma16(const void* g, const char* l) {
-  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)l;
-  if (COHERENT)
-    asm volatile("global_load_lds_dwordx4 %0, off sc1" ::"v"(g), "{m0}"(a) : "memory");
-  else
-    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(a) : "memory");
-}
-// s_waitcnt vmcnt(N): all but this wave's N most recent vector-memory
-// operations (LDS copies included) have completed.
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-__device__ __forceinline__ void lds_dma_wait() { vm_wait<0>(); }
 
 constexpr float kLog2e = 1.4426950408889634f;
 // The running maximum of a column is raised only when a block's logit exceeds
@@ -143,8 +114,6 @@ struct AttnArgs {
   const uint16_t* v_new;
 };
 
-__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
 // 16-byte load / store at device scope (bypassing stale copies in another
 // die's L2): two 8-byte device-scope atomics.  Used where one launch both
@@ -200,16 +169,8 @@ __device__ __forceinline__ void wait_appended(const AttnArgs& a) {
     __builtin_amdgcn_s_sleep(8);
   }
 }
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-__device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
 
-__device__ __forceinline__ uint32_t pack2(float a, float b) {
-  f32x2 v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-}
 
 __device__ __forceinline__ bf16x8 pack8(const float (&p)[8]) {
   u32x4 r = {pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};

@@ -13,6 +13,7 @@
 #include <stdint.h>
 
 #include "../../include/ssa_layer.h"
+#include "ssa_device.h"
 #include "ssa_plan_format.h"
 
 namespace ssa {
@@ -21,23 +22,9 @@ int check_plan(const ssa_shape* s, const void* plan_host, const PlanHeader** out
 
 namespace {
 using namespace ssa;
-
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+using namespace ssa_dev;
 
 constexpr int kLayerThreads = 256;
-
-__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
-// two fp32 to packed bf16, round to nearest even
-__device__ __forceinline__ uint32_t pack2(float a, float b) {
-  f32x2 v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-}
 
 // Rotate 8 pairs: x1 = dims i..i+7, x2 = dims i+D/2..i+D/2+7 of one head.
 __device__ __forceinline__ void rotate8(u32x4 x1, u32x4 x2, const float* cs, int half, int i,

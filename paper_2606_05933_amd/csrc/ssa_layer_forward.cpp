@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <cmath>
 
 #include "../../include/ssa_layer.h"
 #include "ssa_plan_format.h"
@@ -71,6 +72,21 @@ int layer_ws(const ssa_shape* shape, const void* plan_host, const ssa_layer_weig
 }  // namespace
 
 extern "C" {
+
+int ssa_rope_table(int32_t max_position, int32_t d, double base, float* out) {
+  if (!out) return SSA_ERR_NULL;
+  if (max_position < 1 || d < 2 || d % 2 || !std::isfinite(base) || !(base > 1.0)) return SSA_ERR_ARG;
+  const int half = d / 2;
+  for (int i = 0; i < half; ++i) {
+    const double t = std::pow(base, -2.0 * i / d);
+    for (int64_t p = 0; p < max_position; ++p) {
+      const double a = (double)p * t;
+      out[p * d + i] = (float)std::cos(a);
+      out[p * d + half + i] = (float)std::sin(a);
+    }
+  }
+  return SSA_OK;
+}
 
 int ssa_layer_workspace_size(const ssa_shape* shape, const void* plan_host,
                              const ssa_layer_weights* w, size_t* ws_bytes) {

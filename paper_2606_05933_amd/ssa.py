@@ -134,6 +134,8 @@ def _load():
                           + "; load libssa.so only after torch (import torch first)")
     vp, sz = ctypes.c_void_p, ctypes.c_size_t
     P = ctypes.POINTER
+    lib.ssa_rope_table.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_double, vp]
+    lib.ssa_rope_table.restype = ctypes.c_int
     lib.ssa_status_string.argtypes = [ctypes.c_int]
     lib.ssa_status_string.restype = ctypes.c_char_p
     lib.ssa_plan_size.argtypes = [P(SsaShape), vp, vp, ctypes.c_int32, P(SsaTuning), P(sz), P(sz)]
@@ -199,7 +201,7 @@ EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_check_block_t
             "ssa_predictor_add",
             "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
             "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor",
-            "ssa_rope_append", "ssa_linear_workspace_size", "ssa_linear", "ssa_rms_norm",
+            "ssa_rope_append", "ssa_rope_table", "ssa_linear_workspace_size", "ssa_linear", "ssa_rms_norm",
             "ssa_layer_workspace_size", "ssa_layer_forward", "ssa_probe_hbm_read",
             "ssa_probe_hbm_gather", "ssa_probe_mfma_bf16")
 
@@ -527,12 +529,13 @@ def bind_mixed_attention(shape: SsaShape, plan_host, plan_dev, q, k_cache, v_cac
 
 
 def rope_cos_sin(max_position: int, d: int, base: float = 500000.0) -> np.ndarray:
-    """[max_position, d] fp32 table of ssa_rope_append: cos(p t_i) in columns
-    i < d/2, sin(p t_i) in columns d/2 + i, t_i = base^(-2i/d) (angles in fp64)."""
-    i = np.arange(d // 2, dtype=np.float64)
-    inv = base ** (-2.0 * i / d)
-    ang = np.arange(max_position, dtype=np.float64)[:, None] * inv[None, :]
-    return np.concatenate([np.cos(ang), np.sin(ang)], axis=1).astype(np.float32)
+    """[max_position, d] fp32 table of ssa_rope_append (ssa_rope_table): cos(p t_i)
+    in columns i < d/2, sin(p t_i) in columns d/2 + i, t_i = base^(-2i/d)."""
+    out = np.empty((max_position, d), dtype=np.float32)
+    rc = LIB.ssa_rope_table(int(max_position), int(d), float(base), out.ctypes.data)
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_rope_table")
+    return out
 
 
 def rope_append(shape: SsaShape, plan_host, plan_dev, qkv, cos_sin, q_out, k_cache, v_cache,

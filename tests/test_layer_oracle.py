@@ -60,6 +60,19 @@ def test_library_rope_table_matches_the_oracle_angles():
         assert np.allclose(tab[p, 64:], r[64:], atol=6e-8, rtol=0)
 
 
+def test_library_rope_table_rejects_bad_arguments():
+    import ctypes
+    out = np.zeros((4, 8), dtype=np.float32)
+    f = ssa.LIB.ssa_rope_table
+    assert f(4, 8, 10000.0, None) == ssa.SSA_ERR_NULL
+    for mp, d, base in ((0, 8, 1e4), (4, 7, 1e4), (4, 0, 1e4), (4, 8, 1.0), (4, 8, float("inf")),
+                        (4, 8, float("nan"))):
+        assert f(mp, d, base, out.ctypes.data) == ssa.SSA_ERR_ARG, (mp, d, base)
+    assert not out.any()  # nothing written on an error
+    assert f(4, 8, 10000.0, out.ctypes.data) == ssa.SSA_OK
+    assert out[0, :4].tolist() == [1.0] * 4 and out[0, 4:].tolist() == [0.0] * 4
+
+
 def test_rms_norm_and_silu_closed_forms():
     w = np.linspace(0.5, 2.0, 8)
     assert np.allclose(orc.rms_norm(np.full(8, 3.0), w, eps=0.0), w, rtol=1e-15)
