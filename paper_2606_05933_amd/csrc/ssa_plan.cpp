@@ -13,6 +13,7 @@
 #include <climits>
 #include <cmath>
 #include <cstring>
+#include <functional>
 #include <new>
 #include <vector>
 
@@ -33,6 +34,10 @@ constexpr double kHbmRate = 8.0e12 * 0.7;
 // each piece costs a partial record of ncols*(D+2) floats written and read back.
 constexpr int kMinChunkSplitKeys = 1024;
 constexpr int kMaxChunkSplits = 16;
+// What one extra piece of a split chunk tile costs, in keys of the tile's work
+// (its prologue, partial record and share of the merge; measured: three
+// pieces of a 33k-key tile about 6% slower than one).
+constexpr double kSplitCostKeys = 768.0;
 // Decode key ranges are cut into equal pieces of about this many keys: long
 // enough that the load latency at the start of an item is amortised over 32
 // blocks per wave, short enough that long and short contexts balance over the
@@ -377,6 +382,70 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
     return (int32_t)p->groups.size() - 1;
   };
 
+  // Key splits of a chunk tile (automatic): pieces of at most half the
+  // estimated makespan, times `mult`, within [1, kMaxChunkSplits] and pieces of
+  // at least kMinChunkSplitKeys keys.
+  auto auto_nsplit = [&](int kend, int mult) {
+    const double t_tile = 4.0 * D * (double)tu.tile_cols * kend / kMfmaRatePerCu;
+    int ns = makespan > 0 ? (int)std::ceil(t_tile / (0.5 * makespan)) : 1;
+    ns = std::max(1, ns) * mult;
+    ns = std::min(ns, std::max(1, kend / kMinChunkSplitKeys));
+    return std::max(1, std::min(ns, kMaxChunkSplits));
+  };
+  // The multiplier: chunk items are long, and when their number is not close
+  // to a multiple of the workgroup slots (two per CU) the last round runs part
+  // empty (768 equal tiles on 512 slots take two tile times; cut in two, three
+  // half times).  The chunk items' greedy longest-first schedule on the slots
+  // (decode items left out) is simulated for multipliers 1..3, each extra
+  // piece charged kSplitCostKeys keys; a larger multiplier must win by 3%.
+  int split_mult = 1;
+  if (tu.chunk_split_keys == 0 && makespan > 0) {
+    std::vector<double> best_pieces;
+    double best = 0.0;
+    for (int mult = 1; mult <= 3; ++mult) {
+      std::vector<double> pieces;
+      bool too_many = false;  // left to the item loop below (which reports it)
+      for (int i = 0; i < n && !too_many; ++i) {
+        const int c = q_len[i], u = ctx_len[i];
+        if (c <= 1) continue;
+        const int64_t total_cols = (int64_t)c * G;
+        for (int64_t col0 = 0; col0 < total_cols && !too_many; col0 += tu.tile_cols) {
+          const int64_t ncols = std::min<int64_t>(tu.tile_cols, total_cols - col0);
+          const int kend = u + (int)((col0 + ncols - 1) / G) + 1;
+          const int ns = auto_nsplit(kend, mult);
+          const int piece = (int)ceil_div(ceil_div(kend, ns), kBlockKeys) * kBlockKeys;
+          for (int k0 = 0; k0 < kend; k0 += piece)
+            pieces.push_back((double)std::min(piece, kend - k0) + (ns > 1 ? kSplitCostKeys : 0));
+          too_many = (int64_t)pieces.size() * Hkv > kMaxItems;
+        }
+      }
+      if (pieces.empty() || too_many) break;
+      // beyond four rounds of the slots the last round's loss is small
+      const size_t slots = 2 * (size_t)tu.num_cus;
+      if (mult == 1 && pieces.size() * Hkv > 4 * slots) break;
+      std::sort(pieces.begin(), pieces.end(), std::greater<double>());
+      // every kv head has the same pieces, launched next to each other: the
+      // schedule of one head's pieces on slots / Hkv slots stands for it
+      std::vector<double> slot(std::max<size_t>(1, slots / Hkv), 0.0);
+      double end = 0.0;
+      for (double t : pieces) {
+        std::pop_heap(slot.begin(), slot.end(), std::greater<double>());
+        slot.back() += t;
+        end = std::max(end, slot.back());
+        std::push_heap(slot.begin(), slot.end(), std::greater<double>());
+      }
+      if (mult == 1 || end < 0.97 * best) {
+        if (mult > 1) split_mult = mult;
+        best = end;
+      }
+      // no split can beat a schedule within 3% of the larger of the longest
+      // piece and the work per slot
+      double total = 0.0;
+      for (double t : pieces) total += t;
+      if (mult == 1 && end <= 1.03 * std::max(pieces.front(), total / slot.size())) break;
+    }
+  }
+
   for (int i = 0; i < n; ++i) {
     const int c = q_len[i], u = ctx_len[i];
     if (c > 1) {
@@ -393,15 +462,11 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
         const int j_last = (col0 + ncols - 1) / G;
         const int kend = u + j_last + 1;
         for (int h = 0; h < Hkv; ++h) {
-          const double t_tile = 4.0 * D * (double)tu.tile_cols * kend / kMfmaRatePerCu;
           int nsplit = 1;
-          if (tu.chunk_split_keys > 0) {
+          if (tu.chunk_split_keys > 0)
             nsplit = (int)ceil_div(kend, tu.chunk_split_keys);
-          } else if (makespan > 0) {
-            nsplit = (int)std::ceil(t_tile / (0.5 * makespan));
-            nsplit = std::min(nsplit, std::max(1, kend / kMinChunkSplitKeys));
-            nsplit = std::max(1, std::min(nsplit, kMaxChunkSplits));
-          }
+          else if (makespan > 0)
+            nsplit = auto_nsplit(kend, split_mult);
           int piece = (int)ceil_div(ceil_div(kend, nsplit), kBlockKeys) * kBlockKeys;
           nsplit = (int)ceil_div(kend, piece);
           const int32_t grp = nsplit > 1 ? add_group(nsplit, ncols) : -1;

@@ -239,6 +239,26 @@ def test_automatic_launch_order_pairs_only_decode_heavy_full_chunk_batches():
     assert (k[:info.num_chunk_items] == k[0]).all()  # all chunk items first
 
 
+def test_automatic_chunk_splits_fill_the_last_round():
+    """With the split length left at 0, chunk tiles that would leave the last
+    round of the 512 workgroup slots part empty are cut: the 70B-shaped chunk of
+    1536 tokens alone (768 tiles) runs as 1536 pieces (three rounds of half
+    tiles), while 512 tiles (c = 1024) and 1024 tiles (c = 2048), whole rounds,
+    stay whole; an explicit split length is kept."""
+    from paper_2606_05933_amd import workload
+    for chunk, items in ((1024, 512), (1536, 1536), (2048, 1024)):
+        b = workload.make_workload("l70b", seed=0, chunk=chunk)
+        sb = workload.sub_batch(b, b.q_len > 1)
+        s = sb.shape
+        shape = ssa.make_shape(s.hq, s.hkv, s.d, sb.num_pages, sb.block_table.shape[1],
+                               s.softmax_scale)
+        _, info = ssa.ssa_plan(shape, sb.q_len, sb.ctx_len)
+        assert info.num_chunk_items == items, (chunk, info.num_chunk_items)
+        _, info = ssa.ssa_plan(shape, sb.q_len, sb.ctx_len,
+                               ssa.make_tuning(chunk_split_keys=1 << 20))
+        assert info.num_chunk_items == 768 * chunk // 1536, chunk
+
+
 def test_plan_is_deterministic():
     q_len = np.array([300, 1, 1, 1], np.int32)
     ctx_len = np.array([0, 5, 900, 40], np.int32)
