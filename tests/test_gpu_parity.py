@@ -213,11 +213,13 @@ def sampled_parity(b, n_chunk_rows=24, heads_per_row=4, seed=0):
 
 
 @pytest.mark.parametrize("name,chunk,prefix", [
-    ("multi", 1024, None), ("l70b", 2048, None), ("l8b", 2048, None),
+    ("multi", 1024, None), ("l70b", 2048, None), ("l8b", 2048, None), ("l70b", 1536, None),
 ])
 def test_extra_sweep_rows_sampled_parity(torch_dev, name, chunk, prefix):
     """Latency-table rows beyond the five configurations (chunk sizes of the
-    sweep): the oracle at sampled (row, head) pairs."""
+    sweep; at c = 1536 the planner cuts every 70B chunk tile in two key pieces
+    to fill the last round of workgroup slots): the oracle at sampled (row,
+    head) pairs."""
     from paper_2606_05933_amd import workload
     b = workload.make_workload(name, seed=0, chunk=chunk, prefix=prefix)
     b.name = f"{name}(c={chunk},u={prefix})"
