@@ -74,7 +74,10 @@ METRIC = "mixed prefill+decode attention µs/iter vs chunk size; % HBM / MFMA ro
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 TIME_EVERY = 4  # timed steps whose kernel stamps its start and end
-KERNEL_SRC = os.path.join(ROOT, "paper_2606_05933_amd", "csrc", "ssa_kernels.hip")
+# the sources the fused launch is compiled from (its traffic counters are valid
+# only for these exact files)
+KERNEL_SRC = [os.path.join(ROOT, "paper_2606_05933_amd", "csrc", f)
+              for f in ("ssa_kernels.hip", "ssa_device.h", "ssa_plan_format.h")]
 def traffic_file(workload):
     return os.path.join(ROOT, "profiles", f"traffic_append_attention_{workload}.json")
 
@@ -97,9 +100,13 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def sha256_file(p):
-    with open(p, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def sha256_file(paths):
+    """SHA-256 of one file, or of several files' bytes in order."""
+    h = hashlib.sha256()
+    for p in ([paths] if isinstance(paths, str) else paths):
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def kernel_event_samples(fn, n, flush=None):

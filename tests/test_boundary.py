@@ -201,14 +201,23 @@ def test_scene_and_features_follow_the_paper():
         assert inf.scene == scene
 
 
+def _lengths_plan(name, chunk, tuning=None, keep=None):
+    """Plan (blob, info) of a named workload's lengths (no tensors drawn);
+    keep: optional filter on q_len (e.g. the chunk rows alone)."""
+    from paper_2606_05933_amd import workload
+    s, q_len, ctx_len = workload.workload_lengths(name, 0, chunk)
+    q_len, ctx_len = np.asarray(q_len, np.int32), np.asarray(ctx_len, np.int32)
+    if keep is not None:
+        m = keep(q_len)
+        q_len, ctx_len = q_len[m], ctx_len[m]
+    pages = int(sum((u + c + 15) // 16 for c, u in zip(q_len, ctx_len)))
+    shape = shape_of(s.hq, s.hkv, s.d, q_len, ctx_len, num_pages=pages + 64)
+    return ssa.ssa_plan(shape, q_len, ctx_len, tuning)
+
+
 def _plan_kinds(name, chunk, tuning=None):
     """Work-item kinds of a generated workload's plan, in launch order."""
-    from paper_2606_05933_amd import workload
-    b = workload.make_workload(name, seed=0, chunk=chunk)
-    s = b.shape
-    shape = ssa.make_shape(s.hq, s.hkv, s.d, b.num_pages, b.block_table.shape[1],
-                           s.softmax_scale)
-    blob, info = ssa.ssa_plan(shape, b.q_len, b.ctx_len, tuning)
+    blob, info = _lengths_plan(name, chunk, tuning)
     hdr = np.frombuffer(blob[:128].tobytes(), dtype=np.int32)
     off = int(hdr[19])  # off_items
     items = np.frombuffer(blob[off:off + 48 * info.num_items].tobytes(), np.int32).reshape(-1, 12)
@@ -245,17 +254,12 @@ def test_automatic_chunk_splits_fill_the_last_round():
     1536 tokens alone (768 tiles) runs as 1536 pieces (three rounds of half
     tiles), while 512 tiles (c = 1024) and 1024 tiles (c = 2048), whole rounds,
     stay whole; an explicit split length is kept."""
-    from paper_2606_05933_amd import workload
+    chunk_rows = lambda q: q > 1
     for chunk, items in ((1024, 512), (1536, 1536), (2048, 1024)):
-        b = workload.make_workload("l70b", seed=0, chunk=chunk)
-        sb = workload.sub_batch(b, b.q_len > 1)
-        s = sb.shape
-        shape = ssa.make_shape(s.hq, s.hkv, s.d, sb.num_pages, sb.block_table.shape[1],
-                               s.softmax_scale)
-        _, info = ssa.ssa_plan(shape, sb.q_len, sb.ctx_len)
+        _, info = _lengths_plan("l70b", chunk, keep=chunk_rows)
         assert info.num_chunk_items == items, (chunk, info.num_chunk_items)
-        _, info = ssa.ssa_plan(shape, sb.q_len, sb.ctx_len,
-                               ssa.make_tuning(chunk_split_keys=1 << 20))
+        _, info = _lengths_plan("l70b", chunk, ssa.make_tuning(chunk_split_keys=1 << 20),
+                                keep=chunk_rows)
         assert info.num_chunk_items == 768 * chunk // 1536, chunk
 
 
