@@ -675,6 +675,11 @@ def main_pmc_md(args):
         raise SystemExit(f"no trace statistics of {kernel}")
     calls = int(stats[0]["Calls"])
     dur_ns = float(stats[0]["AverageNs"])
+    # per dispatch, in launch order: the first ones are the warm-up launches
+    trace = sorted((r for r in csv.DictReader(open(os.path.join(d, "t", "run_kernel_trace.csv")))
+                    if kernel in r["Kernel_Name"]), key=lambda r: int(r["Start_Timestamp"]))
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in trace]
+    warm_ns = statistics.mean(durs[3:]) if len(durs) > 3 else dur_ns
     cf, _ = _pmc_means(os.path.join(d, "e", "run_counter_collection.csv"), "copyBuffer")
     cw, _ = _pmc_means(os.path.join(d, "f", "run_counter_collection.csv"), "copyBuffer")
     copy_kib = float(1 << 20)
@@ -694,7 +699,8 @@ def main_pmc_md(args):
     cmd = args.pmc_cmd
     rows = [
         ("dispatches (trace / counter passes a, b, c, d)", f"{calls} / {nd['a']}, {nd['b']}, {nd['c']}, {nd['d']}"),
-        ("kernel duration, trace average", f"{dur_ns / 1e3:.1f} us"),
+        ("kernel duration, trace average (all dispatches / after the 3 warm-up launches)",
+         f"{dur_ns / 1e3:.1f} / {warm_ns / 1e3:.1f} us"),
         ("GRBM_GUI_ACTIVE per die", f"{gui:.4g} cycles -> clock {clock:.3f} GHz"),
         ("MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES / (GUI per die x 1024 SIMDs)", f"{busy:.3f}"),
         ("MFMA flops: 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16", f"{mops:.4g}"
