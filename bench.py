@@ -17,8 +17,10 @@ iteration of back-to-back steps), the fused launch's roofline (live timing from
 events the kernel stamps itself; bound by whichever floor is larger, the chunk
 flops at the bf16 MFMA peak or the algorithmic bytes at the HBM peak, with the
 overlap floor and each segment's own fraction beside it), the same launch with
-a cold cache, the Llama-3-8B-shaped line for context, and the CPU oracle timed
-on this host on a bounded sample (a reported baseline, not the target).
+a cold cache, the latency-vs-chunk-size curve (this batch with its chunk cut to
+smaller sizes, and the 8B-shaped sweep configuration at three prefixes), the
+Llama-3-8B-shaped line for context, and the CPU oracle timed on this host on a
+bounded sample (a reported baseline, not the target).
 
 Other modes (all single GPU):
   --sweep OUT        latency-vs-chunk-size table of every workload (JSON lines)
@@ -245,6 +247,45 @@ def cpu_baseline(b, target_s=15.0, threads=0, repeats=3):
             "tokens_per_s": round(b.num_tokens / t_iter, 1)}
 
 
+def chunk_row(b, i, c, u):
+    """Batch b with request i's chunk cut to its first c tokens at prefix u
+    (rows, pools and block table shared; needs c <= b.q_len[i] and
+    u + c <= b.ctx_len[i] + b.q_len[i])."""
+    from paper_2606_05933_amd import workload
+    starts = np.concatenate([[0], np.cumsum(b.q_len)]).astype(np.int64)
+    keep = np.concatenate([np.arange(starts[k], starts[k + 1]) if k != i
+                           else np.arange(starts[k], starts[k] + c) for k in range(b.num_reqs)])
+    q_len, ctx_len = b.q_len.copy(), b.ctx_len.copy()
+    q_len[i], ctx_len[i] = c, u
+    return workload.Batch(b.shape, q_len, ctx_len, b.block_table, b.num_pages, b.q[keep],
+                          b.k_new[keep], b.v_new[keep], b.k_cache, b.v_cache, name=b.name,
+                          seed=b.seed)
+
+
+def chunk_curve(db, rows, n=10):
+    """Fused-launch time (us, average of n warm launches) of each (c, u) row
+    derived from db's batch (its one chunk request cut to c tokens at prefix u),
+    on db's device pools, with the algorithmic rates.  The curve the latency
+    predictor and the SlidingChunker consume (Sec. 3.2, 3.4)."""
+    from paper_2606_05933_amd.device import DeviceBatch
+    b = db.b
+    i = int(np.nonzero(b.q_len > 1)[0][0])
+    out = []
+    for c, u in rows:
+        rb = DeviceBatch(chunk_row(b, i, c, u), pools=(db.k_cache, db.v_cache, db.block_table))
+        for _ in range(3):
+            rb.step_fused()
+        t = time_kernel_events(rb.step_fused, n)
+        info = rb.info
+        nbytes = info.decode_bytes + info.chunk_bytes + info.append_bytes
+        out.append({"chunk": int(c), "prefix": int(u), "fused_us": round(t * 1e6, 2),
+                    "tokens_per_s": round(rb.b.num_tokens / t, 1),
+                    "hbm_frac": round(nbytes / t / 1e9 / HBM_PEAK_GBS, 4),
+                    "mfma_frac": round(info.chunk_flops / t / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)})
+        del rb
+    return out
+
+
 def traffic_bytes(workload):
     """HBM bytes per fused launch from committed rocprofv3 counter runs on this
     workload, if they were taken on the current kernel source."""
@@ -362,8 +403,32 @@ def main_bench(args):
         "decode_segment_hbm_frac": segs.get("decode", {}).get("hbm_frac"),
     })
 
-    # the Llama-3-8B-shaped line (the previous headline), back-to-back steps
+    # latency vs chunk size (the curve the predictor and the SlidingChunker
+    # consume): this batch with its chunk cut to smaller sizes, and the 8B-shaped
+    # sweep configuration (one 8192-token prompt at prefixes 0 / 2048 / 6144)
     extra = {}
+    if not args.no_curve and (b.q_len > 1).any():
+        i0 = int(np.nonzero(b.q_len > 1)[0][0])
+        cmax, u0 = int(b.q_len[i0]), int(b.ctx_len[i0])
+        cs = sorted({c for c in (128, 256, 512) if c < cmax} | {cmax})
+        curve = {args.workload: chunk_curve(db, [(c, u0) for c in cs])}
+        del db, flush
+        torch.cuda.empty_cache()
+        bs = workload.make_workload("l8b_sweep", seed=args.seed, chunk=2048, prefix=6144)
+        ds = DeviceBatch(bs)
+        curve["l8b_sweep"] = chunk_curve(ds, [(c, u) for u in (0, 2048, 6144)
+                                              for c in (128, 256, 512, 1024, 2048)])
+        del ds, bs
+        torch.cuda.empty_cache()
+        extra["latency_vs_chunk"] = {
+            "note": "fused launch us (average of 10 warm launches) per (chunk, prefix); the "
+                    "batch's other requests unchanged", **curve}
+        log("[bench] latency vs chunk: " + ", ".join(
+            f"{k} c={r['chunk']} u={r['prefix']}: {r['fused_us']} us"
+            for k, v in curve.items() for r in v[:3]) + " ...")
+        db = flush = None
+
+    # the Llama-3-8B-shaped line (the previous headline), back-to-back steps
     if args.workload != "l8b" and not args.no_extra_line:
         del db, flush
         torch.cuda.empty_cache()
@@ -1385,6 +1450,8 @@ def main():
     ap.add_argument("--prefix", type=int, default=None)
     ap.add_argument("--scene", choices=["mixed", "decode", "prefill"], default="mixed")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-curve", action="store_true",
+                    help="skip the latency-vs-chunk-size curve of the default line")
     ap.add_argument("--no-extra-line", action="store_true",
                     help="skip the Llama-3-8B-shaped line reported beside the default one")
     ap.add_argument("--sweep", metavar="OUT", default=None)

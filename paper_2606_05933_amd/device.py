@@ -27,7 +27,9 @@ def bits_of(t: torch.Tensor) -> np.ndarray:
 
 class DeviceBatch:
     def __init__(self, b, tuning: ssa.SsaTuning | None = None, device="cuda",
-                 plan_on_device: bool = False):
+                 plan_on_device: bool = False, pools=None):
+        """pools: optional (k_cache, v_cache, block_table) device tensors of
+        another DeviceBatch over the same pools, used instead of uploading b's."""
         self.b = b
         self.plan_on_device = plan_on_device
         self.device = torch.device(device)
@@ -39,9 +41,12 @@ class DeviceBatch:
         self.q = bf16_tensor(b.q, dev)
         self.k_new = bf16_tensor(b.k_new, dev)
         self.v_new = bf16_tensor(b.v_new, dev)
-        self.k_cache = bf16_tensor(b.k_cache, dev)
-        self.v_cache = bf16_tensor(b.v_cache, dev)
-        self.block_table = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(dev)
+        if pools is not None:
+            self.k_cache, self.v_cache, self.block_table = pools
+        else:
+            self.k_cache = bf16_tensor(b.k_cache, dev)
+            self.v_cache = bf16_tensor(b.v_cache, dev)
+            self.block_table = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(dev)
         self.out = torch.zeros((b.num_tokens, s.hq, s.d), dtype=torch.bfloat16, device=dev)
         self.plan()
 
