@@ -932,10 +932,9 @@ __device__ void chunk_item(const AttnArgs& a, const WorkItem& it, const ReqEntry
         st_dev(rec + Cn + cl, cs[nt].l);
       }
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj)
-          st_dev(rec + rec_o_off(Cn) + (int64_t)cl * D + mt * 16 + 4 * g + jj, o[nt][mt][jj]);
+      for (int mt = 0; mt < MT; ++mt)  // 16-byte aligned, as records and o rows are
+        st16_dev(rec + rec_o_off(Cn) + (int64_t)cl * D + mt * 16 + 4 * g,
+                 __builtin_bit_cast(u32x4, o[nt][mt]));
     }
     finish_split<D>(a, it, rq, lds);
   }
@@ -1130,8 +1129,9 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
         st_dev(rec + col, M);
         st_dev(rec + G + col, L);
       }
-#pragma unroll
-      for (int k = 0; k < 4; ++k) st_dev(rec + rec_o_off(G) + (int64_t)col * D + d0 + k, acc[k]);
+      st16_dev(rec + rec_o_off(G) + (int64_t)col * D + d0,  // 16-byte aligned
+               u32x4{__builtin_bit_cast(uint32_t, acc[0]), __builtin_bit_cast(uint32_t, acc[1]),
+                     __builtin_bit_cast(uint32_t, acc[2]), __builtin_bit_cast(uint32_t, acc[3])});
     } else {
       const float inv = 1.f / L;
       store_bf16x4(a.out + ((size_t)rq.q_start * a.hq + it.kvh * G + col) * D + d0,
