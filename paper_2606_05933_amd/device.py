@@ -27,9 +27,15 @@ def bits_of(t: torch.Tensor) -> np.ndarray:
 
 class DeviceBatch:
     def __init__(self, b, tuning: ssa.SsaTuning | None = None, device="cuda",
-                 plan_on_device: bool = False, pools=None):
-        """pools: optional (k_cache, v_cache, block_table) device tensors of
-        another DeviceBatch over the same pools, used instead of uploading b's."""
+                 plan_on_device=False, pools=None):
+        """plan_on_device: False, the kernels read the plan in place from pinned,
+        device-mapped host memory; True, each re-plan is copied to device memory
+        on the launch stream; "async", copied on a side stream that the launch
+        stream waits for (the copy overlaps the previous iteration's kernels).
+        pools: optional (k_cache, v_cache, block_table) device tensors of another
+        DeviceBatch over the same pools, used instead of uploading b's."""
+        if plan_on_device not in (False, True, "async"):
+            raise ValueError("plan_on_device: False, True or 'async'")
         self.b = b
         self.plan_on_device = plan_on_device
         self.device = torch.device(device)
@@ -68,6 +74,11 @@ class DeviceBatch:
                          for _ in range(2)]
         else:
             self._dev = self._host  # device-mapped pinned memory, read in place
+        # the stream the calls are bound to, and (async copies) the side stream
+        self._stream = torch.cuda.current_stream(self.device)
+        if self.plan_on_device == "async":
+            self._copy_stream = torch.cuda.Stream(self.device)
+            self._copied = [torch.cuda.Event(), torch.cuda.Event()]
         # "the slot's kernels are done": the attention launch of the slot stamps
         # its own end into one of these (no extra packet on the stream)
         self._own_done = [torch.cuda.Event(), torch.cuda.Event()]
@@ -108,13 +119,21 @@ class DeviceBatch:
     def replan_host(self):
         """Plan the (same) batch again on the host into the other slot, as a
         serving loop does every iteration: wait until the kernels that last read
-        that slot have finished, plan into it, and (only with plan_on_device)
-        copy it to its device buffer on the current stream."""
+        that slot have finished, plan into it, and (with plan_on_device) copy it
+        to its device buffer, on the launch stream or (async) on a side stream
+        the launch stream waits for."""
         slot = self._slot ^ 1
         if self._used[slot]:
             self._done[slot].synchronize()
         self._bound[slot][0]()
-        if self.plan_on_device:
+        if self.plan_on_device == "async":
+            # the slot's last kernels have finished (waited for above), so its
+            # device copy may be overwritten at once; the launch stream waits
+            with torch.cuda.stream(self._copy_stream):
+                self._dev[slot].copy_(self._host[slot], non_blocking=True)
+            self._copied[slot].record(self._copy_stream)
+            self._stream.wait_event(self._copied[slot])
+        elif self.plan_on_device:
             self._dev[slot].copy_(self._host[slot], non_blocking=True)
         self._used[slot] = True
         self._slot = slot

@@ -119,24 +119,33 @@ def test_tiny_workload_matches_oracle(torch_dev):
     full_parity(workload.make_workload("tiny", seed=0))
 
 
-@pytest.mark.parametrize("plan_on_device", [False, True])
+@pytest.mark.parametrize("plan_on_device", [False, True, "async"])
 def test_llama8b_mixed_full_parity(torch_dev, plan_on_device):
     from paper_2606_05933_amd import workload
     full_parity(workload.make_workload("l8b", seed=0), plan_on_device=plan_on_device)
 
 
-def test_replanned_iterations_alternate_plan_slots(torch_dev):
+@pytest.mark.parametrize("plan_on_device", [False, "async"])
+def test_replanned_iterations_alternate_plan_slots(torch_dev, plan_on_device):
     """Several iterations in a row, each re-planned into the other plan slot
-    while the previous one may still run: every output matches the oracle."""
+    while the previous one may still run (with "async", each plan copied to the
+    device on a side stream): every output matches the oracle."""
     import torch
     from oracle import oracle
     from paper_2606_05933_amd import workload
+    from paper_2606_05933_amd.device import DeviceBatch
     b = workload.make_workload("l8b", seed=2)
-    db = run(b)
-    for _ in range(5):
+    db = DeviceBatch(b, plan_on_device=plan_on_device)
+    db.step()
+    for k in range(6):
         db.replan_host()
-        db.step()
+        db.out.zero_()
+        if k % 2:
+            db.step_fused()
+        else:
+            db.step()
     torch.cuda.synchronize()
+    assert db.status() == 0
     kc, vc = oracle.batch_kv_append(b)
     ref, _ = oracle.batch_attention(b, kc, vc)
     assert_close(db.out_f32(), ref, "l8b replanned")
