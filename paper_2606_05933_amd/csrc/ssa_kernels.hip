@@ -1,5 +1,6 @@
-// HIP kernels for gfx950 (CDNA4) and the two launching entry points of the
-// C ABI: ssa_kv_append and ssa_mixed_attention.
+// HIP kernels for gfx950 (CDNA4) and the launching entry points of the C ABI:
+// ssa_kv_append, ssa_mixed_attention, and ssa_append_attention (both in one
+// launch; also without a workspace argument, ssa_append_attention_static).
 //
 // Attention work is one launch of a flat grid; workgroup b runs work item b of
 // the plan (longest first).  Two kinds of item share the launch:
@@ -19,9 +20,11 @@
 //  * decode split (c_i == 1; Tab. 1 x4/x5): the G q heads of one kv head are the
 //    N columns of the same MFMA formulation, so each K/V byte read from HBM is
 //    used by the whole GQA group.  The 4 waves of the workgroup take
-//    interleaved 32-key blocks of the split's key range straight from global
-//    memory (16-byte coalesced loads, next block prefetched into registers),
-//    and merge their (m, l, O) partials through LDS at the end.
+//    interleaved 32-key blocks of the split's key range, the next block in
+//    flight while one is computed: key rows through two LDS stages per wave
+//    (whole-row global -> LDS copies), value rows straight into registers
+//    (non-temporal 16-byte loads); the waves merge their (m, l, O) partials
+//    through LDS at the end.
 //
 // Items that cover part of a key range write an fp32 partial record; the last
 // item of the group to finish (atomic ticket) merges the records in split
