@@ -87,9 +87,10 @@ struct Cfg {
   static constexpr int V_PAGE = D * 32;      // LDS bytes of one value page: D rows of 16 slots
   static constexpr int V_STAGE = 2 * V_PAGE;
   static constexpr int STAGE = K_STAGE + V_STAGE;
-  static constexpr int LDS_CHUNK = kChunkStages * STAGE;
-  static constexpr int LDS_DECODE = kWaves * (32 + 16 * D) * 4;
-  static constexpr int LDS = (LDS_CHUNK > LDS_DECODE + 16 ? LDS_CHUNK : LDS_DECODE + 16);
+  static constexpr int LDS_CHUNK = kChunkStages * STAGE;          // chunk item: K/V stages
+  static constexpr int LDS_DECODE_KEYS = kWaves * 2 * K_STAGE;    // decode item: key stages
+  static constexpr int LDS_DECODE_MERGE = kWaves * (32 + 16 * D) * 4;  // decode: waves' m, l, o
+  static constexpr int LDS = std::max({LDS_CHUNK, LDS_DECODE_KEYS, LDS_DECODE_MERGE + 16});
   static constexpr int LOADS = D / 64;       // 16-byte K (and V) chunks per thread per block
   static constexpr int KROWS_PER_LOAD = 64 / CPR;  // key rows one wave-wide 1 KB load fills
 };
@@ -465,7 +466,9 @@ __device__ void merge_group(const AttnArgs& a, const WorkItem& it, const ReqEntr
 template <int D>
 __device__ void finish_split(const AttnArgs& a, const WorkItem& it, const ReqEntry& rq,
                              char* lds) {
-  // a word of the kernel's LDS buffer past both items' working areas
+  // the last word of the kernel's LDS buffer: past the decode merge area, and
+  // in staging that is dead once every wave has passed the barrier below
+  // (each wave waited for its own copies before leaving its loop)
   int& s_last = *reinterpret_cast<int*>(lds + Cfg<D>::LDS - 16);
   const MergeGroup grp = reinterpret_cast<const MergeGroup*>(a.plan + a.off_groups)[it.group];
   int* tickets = reinterpret_cast<int*>(a.ws) + kLaunchCounters;
@@ -1014,6 +1017,7 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   // counts: one block's KLOADS copies and MT loads stay in flight while the
   // block before it is computed.
   constexpr int KLOADS = C::K_STAGE / 1024;
+  static_assert(kWaves * 2 * C::K_STAGE <= C::LDS, "key stages fit the kernel's LDS");
   char* kst = lds + w * 2 * C::K_STAGE;
   int kgo[KLOADS], kch[KLOADS];
 #pragma unroll
