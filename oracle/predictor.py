@@ -6,12 +6,16 @@ nothing from the library package.
 
 What it computes, following Sec. 3.2:
 
-* Eq. 3 scenes: pure decode (no request with c > 1), pure prefill (no request
-  with c <= 1), mixed; an empty batch has no scene.
+* Eq. 2 sets: P = {c > 1}; D = {c <= 1} holds the requests with one new
+  token.  A request with c = 0 has no new token this iteration and is not
+  part of the batch that runs: it is in neither set, in no feature and decides
+  no scene (the reading the planner and batch forming follow too).
+* Eq. 3 scenes: pure decode (D only), pure prefill (P only), mixed; a batch
+  with no new token has no scene.
 * Tab. 1 features of a batch {(c_i, u_i)}: x1 = sum over P of c(u + c),
-  x2 = sum over P of c^2, x3 = sum of u over all requests, x4 = |D|,
-  x5 = sum over D of u, x6 = sum over P of c, x7 = max over P of c (0 if P is
-  empty), with D = {c <= 1}, P = {c > 1} (Eq. 2).
+  x2 = sum over P of c^2, x3 = sum of u over the batch's requests (P and D),
+  x4 = |D|, x5 = sum over D of u, x6 = sum over P of c, x7 = max over P of c
+  (0 if P is empty).
 * Eq. 5 per model: latency = b + sum_{j=1..7} w_j x_j.  (The printed sum runs
   over j = 0..7 with a separate intercept; read here as j = 1..7 plus b.)
 * "Model training": a global model on all samples, and a scene's own model
@@ -36,10 +40,10 @@ SCENES = (SCENE_PURE_DECODE, SCENE_PURE_PREFILL, SCENE_MIXED)
 def scene(q_len, ctx_len) -> int:
     """Eq. 3 scene of a batch (0 for an empty batch)."""
     c = np.asarray(q_len)
-    if c.size == 0:
-        return 0
     n_p = int((c > 1).sum())
-    n_d = int((c <= 1).sum())
+    n_d = int((c == 1).sum())
+    if n_p + n_d == 0:
+        return 0
     if n_p == 0:
         return SCENE_PURE_DECODE
     if n_d == 0:
@@ -52,11 +56,11 @@ def features(q_len, ctx_len) -> np.ndarray:
     c = np.asarray(q_len, dtype=np.float64)
     u = np.asarray(ctx_len, dtype=np.float64)
     p = c > 1
-    d = ~p
+    d = c == 1
     return np.array([
         float(np.sum(c[p] * (u[p] + c[p]))),
         float(np.sum(c[p] ** 2)),
-        float(np.sum(u)),
+        float(np.sum(u[p | d])),
         float(d.sum()),
         float(np.sum(u[d])),
         float(np.sum(c[p])),

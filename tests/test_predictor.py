@@ -51,12 +51,16 @@ def samples(n, seed, noise=0.0):
 # ---------------------------------------------------------------- oracle pins
 
 def test_features_and_scene_worked_by_hand():
-    # P = {(5, 10), (3, 0)}, D = {(1, 7), (0, 4)} (Eq. 2 puts c = 0 in D)
+    # P = {(5, 10), (3, 0)}, D = {(1, 7)}; the request (0, 4) has no new token
+    # and is in neither set (the reading of Eq. 2 for c = 0)
     c, u = [5, 1, 3, 0], [10, 7, 0, 4]
-    assert list(orc.features(c, u)) == [5 * 15 + 3 * 3, 25 + 9, 21, 2, 11, 8, 5]
+    assert list(orc.features(c, u)) == [5 * 15 + 3 * 3, 25 + 9, 10 + 7 + 0, 1, 7, 8, 5]
     assert orc.scene(c, u) == orc.SCENE_MIXED
     assert orc.scene([1, 0], [3, 3]) == orc.SCENE_PURE_DECODE
     assert orc.scene([4, 2], [0, 9]) == orc.SCENE_PURE_PREFILL
+    assert orc.scene([4, 0], [0, 9]) == orc.SCENE_PURE_PREFILL
+    assert orc.scene([0, 0], [5, 9]) == 0
+    assert list(orc.features([0, 0], [5, 9])) == [0] * 7
     assert orc.scene([], []) == 0
 
 
@@ -64,6 +68,11 @@ def test_features_match_the_planner():
     rng = np.random.default_rng(1)
     for s in (1, 2, 3):
         c, u = random_batch(rng, s)
+        # requests with no new token this iteration, anywhere in the batch
+        for _ in range(3):
+            k = int(rng.integers(0, len(c) + 1))
+            c.insert(k, 0)
+            u.insert(k, int(rng.integers(0, 4096)))
         shape = ssa.make_shape(32, 8, 128, 1 << 20, max((a + b + 15) // 16 for a, b in zip(c, u)),
                                128 ** -0.5)
         _, info = ssa.ssa_plan(shape, c, u)
