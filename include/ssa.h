@@ -224,6 +224,26 @@ int ssa_check_block_table(const ssa_shape* shape, const void* plan_host,
                           const int32_t* block_table_host);
 
 /*
+ * Layout conversion of a value pool, for callers that keep value pages in the
+ * key pool's token-major layout.  It is not an operation of the paper: the
+ * paged cache that every batch attends over (Sec. 3.2) only fixes which page
+ * and slot hold a token, and these kernels read value pages dim-major.
+ *   to_dim_major = 1: src [num_pages, Hkv, P, D] (P slots of D values) ->
+ *                     dst [num_pages, Hkv, D, P] (D rows of P slots, v_cache
+ *                     as the calls above take it);
+ *   to_dim_major = 0: the inverse, dst [num_pages, Hkv, P, D].
+ *   Uses num_kv_heads, head_dim, page_size and num_pages of the shape (the
+ *   other fields are not read).  src and dst are device pointers, 16-byte
+ *   aligned, to whole pools that must not overlap (no in-place conversion);
+ *   the bytes are moved unchanged.  One kernel launch on stream.
+ * Errors: NULL; SHAPE (num_kv_heads < 1); HEAD_DIM; PAGE_SIZE; PAGES
+ * (num_pages < 1, or a grid beyond 2^31 workgroups); ARG (to_dim_major not 0 or
+ * 1, a misaligned pointer, or overlapping pools); HIP.
+ */
+int ssa_v_pool_convert(const ssa_shape* shape, const uint16_t* src, uint16_t* dst,
+                       int32_t to_dim_major, void* stream);
+
+/*
  * KV append (one kernel): new token j of request i, at position t = u_i + j,
  * is copied bit for bit from k_new/v_new row (q_start_i + j) into page
  * block_table[i][t / P], slot t % P, of k_cache / v_cache.  No other pool

@@ -16,7 +16,7 @@ LIB = os.path.join(HERE, "libssa.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["ssa_kernels.hip", "ssa_layer.hip", "ssa_gemm.hip", "ssa_layer_forward.cpp", "ssa_probe.hip", "ssa_plan.cpp", "ssa_predictor.cpp", "ssa_scheduler.cpp"]
+SOURCES = ["ssa_kernels.hip", "ssa_pool.hip", "ssa_layer.hip", "ssa_gemm.hip", "ssa_layer_forward.cpp", "ssa_probe.hip", "ssa_plan.cpp", "ssa_predictor.cpp", "ssa_scheduler.cpp"]
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
     # no packed-fp32 VALU forms anywhere in the device code

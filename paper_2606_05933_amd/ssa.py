@@ -175,6 +175,8 @@ def _load():
     lib.ssa_linear.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     lib.ssa_rms_norm.argtypes = [i32, i32, vp, vp, ctypes.c_float, vp, vp]
     lib.ssa_check_block_table.argtypes = [P(SsaShape), vp, vp]
+    lib.ssa_v_pool_convert.argtypes = [P(SsaShape), vp, vp, i32, vp]
+    lib.ssa_v_pool_convert.restype = ctypes.c_int
     lib.ssa_probe_hbm_read.argtypes = [vp, sz, vp, i32, vp]
     lib.ssa_probe_hbm_gather.argtypes = [vp, sz, vp, i32, i32, i32, vp, i32, vp]
     lib.ssa_probe_mfma_bf16.argtypes = [i32, i32, vp, vp]
@@ -195,7 +197,7 @@ def _load():
 LIB = _load()
 
 EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_check_block_table",
-            "ssa_kv_append",
+            "ssa_v_pool_convert", "ssa_kv_append",
             "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed",
             "ssa_append_attention", "ssa_append_attention_static", "ssa_predictor_init",
             "ssa_predictor_add",
@@ -589,6 +591,19 @@ def linear(x, w, out, epilogue: int = EPILOGUE_NONE, residual=None, workspace=No
                         ctypes.c_size_t(ws_bytes), vp(_stream(stream)))
     if rc != SSA_OK:
         raise SsaError(rc, "ssa_linear")
+
+
+def v_pool_convert(shape: SsaShape, src, dst, to_dim_major: bool = True, stream=None):
+    """ssa_v_pool_convert: a value pool [num_pages, Hkv, 16, D] -> [num_pages, Hkv, D, 16]
+    (to_dim_major) or back, device tensors of 2-byte elements."""
+    numel = shape.num_pages * shape.num_kv_heads * shape.page_size * shape.head_dim
+    _check_dev("src", src, numel, 2)
+    _check_dev("dst", dst, numel, 2)
+    vp = ctypes.c_void_p
+    rc = LIB.ssa_v_pool_convert(ctypes.byref(shape), vp(_ptr(src)), vp(_ptr(dst)),
+                                int(bool(to_dim_major)), vp(_stream(stream)))
+    if rc != SSA_OK:
+        raise SsaError(rc, "ssa_v_pool_convert")
 
 
 def rms_norm(x, weight, out, eps: float = 1e-5, stream=None):
