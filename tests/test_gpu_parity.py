@@ -219,20 +219,33 @@ def sampled_parity(b, n_chunk_rows=24, heads_per_row=4, seed=0):
     got = out[np.array(sel_rows), np.array(sel_heads)]
     assert_close(got, ref, f"{b.name} sampled")
     assert np.isfinite(out).all(), "non-finite output outside the sample"
+    assert db.status() == 0
+    return db.out.clone()
 
 
 @pytest.mark.parametrize("name,chunk,prefix", [
     ("multi", 1024, None), ("l70b", 2048, None), ("l8b", 2048, None), ("l70b", 1536, None),
+    ("l70b_tp8", 2048, 131072), ("l70b_tp8", 4096, 262144),
 ])
 def test_extra_sweep_rows_sampled_parity(torch_dev, name, chunk, prefix):
     """Latency-table rows beyond the five configurations (chunk sizes of the
     sweep; at c = 1536 the planner cuts every 70B chunk tile in two key pieces
-    to fill the last round of workgroup slots): the oracle at sampled (row,
-    head) pairs."""
+    to fill the last round of workgroup slots), and long contexts (a chunk on a
+    128K- or 256K-token prefix: chunk tiles of up to 266K keys cut into many
+    key pieces): the oracle at sampled (row, head) pairs, and the fused launch
+    equal to the two launches bit for bit."""
+    import torch
     from paper_2606_05933_amd import workload
+    from paper_2606_05933_amd.device import DeviceBatch
     b = workload.make_workload(name, seed=0, chunk=chunk, prefix=prefix)
     b.name = f"{name}(c={chunk},u={prefix})"
-    sampled_parity(b)
+    two = sampled_parity(b)
+    say(f"[gpu fused] {b.name}")
+    fz = DeviceBatch(b)
+    fz.step_fused()
+    torch.cuda.synchronize()
+    assert fz.status() == 0
+    assert torch.equal(fz.out.view(torch.int16), two.view(torch.int16)), "fused != two launches"
 
 
 def both_paths_parity(b):
