@@ -296,6 +296,17 @@ def test_full_size_parity_both_paths(torch_dev, name, chunk, prefix):
     both_paths_parity(b)
 
 
+def test_long_decode_contexts_both_paths(torch_dev):
+    """Decode rows over 64K-256K cached tokens (up to 64 key pieces per row and
+    kv head, merged in one group) beside a chunk on an empty cache: every
+    element against the oracle on both launch paths."""
+    from paper_2606_05933_amd import workload
+    b = workload.make_batch(workload.Shape(16, 2, 128), [1, 1, 1, 1, 256],
+                            [262143, 200000, 131071, 65536, 0], seed=7, spare_pages=3,
+                            name="long-decodes")
+    both_paths_parity(b)
+
+
 def test_random_small_batches_both_paths(torch_dev):
     """100 seeded random batches: group size 1..16, head dim 64 or 128, 1..6
     requests with c in [0, 300] (a third of them decodes) and u in [0, 5000],
