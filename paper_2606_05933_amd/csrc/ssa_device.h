@@ -47,6 +47,13 @@ __device__ __forceinline__ void dma16(const void* g, const char* l) {
     asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(a) : "memory");
 }
 
+// dma16 with the non-temporal hint (nt), for rows a workgroup reads once: they
+// should not displace what the caches hold for other workgroups.
+__device__ __forceinline__ void dma16_stream(const void* g, const char* l) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)l;
+  asm volatile("global_load_lds_dwordx4 %0, off nt" ::"v"(g), "{m0}"(a) : "memory");
+}
+
 // s_waitcnt vmcnt(N): all but this wave's N most recent vector-memory
 // operations (LDS copies included) have completed.
 template <int N>

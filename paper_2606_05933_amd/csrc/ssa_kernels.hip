@@ -1010,7 +1010,9 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
   }
   // Key rows pass through LDS: each wave owns two stages of one 32-key block
   // (the chunk path's swizzled row layout), filled with global_load_lds so
-  // that every load instruction reads whole key rows; the MFMA operands are
+  // that every load instruction reads whole key rows (non-temporal, like the
+  // value loads: a decode reads each row once, while chunk tiles beside it
+  // reread theirs from the caches); the MFMA operands are
   // then read from LDS in the permuted-key layout.  Value rows (dim-major
   // pages) load straight into registers, 16 bytes of 8 slots of one dim per
   // lane.  Both are issued as inline assembly and waited for with exact
@@ -1039,8 +1041,8 @@ __device__ void decode_item(const AttnArgs& a, const WorkItem& it, const ReqEntr
 #pragma unroll
     for (int r = 0; r < KLOADS; ++r) {
       const int key = r * C::KROWS_PER_LOAD + lane / C::CPR;
-      dma16(a.kc + (size_t)((key >> 4) ? pg1 : pg0) * page_stride + head_off + kgo[r],
-            kst + stage * C::K_STAGE + r * 1024);
+      dma16_stream(a.kc + (size_t)((key >> 4) ? pg1 : pg0) * page_stride + head_off + kgo[r],
+                   kst + stage * C::K_STAGE + r * 1024);
     }
     const uint16_t* vs = a.vc + (size_t)((g >> 1) ? pg1 : pg0) * page_stride + head_off +
                          r16 * 16 + (g & 1) * 8;
