@@ -99,7 +99,7 @@ typedef struct ssa_shape {
  *                    many keys (multiple of 32); default: chosen by the planner
  *   decode_split_keys a decode key range of k keys is cut into
  *                    max(1, round(k / decode_split_keys)) equal pieces, each a
- *                    multiple of 32 keys (multiple of 32; default 4096)
+ *                    multiple of 32 keys (multiple of 32; default 3072)
  *   num_cus          compute units the planner balances for (default 256)
  *   num_xcds         if > 1, die-aware placement: workgroups are taken to be
  *                    dealt to num_xcds dies round-robin (workgroup b on die

@@ -42,7 +42,7 @@ constexpr double kSplitCostKeys = 768.0;
 // enough that the load latency at the start of an item is amortised over 32
 // blocks per wave, short enough that long and short contexts balance over the
 // compute units; partial records cost G*(D+2) floats per piece.
-constexpr int kDefaultDecodeSplitKeys = 4096;
+constexpr int kDefaultDecodeSplitKeys = 3072;
 
 // Work items of one launch: their blob section must stay within the int32
 // offsets of the plan header (and the grid within 2^31 workgroups).
