@@ -28,7 +28,10 @@
  *     arguments are validated before any HIP call; on an error nothing is
  *     written and nothing is launched.  No C++ exception crosses this ABI and
  *     nothing is printed.
- *   - The library allocates no memory and keeps no state between calls.
+ *   - The library allocates no memory and keeps no state between calls, with
+ *     two exceptions: the per-GPU scratch of ssa_append_attention_static, and
+ *     the fork/join events of ssa_append_attention_streams (two per host
+ *     thread and device, created on first use).
  *   - "bf16" arguments are bfloat16 bit patterns (uint16_t); they are device
  *     pointers unless the name ends in _host.
  *   - stream is a hipStream_t passed as void* (NULL = the null stream).
@@ -118,7 +121,18 @@ typedef struct ssa_shape {
  *                    interleaved (workgroups 0 .. num_cus-1 are taken to land on
  *                    distinct units, the next num_cus on their second slots),
  *                    4 = as 3, then the other decode items, then the other
- *                    chunk items
+ *                    chunk items,
+ *                    5 = for ssa_append_attention_streams: where the
+ *                    two-stream split pays (head_dim 128, Hq/Hkv <= 8,
+ *                    1.5 * num_cus to 2 * num_cus chunk items (one round of
+ *                    two per compute unit), and at least 0.9 of the
+ *                    decode rows' K/V bytes fit beside the chunk rows: bytes at
+ *                    2.5 TB/s over the chunk rows' time at 0.95 PFLOP/s, the
+ *                    rates measured on MI355X with the two side by side), all
+ *                    chunk items first and the split recorded in the plan;
+ *                    elsewhere as 0, and the call runs as one launch,
+ *                    6 = the split forced (for tests): chunk items first, half
+ *                    of the decode items beside the chunk rows, half after
  *   append_wait_polls  ssa_append_attention: polls (about 0.25 us each) before a
  *                    chunk item's wait for the rows appended in the same launch
  *                    gives up and sets SSA_STATUS_WAIT_TIMEOUT (default 2^21,
@@ -348,6 +362,50 @@ int ssa_append_attention_static(const ssa_shape* shape, const void* plan_host,
                                 const uint16_t* v_new, uint16_t* k_cache, uint16_t* v_cache,
                                 const int32_t* block_table, uint16_t* out, void* stream,
                                 void* start_event, void* stop_event);
+
+/*
+ * One iteration (Sec. 3.2) with the chunked-prefill rows (Sec. 2.1; Tab. 1
+ * x1/x2) and the decode rows (Tab. 1 x4/x5) in launches of their own that run
+ * at the same time on two streams, where the plan asks for it (tuning
+ * mix_order 5 or 6); otherwise exactly ssa_append_attention on `stream`.  Same
+ * inputs, outputs, pool image and workspace rules as ssa_append_attention.
+ *   Why: a CU holds two chunk workgroups, and the decode kernel of this call is
+ *   built to fit in the registers and LDS they leave (80 VGPRs per lane, 8 KB),
+ *   so its workgroups stream the decode rows' K/V beside the chunk tiles
+ *   instead of taking their slots, as the decode items of one launch do.  It
+ *   pays where the chunk tiles fill both slots of every CU and the decode rows
+ *   fit in their time (mix_order 5 decides; on the 70B-shaped batch the pair
+ *   takes about 0.9 of the one launch).
+ *   Split: the first streams_beside decode items of the plan (ssa_plan
+ *   records how many) run on `decode_stream`, in launches of at most one
+ *   workgroup per CU, beside the chunk rows' launch on `stream`; the other
+ *   decode items run in one launch on `stream` after the chunk rows.  The chunk
+ *   rows' outputs and the pool image are bit for bit those of
+ *   ssa_append_attention with the same plan; the decode rows' outputs agree
+ *   to within fp32 summation order (their kernel splits the head dim over its
+ *   waves).
+ *   stream, decode_stream: hipStream_t as void* (NULL: the null stream).  The
+ *   call records an event on `stream` that `decode_stream` waits for, and
+ *   makes `stream` wait for an event recorded on `decode_stream` after its
+ *   launches: work queued on `stream` after the call sees the whole iteration.
+ *   The events belong to the library, one pair per host thread and device.  The
+ *   two streams should map to different hardware queues (on ROCm, streams are
+ *   dealt round-robin to GPU_MAX_HW_QUEUES queues): on one queue the launches
+ *   run one after the other, with the same results.
+ *   One launch on `stream` (ssa_append_attention) instead: plans without the
+ *   split, shapes the decode kernel does not take (head_dim 64, Hq/Hkv > 8),
+ *   batches without decode rows.  A split plan without chunk rows runs its
+ *   decode kernel on `stream` alone.
+ *   start_event, stop_event: optional timing events recorded on `stream` before
+ *   the fork and after the join (so they span both streams' launches).
+ * Errors: those of ssa_append_attention.
+ */
+int ssa_append_attention_streams(const ssa_shape* shape, const void* plan_host,
+                                 const void* plan_dev, const uint16_t* q, const uint16_t* k_new,
+                                 const uint16_t* v_new, uint16_t* k_cache, uint16_t* v_cache,
+                                 const int32_t* block_table, uint16_t* out, void* workspace,
+                                 size_t workspace_bytes, void* stream, void* decode_stream,
+                                 void* start_event, void* stop_event);
 
 #ifdef __cplusplus
 }

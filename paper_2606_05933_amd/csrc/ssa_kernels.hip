@@ -113,6 +113,9 @@ struct AttnArgs {
   // launch); 0 for a plain attention launch
   int append_wgs, num_chunk_items;
   int wait_polls;  // polls before the wait for appended rows gives up
+  // two-stream launch: the chunk launch's last workgroup sets the dispatch
+  // flag when it starts (every workgroup of the launch has then been placed)
+  int signal_dispatched;
   // fused launch: this iteration's new key / value rows ([T, Hkv, D])
   const uint16_t* k_new;
   const uint16_t* v_new;
@@ -1178,6 +1181,273 @@ __global__ __launch_bounds__(kThreads, 2) void mixed_attention_kernel(AttnArgs a
   attention_wg<D, false>(a, it, lds);
 }
 
+// ---------------------------------------------- decode rows on a second stream
+//
+// The decode items of ssa_append_attention_streams, in a kernel of their own
+// that runs beside the chunk rows' launch.  A CU holds two chunk workgroups
+// (two waves of 216 registers per SIMD, 64 KB of LDS each); this kernel is
+// built to fit in what they leave, 80 registers per lane and 32 KB, so that one
+// of its workgroups runs on every CU as a third resident workgroup and streams
+// the decode rows' K/V while the chunk tiles compute.
+//
+// The 4 waves split the head dim (wave w owns dims 32w .. 32w+31) and walk the
+// same 32-key blocks of the item.  QK tile p of a block holds the 16 keys of
+// its page p (A row r = slot r; this wave's 32 dims), so the output gives lane
+// group g keys 4g..4g+3 of each page: element e of the lane's 8 probabilities
+// is key 16*(e/4) + 4g + e%4, and the V operand takes the same keys (8 bytes of
+// 4 slots of one dim from each dim-major page).  Each wave's partial logits
+// (over its dims) are summed through LDS: G <= 8, so only columns 0..7 hold
+// logits and lanes 8..15 of each row carry those of the second tile; one
+// 16-byte record per lane, double-buffered, one barrier per block.  Every wave
+// then forms the same probabilities and accumulates O for its own dims.
+// Every load reads one page through a buffer resource of that page's head (16
+// slots x D, range-checked), non-temporal, with a loop-invariant lane offset;
+// the loads of two blocks are in flight (K of block i+2 issued once block i's
+// QK MFMAs have read their operands, V once its PV MFMAs have).
+constexpr int kStreamMaxG = 8;
+constexpr int kWaitDispatchedPolls = 2048;  // about 1 ms
+constexpr int kStreamD = 128;
+constexpr int kCachePolicyNt = 2;  // buffer-load cache policy: non-temporal
+
+// value of lane (l & ~15) | ((l + 8) & 15): rotate each row of 16 lanes by 8
+__device__ __forceinline__ float row_ror8(float x) {
+  return as_f32((unsigned)__builtin_amdgcn_update_dpp(0, (int)as_u32(x), 0x128, 0xF, 0xF, false));
+}
+
+// Keep the bf16 elements whose bit is set in `valid`, zero the others.
+__device__ __forceinline__ u32x4 keep_valid(u32x4 v, unsigned valid) {
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t m = (((valid >> (2 * i)) & 1) ? 0x0000FFFFu : 0u) |
+                       (((valid >> (2 * i + 1)) & 1) ? 0xFFFF0000u : 0u);
+    r[i] = v[i] & m;
+  }
+  return r;
+}
+
+// One decode item.  xs: each wave's partial logits of the current block,
+// [buffer][wave][lane]; s_last: the merge ticket's verdict (both in LDS).
+__device__ __forceinline__ void decode_stream_item(const AttnArgs& a, const WorkItem& it,
+                                                   f32x4 (&xs)[2][kWaves][64], int& s_last) {
+  constexpr int D = kStreamD;
+  ReqEntry rq;
+  rq.q_start = it.q_start;
+  rq.ctx_len = it.ctx_len;
+  rq.q_len = it.nvalid - it.ctx_len;
+  rq.n_pages = (it.nvalid + 15) >> 4;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, r16 = lane & 15;
+  const int G = a.G;
+  cint32* bt = (cint32*)a.bt + (size_t)it.req * a.maxp;
+  const size_t page_stride = (size_t)a.hkv * 16 * D;
+  const size_t head_off = (size_t)it.kvh * 16 * D;
+  const int key0 = it.key0, key1 = it.key1;
+  const int nb = (key1 - key0 + 31) / 32;
+
+  // The item that holds key u appends the request's new row first: each wave
+  // stores its own 32 dims of the key row and of the value column of slot u
+  // and waits for them; those are the only bytes of the slot that wave reads
+  // back, and no other workgroup reads the slot in this launch.
+  if (rq.q_len > 0 && key0 <= rq.ctx_len && rq.ctx_len < key1) {
+    const size_t new_off = ((size_t)rq.q_start * a.hkv + it.kvh) * D + 32 * w;
+    const size_t pg = (size_t)bt[rq.ctx_len >> 4] * page_stride + head_off;
+    const int slot = rq.ctx_len & 15;
+    uint16_t* kp = const_cast<uint16_t*>(a.kc) + pg + slot * D + 32 * w;
+    uint16_t* vp = const_cast<uint16_t*>(a.vc) + pg + (size_t)(32 * w) * 16 + slot;
+    if (lane < 4) st16(kp + lane * 8, ld16(a.k_new + new_off + lane * 8));
+    if (lane < 32) vp[lane * 16] = a.v_new[new_off + lane];
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+
+  bf16x8 qop = as_bf16x8(u32x4{0, 0, 0, 0});
+  if (r16 < G)
+    qop = as_bf16x8(ld16(a.q + ((size_t)rq.q_start * a.hq + it.kvh * G + r16) * D + 32 * w + 8 * g));
+
+  const int voffK = r16 * (2 * D) + 2 * (32 * w + 8 * g);  // bytes: slot r16, 8 dims
+  const int voffV = (32 * w + r16) * 32 + 8 * g;           // bytes: dim row, slots 4g..4g+3
+  const uint16_t* kbase = a.kc + head_off;
+  const uint16_t* vbase = a.vc + head_off;
+  auto rsrc = [&](const uint16_t* base, int pg) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base) + (size_t)pg * page_stride,
+                                             (short)0, 16 * D * 2, 0x00020000);
+  };
+  // the block's two pages; a page past the request's last one is read from the
+  // first (in range; its keys are at or past key1 and masked)
+  auto pages = [&](int i, int& pg0, int& pg1) {
+    const int lp0 = (key0 + min(i, nb - 1) * 32) >> 4;
+    pg0 = bt[lp0];
+    pg1 = (lp0 + 1 < rq.n_pages) ? bt[lp0 + 1] : pg0;
+  };
+  auto issue_k = [&](int i, u32x4 (&r)[4]) {
+    int pg0, pg1;
+    pages(i, pg0, pg1);
+    r[0] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc(kbase, pg0), voffK, 0, kCachePolicyNt));
+    r[1] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc(kbase, pg1), voffK, 0, kCachePolicyNt));
+  };
+  auto issue_v = [&](int i, u32x4 (&r)[4]) {
+    int pg0, pg1;
+    pages(i, pg0, pg1);
+    const auto v0 = rsrc(vbase, pg0), v1 = rsrc(vbase, pg1);
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      const u32x2 lo = __builtin_bit_cast(
+          u32x2, __builtin_amdgcn_raw_buffer_load_b64(v0, voffV, mt * 512, kCachePolicyNt));
+      const u32x2 hi = __builtin_bit_cast(
+          u32x2, __builtin_amdgcn_raw_buffer_load_b64(v1, voffV, mt * 512, kCachePolicyNt));
+      r[2 + mt] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+    }
+  };
+
+  float m_run = kNegInf, l_run = 0.f;
+  f32x4 o[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  const bool lo8 = r16 < 8;
+  // block i (keys key0 + 32 i ..) from r; then r takes block nxt's loads
+  auto step = [&](int i, u32x4 (&r)[4], int nxt) {
+    const int kb = key0 + i * 32;
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    const f32x4 s0 = mfma(as_bf16x8(r[0]), qop, z);
+    const f32x4 s1 = mfma(as_bf16x8(r[1]), qop, z);
+    issue_k(nxt, r);
+    const int buf = i & 1;
+    f32x4 x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      // the rotate reads other lanes: it runs in every lane, never under a
+      // branch on lo8 (where the lanes it reads would be inactive)
+      float rr = row_ror8(s1[j]);
+      asm volatile("" : "+v"(rr));
+      x[j] = lo8 ? s0[j] : rr;
+    }
+    xs[buf][w][lane] = x;
+    __syncthreads();
+    // the four partials in a fixed order (the same sum in every wave), one
+    // read in flight at a time
+    f32x4 t = xs[buf][0][lane];
+#pragma unroll
+    for (int ww = 1; ww < kWaves; ++ww) {
+      asm volatile("" : "+v"(t)::"memory");
+      t += xs[buf][ww][lane];
+    }
+    float sv[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float rr = row_ror8(t[j]);
+      asm volatile("" : "+v"(rr));
+      sv[j] = t[j];
+      sv[4 + j] = rr;
+    }
+    // element e of the lane: key kb + 16*(e/4) + 4g + e%4, valid below key1
+    unsigned valid = 0xFFu;
+    if (kb + 32 > key1) {
+      const int l0 = key1 - (kb + 4 * g), l1 = key1 - (kb + 16 + 4 * g);
+      const unsigned m0 = l0 <= 0 ? 0u : (l0 >= 4 ? 0xFu : (1u << l0) - 1u);
+      const unsigned m1 = l1 <= 0 ? 0u : (l1 >= 4 ? 0xFu : (1u << l1) - 1u);
+      valid = m0 | (m1 << 4);
+      r[2] = keep_valid(r[2], valid);
+      r[3] = keep_valid(r[3], valid);
+    }
+    const bf16x8 pop = softmax_step<2, true>(sv, valid, a.scale_log2, m_run, l_run, o);
+    o[0] = mfma(as_bf16x8(r[2]), pop, o[0]);
+    o[1] = mfma(as_bf16x8(r[3]), pop, o[1]);
+    issue_v(nxt, r);
+  };
+
+  // Every wave runs every block, in pairs (a padding block past the item's
+  // last one is masked for every key: its loads repeat the last block), so the
+  // waits and barriers match across waves.
+  vm_wait<0>();
+  u32x4 ra[4], rb[4];
+  issue_k(0, ra);
+  issue_v(0, ra);
+  issue_k(1, rb);
+  issue_v(1, rb);
+  const int n2 = (nb + 1) / 2 * 2;
+  for (int i = 0; i < n2; i += 2) {
+    step(i, ra, i + 2);
+    step(i + 1, rb, i + 3);
+  }
+  const float l = wave_sum_cols(l_run);
+
+  float* rec = nullptr;
+  MergeGroup grp{};
+  if (it.group >= 0) {
+    grp = reinterpret_cast<const MergeGroup*>(a.plan + a.off_groups)[it.group];
+    rec = reinterpret_cast<float*>(a.ws + a.ws_partials_off) + grp.ws_off +
+          (int64_t)it.split * rec_floats(G, D);
+  }
+  // lane (g, r16) holds dims 32w + 16mt + 4g .. +3 of column r16
+  if (r16 < G) {
+    if (rec) {
+      if (w == 0 && g == 0) {
+        st_dev(rec + r16, m_run);
+        st_dev(rec + G + r16, l);
+      }
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+        st16_dev(rec + rec_o_off(G) + (int64_t)r16 * D + 32 * w + 16 * mt + 4 * g,
+                 __builtin_bit_cast(u32x4, o[mt]));
+    } else {
+      const float inv = 1.f / l;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+        store_bf16x4(a.out + ((size_t)rq.q_start * a.hq + it.kvh * G + r16) * D + 32 * w + 16 * mt +
+                         4 * g,
+                     o[mt][0] * inv, o[mt][1] * inv, o[mt][2] * inv, o[mt][3] * inv);
+    }
+  }
+  if (!rec) return;
+  // the last of the group's items merges the records (as finish_split)
+  int* tickets = reinterpret_cast<int*>(a.ws) + kLaunchCounters;
+  wait_vm_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int prev = __hip_atomic_fetch_add(&tickets[it.group], 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (prev == grp.nsplit - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  // G * D / 4 <= kThreads units: one pass of the decode merge
+  static_assert(kStreamMaxG * (D / 4) <= kThreads, "one merge pass");
+  const RecordReader rd(reinterpret_cast<const float*>(a.ws + a.ws_partials_off) + grp.ws_off);
+  merge_pass<D, 1, 4, 4>(a, it, rq, rd, grp.ncols, grp.nsplit, 0);
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&tickets[it.group], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// On the decode stream of a two-stream launch, ahead of the decode launch: wait
+// until the chunk launch has placed all its workgroups (its last one sets the
+// flag when it starts), so that decode workgroups only take the slots the
+// chunk tiles leave, then clear the flag (zero at rest).  Where the two streams
+// share a hardware queue this kernel runs after the chunk launch and finds the
+// flag set.  Bounded: after `polls` polls (about half a microsecond each) the
+// decode launch goes ahead anyway.
+__global__ __launch_bounds__(64) void wait_dispatched_kernel(int* flag, int polls) {
+  for (int i = 0; i < polls; ++i) {
+    if (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) break;
+    __builtin_amdgcn_s_sleep(16);
+  }
+  if (threadIdx.x == 0) __hip_atomic_store(flag, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One decode item per workgroup: item item0 + blockIdx.x of the plan.
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(6, 8)))
+void decode_stream_kernel(AttnArgs a, int item0) {
+  __shared__ __attribute__((aligned(16))) f32x4 xs[2][kWaves][64];
+  __shared__ int s_last;
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
+  const WorkItem it = reinterpret_cast<const WorkItem*>(a.plan + a.off_items)[item0 + (int)blockIdx.x];
+  if (hdr->magic != kPlanMagic || hdr->hash != a.hash) {
+    if (threadIdx.x == 0) report(a.ws, SSA_STATUS_PLAN_MISMATCH);
+    return;
+  }
+  decode_stream_item(a, it, xs, s_last);
+}
+
 // ------------------------------------------------------------------ kv_append
 
 struct AppendArgs {
@@ -1320,6 +1590,8 @@ __global__ __launch_bounds__(kThreads, 2) void append_attention_kernel(AttnArgs 
   __shared__ __attribute__((aligned(16))) char lds[Cfg<D>::LDS];
   const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(a.plan);
   int* counters = reinterpret_cast<int*>(a.ws);
+  if (a.signal_dispatched && blockIdx.x == gridDim.x - 1 && threadIdx.x == 0)
+    __hip_atomic_store(&counters[kWsDispatched], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if ((int)blockIdx.x < a.append_wgs) {
     const AppendSeg sg = reinterpret_cast<const AppendSeg*>(a.plan + ap.off_segments)[blockIdx.x];
     if (hdr->magic != kPlanMagic || hdr->hash != a.hash) {
@@ -1434,6 +1706,7 @@ int attention_args(const ssa_shape* shape, const void* plan_host, const void* pl
   a->append_wgs = 0;
   a->num_chunk_items = h->num_chunk_items;
   a->wait_polls = h->wait_polls;
+  a->signal_dispatched = 0;
   a->k_new = nullptr;
   a->v_new = nullptr;
   return SSA_OK;
@@ -1603,6 +1876,121 @@ int ssa_append_attention_static(const ssa_shape* shape, const void* plan_host,
   if (rc) return rc;
   a.ws = static_cast<uint8_t*>(ws);
   return launch_append_attention(h, a, ap, stream, start_event, stop_event);
+}
+
+}  // extern "C"
+
+// ------------------------------------------------ the two-stream launch pair
+
+namespace {
+// Fork and join events of ssa_append_attention_streams, per host thread and
+// device (created on first use, kept until the thread ends): two threads never
+// record the same event.
+struct ForkJoin {
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+thread_local ForkJoin t_fork_join[kMaxScratchDevices];
+
+int fork_join_events(ForkJoin** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return SSA_ERR_HIP;
+  ForkJoin& fj = t_fork_join[dev];
+  for (hipEvent_t* e : {&fj.fork, &fj.join}) {
+    if (*e) continue;
+    if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) {
+      *e = nullptr;
+      (void)hipGetLastError();
+      return SSA_ERR_HIP;
+    }
+  }
+  *out = &fj;
+  return SSA_OK;
+}
+
+// The plan puts every chunk item before every decode item, and decode items
+// start on 32-key block boundaries (both as the planner writes them with
+// mix_order 1).
+bool chunk_items_first(const PlanHeader* h, const void* plan_host) {
+  const WorkItem* items =
+      reinterpret_cast<const WorkItem*>(static_cast<const uint8_t*>(plan_host) + h->off_items);
+  for (int i = 0; i < h->num_items; ++i) {
+    const bool chunk = i < h->num_chunk_items;
+    if ((items[i].kind == kItemChunk) != chunk) return false;
+    if (!chunk && (items[i].key0 & 31)) return false;
+  }
+  return true;
+}
+}  // namespace
+
+extern "C" {
+
+int ssa_append_attention_streams(const ssa_shape* shape, const void* plan_host,
+                                 const void* plan_dev, const uint16_t* q, const uint16_t* k_new,
+                                 const uint16_t* v_new, uint16_t* k_cache, uint16_t* v_cache,
+                                 const int32_t* block_table, uint16_t* out, void* workspace,
+                                 size_t workspace_bytes, void* stream, void* decode_stream,
+                                 void* start_event, void* stop_event) {
+  const PlanHeader* h = nullptr;
+  AttnArgs a;
+  AppendArgs ap;
+  int rc = append_attention_args(shape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
+                                 block_table, out, workspace, workspace_bytes, &h, &a, &ap);
+  if (rc || h->num_items == 0) return rc;
+  // the one-launch path on `stream`: a plan that does not ask for the split,
+  // shapes the decode kernel does not take, batches without decode rows
+  const int nd = h->num_decode_items;
+  if (h->streams_beside < 0 || h->head_dim != kStreamD || a.G > kStreamMaxG || nd == 0 ||
+      !chunk_items_first(h, plan_host))
+    return launch_append_attention(h, a, ap, stream, start_event, stop_event);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipStream_t sd = static_cast<hipStream_t>(decode_stream);
+  ForkJoin* fj = nullptr;
+  rc = fork_join_events(&fj);
+  if (rc) return rc;
+  (void)clear_and_check();
+  bool ok = true;
+  if (start_event) ok = ok && hipEventRecord(static_cast<hipEvent_t>(start_event), s) == hipSuccess;
+  const bool two = h->num_chunk_items > 0;
+  if (two) {
+    ok = ok && hipEventRecord(fj->fork, s) == hipSuccess;
+    ok = ok && hipStreamWaitEvent(sd, fj->fork, 0) == hipSuccess;
+    // the chunk rows (two workgroups per CU); the last workgroup to be placed
+    // releases the decode launch
+    AttnArgs ca = a;
+    ca.signal_dispatched = 1;
+    void* cargs[] = {&ca, &ap};
+    ok = ok && hipExtLaunchKernel(reinterpret_cast<const void*>(&append_attention_kernel<kStreamD>),
+                                  dim3(a.append_wgs + h->num_chunk_items), dim3(kThreads), cargs, 0,
+                                  s, nullptr, nullptr, 0) == hipSuccess;
+  }
+  // decode items: the first `beside` of them (longest first) on the decode
+  // stream once the chunk launch has placed its workgroups, the rest in one
+  // launch on the chunk stream after the chunk rows
+  const int beside = two ? std::min(h->streams_beside, nd) : 0;
+  const void* dfn = reinterpret_cast<const void*>(&decode_stream_kernel);
+  if (beside > 0) {
+    int* flag = reinterpret_cast<int*>(a.ws) + kWsDispatched;
+    int polls = kWaitDispatchedPolls;
+    void* wargs[] = {&flag, &polls};
+    ok = ok && hipExtLaunchKernel(reinterpret_cast<const void*>(&wait_dispatched_kernel), dim3(1),
+                                  dim3(64), wargs, 0, sd, nullptr, nullptr, 0) == hipSuccess;
+    int item0 = h->num_chunk_items;
+    void* dargs[] = {&a, &item0};
+    ok = ok && hipExtLaunchKernel(dfn, dim3(beside), dim3(kThreads), dargs, 0, sd, nullptr, nullptr,
+                                  0) == hipSuccess;
+  }
+  if (beside < nd) {
+    int item0 = h->num_chunk_items + beside;
+    void* dargs[] = {&a, &item0};
+    ok = ok && hipExtLaunchKernel(dfn, dim3(nd - beside), dim3(kThreads), dargs, 0, s, nullptr,
+                                  nullptr, 0) == hipSuccess;
+  }
+  if (two) {
+    ok = ok && hipEventRecord(fj->join, sd) == hipSuccess;
+    ok = ok && hipStreamWaitEvent(s, fj->join, 0) == hipSuccess;
+  }
+  if (stop_event) ok = ok && hipEventRecord(static_cast<hipEvent_t>(stop_event), s) == hipSuccess;
+  return ok && hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
 }
 
 }  // extern "C"

@@ -57,10 +57,27 @@ constexpr int kOrderPairedDecodeFirst = 4;
 constexpr double kPairedMinRatio = 0.85;
 // automatic order: paired, then the other decode items first, from this ratio up
 constexpr double kPairedDecodeFirstRatio = 0.25;
+// mix_order values for ssa_append_attention_streams: automatic, and the split
+// forced (half of the decode items beside the chunk rows, half after them)
+constexpr int kOrderStreamsAuto = 5;
+constexpr int kOrderStreamsForced = 6;
+// The two-stream split (ssa_append_attention_streams) pays where the chunk
+// items fill both slots of (nearly) every compute unit in one round, so that
+// decode work can only take a third slot beside them and no chunk tile waits
+// for a slot that decode work holds, and where the decode rows nearly all fit in
+// the time the chunk rows take: decode bytes streamed at the rate that one
+// decode workgroup per CU reaches beside two chunk tiles, for the chunk rows'
+// flops at their rate with that company (both measured on MI355X, on the
+// 70B-shaped batch).  The decode items that fit run beside, the rest after.
+constexpr double kBesideChunkFlops = 0.95e15;  // chunk rows, flop/s
+constexpr double kBesideDecodeBytes = 2.5e12;  // decode rows, bytes/s
+constexpr double kBesideMinCover = 0.9;        // share of the decode bytes that must fit
+constexpr double kBesideMinFill = 1.5;         // chunk items per compute unit, at least
 
 struct Tuning {
   int tile_cols, chunk_split_keys, decode_split_keys, num_cus, num_xcds, mix_order, wait_polls;
   int auto_order;  // the caller left mix_order at 0: the planner picks it (int: no padding)
+  int streams;     // 0: one-launch plan; 1: split when it pays (mix_order 5); 2: forced (6)
 };
 
 int check_shape(const ssa_shape* s) {
@@ -76,7 +93,8 @@ int check_shape(const ssa_shape* s) {
 }
 
 int resolve_tuning(const ssa_tuning* t, Tuning* out) {
-  Tuning r{kDefaultTileCols, 0, 0, kDefaultCus, kDefaultXcds, kOrderChunkFirst, kDefaultWaitPolls, 1};
+  Tuning r{kDefaultTileCols, 0,    0, kDefaultCus, kDefaultXcds, kOrderChunkFirst, kDefaultWaitPolls,
+           1,                0};
   if (t) {
     if (t->chunk_tile_cols) {
       if (t->chunk_tile_cols != 32 && t->chunk_tile_cols != 64 && t->chunk_tile_cols != 128)
@@ -87,14 +105,20 @@ int resolve_tuning(const ssa_tuning* t, Tuning* out) {
     if (t->decode_split_keys < 0 || t->decode_split_keys % kBlockKeys) return SSA_ERR_TUNING;
     if (t->num_cus < 0 || t->num_cus > 4096) return SSA_ERR_TUNING;
     if (t->num_xcds < 0 || t->num_xcds > 64) return SSA_ERR_TUNING;
-    if (t->mix_order < 0 || t->mix_order > 4) return SSA_ERR_TUNING;
+    if (t->mix_order < 0 || t->mix_order > kOrderStreamsForced) return SSA_ERR_TUNING;
     if (t->append_wait_polls < 0) return SSA_ERR_TUNING;
     if (t->append_wait_polls) r.wait_polls = t->append_wait_polls;
     r.chunk_split_keys = t->chunk_split_keys;
     r.decode_split_keys = t->decode_split_keys;
     if (t->num_cus) r.num_cus = t->num_cus;
     if (t->num_xcds) r.num_xcds = t->num_xcds;
-    if (t->mix_order) {
+    if (t->mix_order == kOrderStreamsAuto) {
+      r.streams = 1;  // the automatic order, or chunk items first where the split pays
+    } else if (t->mix_order == kOrderStreamsForced) {
+      r.streams = 2;
+      r.mix_order = kOrderChunkFirst;
+      r.auto_order = 0;
+    } else if (t->mix_order) {
       r.mix_order = t->mix_order;
       r.auto_order = 0;
     }
@@ -528,9 +552,24 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   //    faster than all chunk items first on the 70B-shaped layer, ratio 0.56,
   //    where interleaving the rest is 20% slower: a long chunk tile that
   //    starts late is the launch's tail).
-  if (tu.auto_order) {
-    size_t nchunk = 0;
-    for (const WorkItem& it : raw) nchunk += it.kind == kItemChunk;
+  //
+  // mix_order 5 (for ssa_append_attention_streams): where the two-stream split
+  // pays, all chunk items first and the split recorded in the plan; otherwise
+  // the automatic order and one launch.
+  size_t nchunk = 0;
+  double decode_kv_bytes = 0;
+  for (const WorkItem& it : raw) {
+    if (it.kind == kItemChunk) nchunk++;
+    else decode_kv_bytes += (double)(it.key1 - it.key0) * 4.0 * D;
+  }
+  const double beside_budget = in.chunk_flops / kBesideChunkFlops * kBesideDecodeBytes;
+  const bool split = tu.streams == 2 ||
+                     (tu.streams == 1 && D == 128 && Hq / Hkv <= 8 &&
+                      nchunk >= kBesideMinFill * tu.num_cus && nchunk <= 2 * (size_t)tu.num_cus &&
+                      decode_kv_bytes > 0 &&
+                      beside_budget >= kBesideMinCover * decode_kv_bytes);
+  if (split) tu.mix_order = kOrderChunkFirst;
+  if (tu.auto_order && !split) {
     const double t_dec = in.decode_bytes / kHbmRate;
     const double t_chk = in.chunk_flops / (kMfmaRatePerCu * tu.num_cus);
     if (nchunk >= 2 * (size_t)tu.num_cus && t_dec >= kPairedMinRatio * t_chk)
@@ -577,6 +616,21 @@ int build(const ssa_shape* s, const int32_t* q_len, const int32_t* ctx_len, int3
   h.chunk_tile_cols = tu.tile_cols;
   h.softmax_scale = s->softmax_scale;
   h.wait_polls = tu.wait_polls;
+  h.streams_beside = -1;
+  if (split) {
+    // the decode items follow the chunk items, longest first
+    const int nd = in.num_decode_items;
+    int beside = (nd + 1) / 2;
+    if (tu.streams == 1) {
+      double bytes = 0;
+      for (beside = 0; beside < nd; ++beside) {
+        const WorkItem& it = p->items[in.num_chunk_items + beside];
+        bytes += (double)(it.key1 - it.key0) * 4.0 * D;
+        if (bytes > beside_budget) break;
+      }
+    }
+    h.streams_beside = beside;
+  }
   // the blob's section offsets are int32 fields: a plan beyond 2 GiB (or a
   // grid beyond 2^31 workgroups) is refused
   int64_t off = sizeof(PlanHeader);

@@ -6,7 +6,8 @@
 //   [MergeGroup x num_groups][AppendSeg x num_segments]
 //
 // The workspace holds kLaunchCounters int32 words (a fused launch's two
-// counters, the sticky status word of ssa.h, one spare) and one int32 ticket
+// counters, the sticky status word of ssa.h, the two-stream launch's dispatch
+// flag) and one int32 ticket
 // per merge group (counters and tickets zero at rest), padded to 256 bytes, then,
 // at ws_partials_off, fp32 partial results:
 // for merge group g and split s, a record of rec_floats(ncols, D) floats at
@@ -19,13 +20,14 @@
 namespace ssa {
 
 constexpr uint32_t kPlanMagic = 0x31415353u;  // "SSA1"
-constexpr uint32_t kPlanVersion = 4;
+constexpr uint32_t kPlanVersion = 5;
 constexpr int kBlockKeys = 32;  // keys per attention block: two 16-slot pages
 constexpr int kWaves = 4;       // waves per workgroup
 constexpr int kThreads = 256;   // threads per workgroup
 constexpr int kChunkWaveCols = 32;  // columns a wave owns in a chunk tile
 constexpr int kLaunchCounters = 4;  // workspace words ahead of the merge tickets
 constexpr int kWsStatusWord = 2;    // the status word among them (ssa.h)
+constexpr int kWsDispatched = 3;    // set once a chunk launch has started all its workgroups
 constexpr int kDefaultWaitPolls = 1 << 21;
 
 // Float offset of o in a partial record of ncols columns, and the record's size.
@@ -49,7 +51,10 @@ struct PlanHeader {
   float softmax_scale;
   int32_t num_chunk_segments;  // segments of chunk requests (c > 1): the first ones
   int32_t wait_polls;          // polls before a fused launch's wait for appended rows gives up
-  int32_t reserved;
+  // ssa_append_attention_streams: decode items (the first ones after the chunk
+  // items) that run beside the chunk rows on the decode stream, the others
+  // after them; -1: the call runs as one launch
+  int32_t streams_beside;
 };
 static_assert(sizeof(PlanHeader) == 128, "plan header size");
 

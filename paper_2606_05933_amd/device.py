@@ -102,6 +102,9 @@ class DeviceBatch:
         # calls bound once per slot (on the stream current now): an iteration
         # only crosses into the library
         self._info_scratch = ssa.SsaPlanInfo()
+        if not hasattr(self, "decode_stream"):
+            # the second stream of ssa_append_attention_streams
+            self.decode_stream = torch.cuda.Stream(self.device)
         self._bound = []
         for hb, db in zip(self._host, self._dev):
             self._bound.append((
@@ -112,7 +115,11 @@ class DeviceBatch:
                                          self.block_table, self.out, self.workspace),
                 ssa.bind_append_attention(self.shape, hb, db, self.q, self.k_new, self.v_new,
                                           self.k_cache, self.v_cache, self.block_table, self.out,
-                                          self.workspace)))
+                                          self.workspace),
+                ssa.bind_append_attention_streams(self.shape, hb, db, self.q, self.k_new,
+                                                  self.v_new, self.k_cache, self.v_cache,
+                                                  self.block_table, self.out, self.workspace,
+                                                  decode_stream=self.decode_stream)))
         torch.cuda.synchronize(self.device)
         return self.info
 
@@ -175,6 +182,18 @@ class DeviceBatch:
         self._bound[self._slot][3](start, stop)
         self._done[self._slot] = stop
 
+    def step_streams(self, events=(None, None)):
+        """The iteration as two launches side by side (ssa_append_attention_streams):
+        the chunk rows on the current stream, the decode rows on this batch's
+        decode stream, joined back into the current stream.  The plan must list
+        chunk items first (tuning mix_order = 1).  The stop event, recorded after
+        the join, marks the slot's kernels done."""
+        start, stop = events
+        if stop is None:
+            stop = self._own_done[self._slot]
+        self._bound[self._slot][4](start, stop)
+        self._done[self._slot] = stop
+
     def status(self) -> int:
         """The workspace's status word (ssa.h: SSA_STATUS_* bits) after the
         launches issued so far have completed."""
@@ -191,6 +210,12 @@ class DeviceBatch:
         (int32, host copy): every word but the status is zero at rest."""
         n = ssa.WS_LAUNCH_WORDS + self.info.num_merge_groups
         return self.workspace[:4 * n].view(torch.int32).cpu().numpy()
+
+    def plan_header_field(self, name: str) -> int:
+        """An int32 field of the current plan's header (ssa_plan_format.h)."""
+        fields = {"num_items": 6, "num_chunk_items": 7, "num_decode_items": 8,
+                  "wait_polls": 30, "streams_beside": 31}
+        return int(self.plan_host[:128].view(torch.int32)[fields[name]].item())
 
     def out_f32(self) -> np.ndarray:
         return self.out.float().cpu().numpy()

@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libssa.so")
 
 SSA_OK = 0
 SSA_ERR_NULL, SSA_ERR_WORKSPACE, SSA_ERR_HIP, SSA_ERR_ARG = -1, -8, -10, -13
+SSA_ERR_PLAN_MISMATCH = -9
 # the workspace's status word (ssa.h): byte offset and error bits
 SSA_WS_STATUS_OFFSET = 8
 SSA_STATUS_WAIT_TIMEOUT, SSA_STATUS_PLAN_MISMATCH = 1, 2
@@ -158,6 +159,9 @@ def _load():
     lib.ssa_append_attention_static.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                 vp, vp]
     lib.ssa_append_attention_static.restype = ctypes.c_int
+    lib.ssa_append_attention_streams.argtypes = [P(SsaShape), vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                 vp, sz, vp, vp, vp, vp]
+    lib.ssa_append_attention_streams.restype = ctypes.c_int
     dp = P(ctypes.c_double)
     lib.ssa_predictor_init.argtypes = [P(SsaPredictor), ctypes.c_int32]
     lib.ssa_predictor_add.argtypes = [P(SsaPredictor), dp, ctypes.c_int32, ctypes.c_double]
@@ -199,7 +203,8 @@ LIB = _load()
 EXPORTED = ("ssa_status_string", "ssa_plan_size", "ssa_plan", "ssa_check_block_table",
             "ssa_v_pool_convert", "ssa_kv_append",
             "ssa_mixed_attention", "ssa_kv_append_timed", "ssa_mixed_attention_timed",
-            "ssa_append_attention", "ssa_append_attention_static", "ssa_predictor_init",
+            "ssa_append_attention", "ssa_append_attention_static",
+            "ssa_append_attention_streams", "ssa_predictor_init",
             "ssa_predictor_add",
             "ssa_predictor_fit", "ssa_predictor_predict", "ssa_form_batch", "ssa_time_to_budget",
             "ssa_sliding_chunker", "ssa_priority_sort", "ssa_batch_constructor",
@@ -740,10 +745,8 @@ def layer_forward(shape: SsaShape, plan_host, plan_dev, weights: LayerWeights, x
         raise SsaError(rc, "ssa_layer_forward")
 
 
-def bind_append_attention(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
-                          block_table, out, workspace, stream=None) -> BoundCall:
-    """ssa_append_attention (kv_append and mixed attention in one launch);
-    calling the result takes optional (start, stop) events."""
+def _check_fused_buffers(shape: SsaShape, plan_host, q, k_new, v_new, k_cache, v_cache,
+                         block_table, out):
     h = _plan_header(plan_host)
     T, n = h["num_tokens"], h["num_reqs"]
     qrow = shape.num_q_heads * shape.head_dim
@@ -756,31 +759,47 @@ def bind_append_attention(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new,
     _check_dev("k_cache", k_cache, pool, 2)
     _check_dev("v_cache", v_cache, pool, 2)
     _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+
+
+def _fused_args(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
+                block_table, out, workspace):
+    _check_fused_buffers(shape, plan_host, q, k_new, v_new, k_cache, v_cache, block_table, out)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     vp = ctypes.c_void_p
-    args = (ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)), vp(_ptr(q)),
+    return (ctypes.byref(shape), vp(_ptr(plan_host)), vp(_ptr(plan_dev)), vp(_ptr(q)),
             vp(_ptr(k_new)), vp(_ptr(v_new)), vp(_ptr(k_cache)), vp(_ptr(v_cache)),
-            vp(_ptr(block_table)), vp(_ptr(out)), vp(_ptr(workspace)), ctypes.c_size_t(ws_bytes),
-            vp(_stream(stream)))
-    return BoundCall(LIB.ssa_append_attention, "ssa_append_attention", args, timed=True)
+            vp(_ptr(block_table)), vp(_ptr(out)), vp(_ptr(workspace)), ctypes.c_size_t(ws_bytes))
+
+
+def bind_append_attention(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
+                          block_table, out, workspace, stream=None) -> BoundCall:
+    """ssa_append_attention (kv_append and mixed attention in one launch);
+    calling the result takes optional (start, stop) events."""
+    args = _fused_args(shape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
+                       block_table, out, workspace)
+    return BoundCall(LIB.ssa_append_attention, "ssa_append_attention",
+                     args + (ctypes.c_void_p(_stream(stream)),), timed=True)
+
+
+def bind_append_attention_streams(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache,
+                                  v_cache, block_table, out, workspace, stream=None,
+                                  decode_stream=None) -> BoundCall:
+    """ssa_append_attention_streams (the chunk rows on `stream`, the decode rows
+    beside them on `decode_stream`); the plan must list chunk items first
+    (tuning mix_order = 1).  Calling the result takes optional (start, stop)
+    events, recorded on `stream` around both launches."""
+    args = _fused_args(shape, plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache,
+                       block_table, out, workspace)
+    vp = ctypes.c_void_p
+    return BoundCall(LIB.ssa_append_attention_streams, "ssa_append_attention_streams",
+                     args + (vp(_stream(stream)), vp(_stream(decode_stream))), timed=True)
 
 
 def append_attention_static(shape: SsaShape, plan_host, plan_dev, q, k_new, v_new, k_cache,
                             v_cache, block_table, out, stream=None, events=(None, None)):
     """ssa_append_attention_static: the fused launch with the library's own
     per-GPU scratch in place of a workspace (nothing is allocated)."""
-    h = _plan_header(plan_host)
-    T, n = h["num_tokens"], h["num_reqs"]
-    qrow = shape.num_q_heads * shape.head_dim
-    row = shape.num_kv_heads * shape.head_dim
-    pool = shape.num_pages * shape.num_kv_heads * shape.page_size * shape.head_dim
-    _check_dev("q", q, T * qrow, 2)
-    _check_dev("out", out, T * qrow, 2)
-    _check_dev("k_new", k_new, T * row, 2)
-    _check_dev("v_new", v_new, T * row, 2)
-    _check_dev("k_cache", k_cache, pool, 2)
-    _check_dev("v_cache", v_cache, pool, 2)
-    _check_dev("block_table", block_table, n * shape.max_pages_per_req, 4)
+    _check_fused_buffers(shape, plan_host, q, k_new, v_new, k_cache, v_cache, block_table, out)
     vp = ctypes.c_void_p
     start, stop = events
     _check(LIB.ssa_append_attention_static(

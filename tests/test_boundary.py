@@ -385,6 +385,69 @@ def test_launchers_validate_before_any_hip_call():
     assert L.ssa_append_attention(ctypes.byref(shape), q, fake, *args, ws, None, None, None) == -9
 
 
+def test_streams_launcher_validates_before_any_hip_call():
+    """ssa_append_attention_streams checks what ssa_append_attention checks, in
+    every launch order, before any HIP call."""
+    q_len = np.array([40, 1, 1, 64], np.int32)
+    ctx_len = np.array([5000, 3000, 9000, 100], np.int32)
+    shape = shape_of(32, 8, 128, q_len, ctx_len)
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
+    L = ssa.LIB
+    args = [fake] * 8  # q, k_new, v_new, k_cache, v_cache, block_table, out, workspace
+    other = shape_of(32, 8, 128, q_len, ctx_len, num_pages=77)
+    for order in range(7):
+        tu = ssa.make_tuning(decode_split_keys=1024, mix_order=order, num_cus=4)
+        blob, info = ssa.ssa_plan(shape, q_len, ctx_len, tu)
+        _, ws = ssa.ssa_plan_size(shape, q_len, ctx_len, tu)
+        p = blob.ctypes.data
+        assert L.ssa_append_attention_streams(ctypes.byref(shape), p, None, *args, ws, None,
+                                              fake, None, None) == -1
+        assert L.ssa_append_attention_streams(ctypes.byref(other), p, fake, *args, ws, None,
+                                              fake, None, None) == -9
+        assert L.ssa_append_attention_streams(ctypes.byref(shape), p, fake, *args, ws - 1, None,
+                                              fake, None, None) == -8
+        nulls = list(args)
+        nulls[1] = None  # k_new
+        assert L.ssa_append_attention_streams(ctypes.byref(shape), p, fake, *nulls, ws, None,
+                                              fake, None, None) == -1
+    assert plan_rc(shape, q_len, ctx_len, tuning=ssa.make_tuning(mix_order=7))[0] == -12
+
+
+def _streams_split(name, chunk=None, tuning=None):
+    shape, q_len, ctx_len = workload.workload_lengths(name, seed=0, chunk=chunk)
+    s = ssa.make_shape(shape.hq, shape.hkv, shape.d, 1 << 20, 4096, shape.softmax_scale)
+    blob, info = ssa.ssa_plan(s, q_len, ctx_len, tuning)
+    h, _, items, _, _ = parse(blob)
+    return int(h["reserved"][1]), items["kind"], info
+
+
+def test_plan_records_the_two_stream_split():
+    """The plan's streams_beside field: -1 (one launch) unless mix_order asks for
+    the two-stream launch.  Order 5 splits where the chunk items fill both slots
+    of every unit in one round and the decode bytes fit beside the chunk rows
+    (the 70B-shaped batch at c = 1024: every decode item beside), with chunk
+    items first; elsewhere it keeps the automatic one-launch order and -1.
+    Order 6 always splits, half of the decode items beside."""
+    for order in (0, 1, 2, 3, 4):
+        beside, _, _ = _streams_split("l70b", tuning=ssa.make_tuning(mix_order=order))
+        assert beside == -1
+    beside, kinds, info = _streams_split("l70b", None, ssa.make_tuning(mix_order=5))
+    nc = info.num_chunk_items
+    assert nc == 512 and (kinds[:nc] == 0).all() and (kinds[nc:] == 1).all()
+    assert beside == info.num_decode_items
+    # two rounds of chunk tiles (c = 2048), fewer than 1.5 per unit (c = 512),
+    # or a decode part too large for the chunk rows' time (l8b): one launch, in
+    # the automatic order
+    for name, chunk in (("l70b", 2048), ("l70b", 512), ("l8b", None), ("l8b", 2048),
+                        ("multi", None)):
+        beside, kinds, _ = _streams_split(name, chunk, ssa.make_tuning(mix_order=5))
+        auto, kinds0, _ = _streams_split(name, chunk, None)
+        assert beside == -1 and auto == -1 and np.array_equal(kinds, kinds0), (name, chunk)
+    beside, kinds, info = _streams_split("l8b", None, ssa.make_tuning(mix_order=6))
+    nc = info.num_chunk_items
+    assert (kinds[:nc] == 0).all() and beside == (info.num_decode_items + 1) // 2
+
+
 def test_block_table_check_covers_exactly_the_entries_the_kernels_read():
     # request 3 has no new token: no work item and no append segment reads its row
     from paper_2606_05933_amd import workload
