@@ -298,14 +298,26 @@ def traffic_bytes(workload):
     return (t["fetch_kib"] / t["copy_fetch_factor"] + t["write_kib"] / t["copy_write_factor"]) * 1024
 
 
-def fused_line(db, steps, warmup):
-    """Back-to-back steps (host plan into the free slot + one fused launch):
-    wall time per step, the average fused kernel time from events the kernel
-    stamps itself on every TIME_EVERY-th step, and host time per step."""
+def chunk_launch_bytes(b, info):
+    """Algorithmic bytes of the chunk rows' launch of a two-stream iteration:
+    the chunk requests' K/V, q and out rows, and the append of their new rows
+    (read from k_new / v_new, written to the pools)."""
+    s = b.shape
+    chunk_tokens = int(b.q_len[b.q_len > 1].sum())
+    return info.chunk_bytes + chunk_tokens * s.hkv * s.d * 2 * 2 * 2
+
+
+def fused_line(db, steps, warmup, streams=False):
+    """Back-to-back steps (host plan into the free slot + the iteration's
+    launch: the fused launch, or with streams the two-stream pair): wall time
+    per step, the average time of the launch that stamps the events (the fused
+    launch, or the chunk rows' launch of the pair) on every TIME_EVERY-th step,
+    and host time per step."""
     import torch
+    launch = db.step_streams if streams else db.step_fused
     for _ in range(warmup):
         db.replan_host()
-        db.step_fused()
+        launch()
     torch.cuda.synchronize()
     timed = list(range(0, steps, TIME_EVERY))
     evs = {i: [torch.cuda.Event(enable_timing=True) for _ in range(2)] for i in timed}
@@ -319,9 +331,9 @@ def fused_line(db, steps, warmup):
         tp = time.perf_counter()
         db.replan_host()   # host plan into the other (device-mapped) plan slot
         if i in evs:
-            db.step_fused(events=(evs[i][0], evs[i][1]))
+            launch(events=(evs[i][0], evs[i][1]))
         else:
-            db.step_fused()
+            launch()
         host_s.append(time.perf_counter() - tp)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -329,36 +341,69 @@ def fused_line(db, steps, warmup):
     return wall / steps, fused_s, statistics.mean(host_s)
 
 
+def iteration_samples(db, n, flush=None):
+    """Durations (s) of n two-stream iterations (db.step_streams), from events
+    recorded on the launch stream around each call (the fork to the join)."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(n)]
+    for a, z in evs:
+        a.record()
+        z.record()
+    torch.cuda.synchronize()
+    for a, z in evs:
+        if flush is not None:
+            flush()
+        a.record()
+        db.step_streams()
+        z.record()
+    torch.cuda.synchronize()
+    return [a.elapsed_time(z) / 1e3 for a, z in evs]
+
+
 def main_bench(args):
     import torch
-    from paper_2606_05933_amd import workload
+    from paper_2606_05933_amd import ssa, workload
     from paper_2606_05933_amd.device import DeviceBatch
 
     torch.cuda.set_device(0)
     log(f"[bench] generating {args.workload} seed={args.seed}")
     b = workload.make_workload(args.workload, seed=args.seed)
-    db = DeviceBatch(b)
+    # the iteration: ssa_append_attention_streams with the planner's choice
+    # (mix_order 5): the chunk rows and the decode rows on two streams where
+    # that pays, else one launch
+    db = DeviceBatch(b, ssa.make_tuning(mix_order=5))
     info = db.info
+    split = db.plan_header_field("streams_beside") >= 0 and info.num_chunk_items > 0
     log(f"[bench] items={info.num_items} (chunk {info.num_chunk_items}, decode "
-        f"{info.num_decode_items}) groups={info.num_merge_groups} scene={info.scene}")
+        f"{info.num_decode_items}) groups={info.num_merge_groups} scene={info.scene} "
+        f"two streams={split}")
 
     # the timed region: K back-to-back steps
-    step_s, fused_s, host_s = fused_line(db, args.steps, args.warmup)
-    assert db.status() == 0, "the fused launch reported an error"
-    # context, after the timed region: the same launch with a cold cache, and the
-    # iteration as two launches
+    step_s, kern_s, host_s = fused_line(db, args.steps, args.warmup, streams=True)
+    assert db.status() == 0, "the iteration's launches reported an error"
+    # context, after the timed region: the iteration with a cold cache, and the
+    # one-launch iteration (ssa_append_attention, the planner's automatic
+    # order) warm, cold and as two launches
     flush = Flusher()
-    cold = kernel_event_samples(db.step_fused, 10, flush)
+    cold = iteration_samples(db, 10, flush)
     cold_p50, cold_p10, cold_p90 = percentiles_us(cold)
-    app_s = time_kernel_events(db.kv_append, 20)
-    attn_s = time_kernel_events(db.attention, 20)
+    one = DeviceBatch(b, pools=(db.k_cache, db.v_cache, db.block_table))
+    one_step_s, fused_s, _ = fused_line(one, 20, 5)
+    cold1_p50, cold1_p10, cold1_p90 = percentiles_us(kernel_event_samples(one.step_fused, 10, flush))
+    app_s = time_kernel_events(one.kv_append, 20)
+    attn_s = time_kernel_events(one.attention, 20)
+    assert one.status() == 0, "the one-launch iteration reported an error"
+    del one
     tp = time.perf_counter()
     for _ in range(200):
         db._bound[0][0]()
     plan_s = (time.perf_counter() - tp) / 200
-    log(f"[bench] step {step_s * 1e6:.1f} us, fused launch {fused_s * 1e6:.1f} us warm, "
-        f"{cold_p50:.1f} us cold (as two launches: kv_append {app_s * 1e6:.1f} us, attention "
-        f"{attn_s * 1e6:.1f} us), host per step {host_s * 1e6:.1f} us, plan {plan_s * 1e6:.1f} us")
+    log(f"[bench] step {step_s * 1e6:.1f} us ({'two streams: chunk launch' if split else 'one launch'} "
+        f"{kern_s * 1e6:.1f} us), {cold_p50:.1f} us cold; one launch: step "
+        f"{one_step_s * 1e6:.1f} us, launch {fused_s * 1e6:.1f} us warm, {cold1_p50:.1f} us cold "
+        f"(as two launches: kv_append {app_s * 1e6:.1f} us, attention {attn_s * 1e6:.1f} us); "
+        f"host per step {host_s * 1e6:.1f} us, plan {plan_s * 1e6:.1f} us")
 
     # each segment alone (Eq. 3's pure scenes), cold cache
     segs = {}
@@ -373,32 +418,42 @@ def main_bench(args):
     log("[bench] segments alone (cold): "
         + ", ".join(f"{k} {v['us']} us" for k, v in segs.items()))
 
-    # roofline of the fused launch: its algorithmic bytes (every K/V byte read
-    # once, the append's rows read and written once) at the HBM peak and its
-    # chunk flops at the bf16 MFMA peak; the larger floor names the bound
-    alg_bytes = info.decode_bytes + info.chunk_bytes + info.append_bytes
+    # roofline of the dominant kernel: with two streams the chunk rows' launch
+    # (its own bytes: the chunk requests' K/V, q, out and appended rows), else
+    # the one fused launch (every K/V byte read once, the append's rows read and
+    # written once); bytes at the HBM peak, chunk flops at the bf16 MFMA peak,
+    # the larger floor names the bound
+    all_bytes = info.decode_bytes + info.chunk_bytes + info.append_bytes
+    alg_bytes = chunk_launch_bytes(b, info) if split else all_bytes
     t_hbm = alg_bytes / (HBM_PEAK_GBS * 1e9)
     t_mfma = info.chunk_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
     tb = traffic_bytes(args.workload)
     if t_mfma > t_hbm:
-        achieved = info.chunk_flops / fused_s / 1e12
+        achieved = info.chunk_flops / kern_s / 1e12
         roofline = {"bound": "mfma", "achieved": round(achieved, 1),
                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4)}
     else:
-        achieved = alg_bytes / fused_s / 1e9
+        achieved = alg_bytes / kern_s / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
-    floor = max(t_hbm, t_mfma)
+    # the whole iteration against its overlap floor: all its bytes at the HBM
+    # peak or its flops at the MFMA peak, whichever is larger
+    floor = max(all_bytes / (HBM_PEAK_GBS * 1e9), t_mfma)
     roofline.update({
         "traffic": None if tb is None else round(tb),
-        "kernel": "append_attention", "kernel_us": round(fused_s * 1e6, 2),
+        "kernel": ("append_attention (the chunk rows' launch of the two-stream iteration)"
+                   if split else "append_attention"),
+        "kernel_us": round(kern_s * 1e6, 2),
         "algorithmic_bytes": round(alg_bytes), "algorithmic_flops": round(info.chunk_flops),
-        "hbm_GBps": round(alg_bytes / fused_s / 1e9, 1),
-        "hbm_frac": round(alg_bytes / fused_s / 1e9 / HBM_PEAK_GBS, 4),
+        "hbm_GBps": round(alg_bytes / kern_s / 1e9, 1),
+        "hbm_frac": round(alg_bytes / kern_s / 1e9 / HBM_PEAK_GBS, 4),
+        "iteration_us": round(step_s * 1e6, 2),
+        "iteration_mfma_frac": round(info.chunk_flops / step_s / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        "iteration_hbm_GBps": round(all_bytes / step_s / 1e9, 1),
         "overlap_floor_us": round(floor * 1e6, 2),
-        "frac_of_overlap_floor": round(floor / fused_s, 4),
-        "sum_of_floors_us": round((t_hbm + t_mfma) * 1e6, 2),
+        "frac_of_overlap_floor": round(floor / step_s, 4),
+        "sum_of_floors_us": round((all_bytes / (HBM_PEAK_GBS * 1e9) + t_mfma) * 1e6, 2),
         "chunk_segment_mfma_frac": segs.get("chunk", {}).get("mfma_frac"),
         "decode_segment_hbm_frac": segs.get("decode", {}).get("hbm_frac"),
     })
@@ -457,9 +512,15 @@ def main_bench(args):
                    "chunk_tokens": int(b.q_len[b.q_len > 1].sum()),
                    "decode_reqs": int((b.q_len == 1).sum())},
         "tokens_per_s": round(b.num_tokens / step_s, 1),
-        "fused_us": round(fused_s * 1e6, 2),
-        "fused_cold_us": {"p50": cold_p50, "p10": cold_p10, "p90": cold_p90},
-        "two_launch": {"kv_append_us": round(app_s * 1e6, 2), "attention_us": round(attn_s * 1e6, 2)},
+        "iteration": {"launch": ("ssa_append_attention_streams: chunk rows and decode rows on "
+                                 "two streams" if split else "ssa_append_attention (one launch)"),
+                      "stamped_launch_us": round(kern_s * 1e6, 2),
+                      "cold_us": {"p50": cold_p50, "p10": cold_p10, "p90": cold_p90}},
+        "one_launch": {"us_per_iter": round(one_step_s * 1e6, 2),
+                       "fused_us": round(fused_s * 1e6, 2),
+                       "fused_cold_us": {"p50": cold1_p50, "p10": cold1_p10, "p90": cold1_p90},
+                       "two_launch": {"kv_append_us": round(app_s * 1e6, 2),
+                                      "attention_us": round(attn_s * 1e6, 2)}},
         "plan_us": round(plan_s * 1e6, 2),
         "host_us_per_step": round(host_s * 1e6, 2),
         "segments_cold": segs,
@@ -678,11 +739,20 @@ def main_only_attention(args):
         b = workload.sub_batch(b, b.q_len == 1)
     elif args.scene == "prefill":
         b = workload.sub_batch(b, b.q_len > 1)
-    db = DeviceBatch(b)
+    from paper_2606_05933_amd import ssa
+    db = DeviceBatch(b, ssa.make_tuning(mix_order=5) if args.streams else None)
     info = db.info
     for _ in range(3):  # warm-up launches (the trace statistics include them)
-        db.step_fused() if args.fused else db.attention()
-    if args.fused:
+        if args.streams:
+            db.step_streams()
+        else:
+            db.step_fused() if args.fused else db.attention()
+    if args.streams:
+        # the chunk rows' launch of the two-stream iteration (its own stamps)
+        us = time_kernel_events(db.step_streams, args.steps) * 1e6
+        assert db.status() == 0, "the two-stream launch reported an error"
+        kernel, nbytes = "append_attention_kernel", chunk_launch_bytes(b, info)
+    elif args.fused:
         # the fused launch appends the rows itself: the algorithmic bytes add them
         us = time_kernel_events(db.step_fused, args.steps) * 1e6
         assert db.status() == 0, "the fused launch reported an error"
@@ -1458,6 +1528,8 @@ def main():
     ap.add_argument("--sweep-workloads", default=None)
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--only-attention", action="store_true")
+    ap.add_argument("--streams", action="store_true",
+                    help="--only-attention: the two-stream iteration (tuning mix_order 5)")
     ap.add_argument("--fused", action="store_true",
                     help="with --only-attention: time the fused launch instead")
     ap.add_argument("--pmc-md", metavar="OUT", default=None,

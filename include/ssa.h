@@ -396,8 +396,12 @@ int ssa_append_attention_static(const ssa_shape* shape, const void* plan_host,
  *   split, shapes the decode kernel does not take (head_dim 64, Hq/Hkv > 8),
  *   batches without decode rows.  A split plan without chunk rows runs its
  *   decode kernel on `stream` alone.
- *   start_event, stop_event: optional timing events recorded on `stream` before
- *   the fork and after the join (so they span both streams' launches).
+ *   start_event, stop_event: optional timing events (as in the _timed calls)
+ *   stamped with the start and end of the chunk rows' launch, the iteration's
+ *   longest kernel (of the one launch where the call runs as one, of the decode
+ *   launch where a split plan has no chunk rows).  They do not mark the end of
+ *   the decode launch: to time the whole iteration, or to know when its plan
+ *   buffer may be reused, record an event on `stream` after the call.
  * Errors: those of ssa_append_attention.
  */
 int ssa_append_attention_streams(const ssa_shape* shape, const void* plan_host,

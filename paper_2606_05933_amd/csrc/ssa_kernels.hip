@@ -1949,7 +1949,7 @@ int ssa_append_attention_streams(const ssa_shape* shape, const void* plan_host,
   if (rc) return rc;
   (void)clear_and_check();
   bool ok = true;
-  if (start_event) ok = ok && hipEventRecord(static_cast<hipEvent_t>(start_event), s) == hipSuccess;
+  hipEvent_t e0 = static_cast<hipEvent_t>(start_event), e1 = static_cast<hipEvent_t>(stop_event);
   const bool two = h->num_chunk_items > 0;
   if (two) {
     ok = ok && hipEventRecord(fj->fork, s) == hipSuccess;
@@ -1961,7 +1961,7 @@ int ssa_append_attention_streams(const ssa_shape* shape, const void* plan_host,
     void* cargs[] = {&ca, &ap};
     ok = ok && hipExtLaunchKernel(reinterpret_cast<const void*>(&append_attention_kernel<kStreamD>),
                                   dim3(a.append_wgs + h->num_chunk_items), dim3(kThreads), cargs, 0,
-                                  s, nullptr, nullptr, 0) == hipSuccess;
+                                  s, e0, e1, 0) == hipSuccess;
   }
   // decode items: the first `beside` of them (longest first) on the decode
   // stream once the chunk launch has placed its workgroups, the rest in one
@@ -1982,14 +1982,13 @@ int ssa_append_attention_streams(const ssa_shape* shape, const void* plan_host,
   if (beside < nd) {
     int item0 = h->num_chunk_items + beside;
     void* dargs[] = {&a, &item0};
-    ok = ok && hipExtLaunchKernel(dfn, dim3(nd - beside), dim3(kThreads), dargs, 0, s, nullptr,
-                                  nullptr, 0) == hipSuccess;
+    ok = ok && hipExtLaunchKernel(dfn, dim3(nd - beside), dim3(kThreads), dargs, 0, s,
+                                  two ? nullptr : e0, two ? nullptr : e1, 0) == hipSuccess;
   }
   if (two) {
     ok = ok && hipEventRecord(fj->join, sd) == hipSuccess;
     ok = ok && hipStreamWaitEvent(s, fj->join, 0) == hipSuccess;
   }
-  if (stop_event) ok = ok && hipEventRecord(static_cast<hipEvent_t>(stop_event), s) == hipSuccess;
   return ok && hipGetLastError() == hipSuccess ? SSA_OK : SSA_ERR_HIP;
 }
 

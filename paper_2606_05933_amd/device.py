@@ -185,14 +185,15 @@ class DeviceBatch:
     def step_streams(self, events=(None, None)):
         """The iteration as two launches side by side (ssa_append_attention_streams):
         the chunk rows on the current stream, the decode rows on this batch's
-        decode stream, joined back into the current stream.  The plan must list
-        chunk items first (tuning mix_order = 1).  The stop event, recorded after
-        the join, marks the slot's kernels done."""
-        start, stop = events
-        if stop is None:
-            stop = self._own_done[self._slot]
-        self._bound[self._slot][4](start, stop)
-        self._done[self._slot] = stop
+        decode stream, joined back into the current stream, where the plan asks
+        for it (tuning mix_order 5 or 6); otherwise the one launch.  events:
+        optional (start, stop) pair stamped by the chunk rows' launch."""
+        self._bound[self._slot][4](*events)
+        # the events (if any) stamp the chunk rows' launch only: the slot is done
+        # once the launch stream has joined the decode stream, after the call
+        done = self._own_done[self._slot]
+        done.record()
+        self._done[self._slot] = done
 
     def status(self) -> int:
         """The workspace's status word (ssa.h: SSA_STATUS_* bits) after the

@@ -186,10 +186,10 @@ def test_streams_plan_without_split_runs_as_one_launch(torch_dev):
     assert torch.equal(s.k_cache.view(torch.int16), f.k_cache.view(torch.int16))
 
 
-def test_streams_events_span_both_launches(torch_dev):
-    """Timing events are recorded on the launch stream around the fork and the
-    join: the span covers the decode kernel too, and timed calls give the same
-    bytes as untimed ones."""
+def test_streams_events_stamp_the_chunk_launch(torch_dev):
+    """Timing events are stamped by the chunk rows' launch itself (the pair's
+    longest kernel): inside the span of events recorded on the stream around
+    the call; timed calls give the same bytes as untimed ones."""
     import torch
     from paper_2606_05933_amd import workload
     from paper_2606_05933_amd.device import DeviceBatch
@@ -198,16 +198,21 @@ def test_streams_events_span_both_launches(torch_dev):
     db.step_streams()
     torch.cuda.synchronize()
     ref = db.out.clone()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    e1.record()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in evs:
+        e.record()
     db.out.zero_()
-    db.step_streams(events=(e0, e1))
+    torch.cuda.synchronize()
+    outer0, k0, k1, outer1 = evs
+    outer0.record()
+    db.step_streams(events=(k0, k1))
+    outer1.record()
     torch.cuda.synchronize()
     assert torch.equal(db.out.view(torch.int16), ref.view(torch.int16))
-    us = e0.elapsed_time(e1) * 1e3
-    say(f"    streams call span {us:.1f} us")
-    assert us > 0
+    kernel_us, span_us = k0.elapsed_time(k1) * 1e3, outer0.elapsed_time(outer1) * 1e3
+    say(f"    chunk launch {kernel_us:.1f} us, whole call {span_us:.1f} us")
+    assert 0 < kernel_us <= span_us
+    assert outer0.elapsed_time(k0) >= 0 and k1.elapsed_time(outer1) >= 0
 
 
 def test_streams_call_replays_from_a_graph(torch_dev):
