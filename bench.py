@@ -836,13 +836,15 @@ def main_pmc_md(args):
         ("dispatches (trace / counter passes a, b, c, d)", f"{calls} / {nd['a']}, {nd['b']}, {nd['c']}, {nd['d']}"),
         ("kernel duration, trace average (all dispatches / after the 3 warm-up launches)",
          f"{dur_ns / 1e3:.1f} / {warm_ns / 1e3:.1f} us"),
-        ("GRBM_GUI_ACTIVE per die", f"{gui:.4g} cycles -> clock {clock:.3f} GHz"),
+        ("GRBM_GUI_ACTIVE per die", f"{gui:.4g} cycles" if args.pmc_concurrent
+         else f"{gui:.4g} cycles -> clock {clock:.3f} GHz"),
         ("MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES / (GUI per die x 1024 SIMDs)", f"{busy:.3f}"),
         ("MFMA flops: 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16", f"{mops:.4g}"
          + (f" (algorithmic {alg_flops:.4g})" if alg_flops else "")),
         ("MFMA rate over the trace duration", f"{mops / dur_ns / 1e3:.1f} TFLOP/s = "
          f"{mops / dur_ns / 1e3 / MFMA_BF16_PEAK_TFLOPS:.3f} of {MFMA_BF16_PEAK_TFLOPS:.0f}"
-         f" ({mops / dur_ns / 1e3 / (MFMA_BF16_PEAK_TFLOPS * clock / 2.4):.3f} of the peak at {clock:.2f} GHz)"),
+         + ("" if args.pmc_concurrent else
+            f" ({mops / dur_ns / 1e3 / (MFMA_BF16_PEAK_TFLOPS * clock / 2.4):.3f} of the peak at {clock:.2f} GHz)")),
         ("SQ_INSTS_MFMA / SQ_WAVES", f"{m['SQ_INSTS_MFMA']:.4g} / {m['SQ_WAVES']:.0f}"),
         ("SQ_BUSY_CU_CYCLES / (GUI per die x 256 CUs)", f"{m['SQ_BUSY_CU_CYCLES'] / (gui * 256):.3f}"),
         ("VALU instructions, SQ_ACTIVE_INST_VALU (quad-cycles)", f"{m['SQ_INSTS_VALU']:.4g}, {m['SQ_ACTIVE_INST_VALU']:.4g}"),
@@ -863,6 +865,11 @@ def main_pmc_md(args):
            + (DESCR.get(run['workload'], run['workload']) + f", scene {run['scene']}" if run else "?") + ".", "",
            "| quantity | value |", "|---|---|"]
     out += [f"| {k} | {v} |" for k, v in rows]
+    if args.pmc_concurrent:
+        out += ["", "The kernel trace runs the iteration's two streams side by side, so the durations (and",
+                "the rates over them) are the kernel's inside the pair.  The counter runs serialise the",
+                "two streams' kernels, so the counts are the kernel's own; no clock is derived, since",
+                "the two kinds of run differ in timing."]
     out += ["", "Commands (from the repository root, after `cd /tmp && export TMPDIR=/tmp` and back):", "", "```"]
     for p, cs in PMC_PASSES.items():
         out.append(f"rocprofv3 --pmc {cs} -d DIR/{p} -o run --output-format csv -- {cmd}")
@@ -870,7 +877,8 @@ def main_pmc_md(args):
     out.append("rocprofv3 --pmc FETCH_SIZE -d DIR/e -o run --output-format csv -- python3 bench.py --copy-probe --steps 3")
     out.append("rocprofv3 --pmc WRITE_SIZE -d DIR/f -o run --output-format csv -- python3 bench.py --copy-probe --steps 3")
     out.append(f"python3 bench.py --pmc-md OUT.md --pmc-md-dir DIR --pmc-kernel {kernel} "
-               f"--pmc-cmd '{cmd}' --pmc-title '{args.pmc_title}'")
+               f"--pmc-cmd '{cmd}' --pmc-title '{args.pmc_title}'"
+               + (" --pmc-concurrent" if args.pmc_concurrent else ""))
     out += ["```", ""]
     text = "\n".join(out)
     with open(args.pmc_md, "w") as f:
@@ -1528,6 +1536,8 @@ def main():
     ap.add_argument("--sweep-workloads", default=None)
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--only-attention", action="store_true")
+    ap.add_argument("--pmc-concurrent", action="store_true",
+                    help="--pmc-md: the traced run has two streams' kernels side by side")
     ap.add_argument("--streams", action="store_true",
                     help="--only-attention: the two-stream iteration (tuning mix_order 5)")
     ap.add_argument("--fused", action="store_true",
